@@ -1,0 +1,124 @@
+/*
+ * mezo_oracle.h — CPU oracle for the seeded perturbation engine.
+ *
+ * TEST INFRASTRUCTURE ONLY. This is a plain, slow, obviously-correct C99
+ * statement of what the engine computes. Only the tests, the smoke check and
+ * the benchmark's CPU-baseline leg may load or call it; the product path
+ * (the HIP library and its Python binding) never does. It shares no code,
+ * header, table or constant with the HIP path.
+ *
+ * What it follows (paper: "Just One Byte (per gradient)", arXiv 2306.10015):
+ *  - PerturbParameters (Appendix A, Algorithm 1, the PerturbParameters
+ *    subroutine): reset an RNG with seed s, draw z ~ N(0,1) per parameter and
+ *    add eps*z to it.
+ *  - the perturb / evaluate triple +eps, -2eps, +eps (Algorithm 1, inner
+ *    inference loop);
+ *  - the apply loop (Algorithm 1, after GetGradients; Section 2 "Applying
+ *    collected scalar projected gradients"): in machine-timestamp order,
+ *    perturb with weight -grad * eta / numel(all_grads) and the same seed;
+ *  - the one-byte gradient (Section 3, "Training Speed": signed log clipped to
+ *    +-127);
+ *  - late-joiner catch-up (Appendix B): apply every logged projected gradient
+ *    of the missed iterations.
+ *
+ * Readings where the paper is silent (each restated in the design notes):
+ *  - the RNG is Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), keyed by
+ *    the machine id, with counter (element>>2, tensor_id, sample, step);
+ *  - a Gaussian is Box-Muller on exact 24-bit uniforms, evaluated in fp64 and
+ *    rounded once to fp32 (the fp32 sample z_ref);
+ *  - perturb/update add in fp64 and round once, straight to the storage type,
+ *    round-to-nearest-even; no flush of subnormals anywhere.
+ *
+ * Parity status: every function here is pinned by the CPU tests (published
+ * Philox engine cross-check, closed-form transform cases, statistics,
+ * exhaustive codec round trips, brute-force rounding, and the invariants of
+ * the update); none is "parity unpinned".
+ */
+#ifndef MEZO_ORACLE_H
+#define MEZO_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A seed s = (machine start time / id, iteration, sample index), Section 2 and
+ * Algorithm 1. Layout: 16 bytes, machine first. */
+typedef struct {
+    uint64_t machine;
+    uint32_t step;
+    uint32_t sample;
+} orc_seed_t;
+
+enum { ORC_F32 = 0, ORC_BF16 = 1 };
+enum { ORC_CODEC_LINEAR = 0, ORC_CODEC_SIGNED_LOG = 1 };
+
+/* Return codes: 0 ok, -1 bad argument, -2 value out of range. */
+
+/* Philox4x32-10 block function: 128-bit counter, 64-bit key -> 4 words. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* The four RNG words of the block that holds element e of tensor tensor_id. */
+void orc_block_words(orc_seed_t s, uint32_t tensor_id, uint64_t e, uint32_t out[4]);
+
+/* Box-Muller on one block of four words, fp64: z[0..3] (not rounded). */
+void orc_box_muller(const uint32_t w[4], double z[4]);
+
+/* The fp32 Gaussian of element e: fl32 of the fp64 Box-Muller value. */
+float orc_z(orc_seed_t s, uint32_t tensor_id, uint64_t e);
+
+/* z_ref and the element's own RNG word for count elements from first. Either
+ * output may be NULL. */
+int orc_generate(orc_seed_t s, uint32_t tensor_id, uint64_t first, uint64_t count,
+                 uint32_t* words, float* z);
+
+/* Direct round-to-nearest-even of an fp64 value to fp32 / bf16 bits. */
+float    orc_round_f32(double x);
+uint16_t orc_round_bf16(double x);
+
+/* One-byte codec. LINEAR: q = clamp(rne(g/scale)), g~ = fl32(q*scale).
+ * SIGNED_LOG: q = sign(g)*min(127, rne(alpha*ln(1+|g|))),
+ *             g~ = fl32(sign(q)*(exp(|q|/alpha)-1)); alpha = 1/ln 2 is a
+ *             base-2 log. NaN g, q = -128, non-positive or non-finite scale,
+ *             and an alpha for which code 127 decodes past fp32 (alpha <
+ *             ~1.4314) are rejected with -2. */
+int orc_quantize(const float* g, int8_t* q, uint32_t n, int kind, float scale, float alpha);
+int orc_dequantize(const int8_t* q, float* g, uint32_t n, int kind, float scale, float alpha);
+
+/* c_k = fl32(-lr * g~_k): the weight of perturbation k in the apply loop. */
+int orc_coefficients(const int8_t* q, uint32_t K, int kind, float scale, float alpha,
+                     float lr, float* c);
+
+/*
+ * The element-wise operations act on n elements of one tensor. Element i of the
+ * buffer `theta` (dtype ORC_F32: float, ORC_BF16: uint16 bits) is tensor
+ * element idx[i], or first+i when idx is NULL. Elements must be < 2^34.
+ */
+
+/* theta_i <- round_st(theta_i + scale * z_ref_i(s)). scale = 0 is a no-op. */
+int orc_perturb(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                uint64_t first, uint64_t n, orc_seed_t s, float scale);
+
+/* theta_i <- round_st(theta_i + sum_k c_k * z_ref_i(s_k)), sum in fp64 over
+ * ascending k, terms with c_k = 0 left out; c_k from orc_coefficients. */
+int orc_update(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+               uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+               uint32_t K, int kind, float scale, float alpha, float lr);
+
+/* T logged steps, each an orc_update with its own seeds, q (K_t of each, packed
+ * one step after another) and lr_t; storage rounding after every step. */
+int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+               uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+               const uint32_t* K_t, const float* lr_t, uint32_t T,
+               int kind, float scale, float alpha);
+
+/* Thread control for the OpenMP loops (1 when built without OpenMP). */
+void orc_set_threads(int n);
+int  orc_get_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEZO_ORACLE_H */
