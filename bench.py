@@ -1,0 +1,358 @@
+"""Throughput of the seeded perturbation engine on one MI355X.
+
+One step is one pass of the whole hot path over a synthetic OPT-125m-shaped
+fp32 parameter set (123,581,952 elements in 123 tensors, N(0, 0.02)):
+
+  1. PerturbParameters +eps, -2eps, +eps with this machine's seed
+     (Algorithm 1, inner inference loop; eps = 1e-3);
+  2. quantize_projgrad of the K = 8 projected gradients of the iteration
+     (Section 3, one byte each; linear code, scale 1/127);
+  3. update_multi: the fused apply loop over the K = 8 (machine, sample)
+     seeds (Algorithm 1; lr = 1e-6);
+  4. replay: a late joiner's catch-up over a log of T = 4 earlier iterations
+     of K = 8 seeds each (Appendix B).
+
+Every parameter is read and written once per call; z is regenerated in
+registers. The metric is param-seed updates per second: elements x seeds
+applied, summed over the step's calls, divided by the time of the step.
+
+Prints ONE JSON line. Also reports, for the engine kernel (the only kernel of
+the step), the ALU roofline fraction (see the design doc for the peak), and the
+CPU oracle timed on a bounded sample of the same step.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+#: VALU issue capacity of one MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+#: = 39.3e12 lane-instructions per second (a wave64 VALU instruction occupies a
+#: 16-lane SIMD for 4 cycles when issued singly). It is the published
+#: 157.3 TFLOP/s fp32 vector peak / (2 flops per fma x 2 lanes per packed op).
+#: gfx950 can dual-issue some VALU instructions, so a kernel can exceed it.
+CLOCK_GHZ = 2.4
+VALU_LANE_INSTR_PER_S = 256 * 4 * 16 * CLOCK_GHZ * 1e9
+HBM_PEAK_GBS = 8000.0
+
+#: VALU instructions per Philox block (4 Gaussians) per seed in the engine's
+#: inner loop, the method's minimal sequence on gfx950: round 1 and the
+#: element-independent half of round 2 hoisted out of the seed loop; rounds
+#: 2..10 cost 17 wide multiplies (v_mad_u64_u32), 16 three-way xors
+#: (v_bitop3_b32) and 3 xors; Box-Muller per pair of Gaussians: 2 shifts, 2
+#: int->float conversions, one fma forming u1, 4 muls, log2, sqrt, sin, cos;
+#: and one fma per Gaussian accumulating c_k * z.
+INNER_LOOP_MIX = {
+    "v_mad_u64_u32": 17, "v_bitop3_b32": 16, "v_xor_b32": 3, "v_lshrrev_b32": 4,
+    "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 8, "v_log_f32": 2, "v_sqrt_f32": 2,
+    "v_sin_f32": 2, "v_cos_f32": 2, "v_fmac_f32": 4,
+}
+#: lane-instructions per param-seed (= 66 / 4)
+INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
+
+#: counter profile of the engine kernel on this workload (FETCH_SIZE /
+#: WRITE_SIZE per dispatch, calibrated against a plain copy); its traffic is
+#: reported only while the kernel sources it was taken on are unchanged.
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_opt125m_f32_traffic.json")
+KERNEL_SOURCES = ["paper_2306_10015_amd/csrc/kernels.hip", "paper_2306_10015_amd/csrc/engine.hpp",
+                  "paper_2306_10015_amd/csrc/records.hpp"]
+
+T_REPLAY = 4
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="opt125m")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--probe", choices=["copy"], default=None,
+                   help="copy: time a plain device copy of the parameter buffer instead")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target CPU work of the oracle baseline sample")
+    return p.parse_args()
+
+
+def flat_views(torch, w, device):
+    """One 256-byte-aligned allocation holding every tensor of the set."""
+    import math
+    esz = 4 if w.dtype == "f32" else 2
+    align = 256 // esz
+    offs, total = [], 0
+    for _, shape in w.shapes:
+        n = int(math.prod(shape))
+        offs.append((total, n))
+        total += (n + align - 1) // align * align
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    flat = torch.empty(total, dtype=dt, device=device)
+    views = [flat[a:a + n] for a, n in offs]
+    return flat, views, offs
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2306_10015_amd import mezo, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.WORKLOADS[args.workload]
+    K = w.K
+    N = w.numel
+
+    # ---- inputs resident in HBM before timing -------------------------------
+    flat, views, offs = flat_views(torch, w, dev)
+    for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
+        h = synth.theta0_tensor(shape, w.dtype, i, 0)
+        if w.dtype == "f32":
+            v.copy_(torch.from_numpy(h))
+        else:
+            v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+    if args.probe == "copy":
+        copy_probe(torch, flat, args)
+        return
+    ps = mezo.ParamSet(views)
+    eps, lr = w.eps, w.lr
+
+    total_steps = args.warmup + args.steps
+    proj = [synth.projected_grads(K, seed=1000 + t) for t in range(total_steps)]
+    seeds_t = [synth.seeds(w.machines, w.samples_per_machine, step=t) for t in range(total_steps)]
+    log = [(synth.seeds(w.machines, w.samples_per_machine, step=10_000 + t),
+            synth.grads_int8(K, "uniform", seed=2000 + t), lr) for t in range(T_REPLAY)]
+    recs = {"perturb": 1, "update": K, "replay": T_REPLAY * K}
+    calls = ["perturb", "perturb", "perturb", "update", "replay"]
+    ps_per_step = N * sum(recs[c] for c in calls)
+
+    stream = torch.cuda.current_stream()
+
+    def step(t, ev=None):
+        s = (0, t, 0)
+        marks = []
+
+        def mark():
+            if ev is not None:
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                marks.append(e)
+
+        mark()
+        ps.perturb(s, eps)
+        mark()
+        ps.perturb(s, -2 * eps)
+        mark()
+        ps.perturb(s, eps)
+        mark()
+        q = mezo.quantize_projgrad(proj[t])
+        ps.update_multi(seeds_t[t], q, lr)
+        mark()
+        ps.replay(log)
+        mark()
+        if ev is not None:
+            ev.append(marks)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly `steps` steps ---------------------------------
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for t in range(args.warmup, total_steps):
+        step(t)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(end)
+    ms_per_step = ms_total / args.steps
+
+    # ---- per-launch durations (same stream, event pairs around each call) ----
+    marks_all = []
+    torch.cuda.synchronize()
+    for t in range(args.warmup, total_steps):
+        step(t, marks_all)
+    torch.cuda.synchronize()
+    per_call = {c: [] for c in recs}
+    for marks in marks_all:
+        for c, a, b in zip(calls, marks[:-1], marks[1:]):
+            per_call[c].append(a.elapsed_time(b))
+    launch_ms = {c: float(np.mean(v)) for c, v in per_call.items()}
+
+    value = ps_per_step * args.steps / (ms_total / 1e3)
+    bytes_per_launch = 2 * N * (4 if w.dtype == "f32" else 2)
+
+    # Engine kernel: every call of the step is one launch of it (per storage
+    # type; this set is all fp32). Achieved ALU work = param-seeds x minimal
+    # lane-instructions per param-seed over the launch time.
+    n_launch = len(calls)
+    kernel_ms = sum(launch_ms[c] for c in calls)
+    ps_per_launch = ps_per_step / n_launch
+    avg_launch_s = kernel_ms / n_launch / 1e3
+    achieved = ps_per_launch * INSTR_PER_PARAM_SEED / avg_launch_s / 1e12
+    peak = VALU_LANE_INSTR_PER_S / 1e12
+    costs = issue_costs()
+    ops = {}
+    for c in recs:
+        t_s = launch_ms[c] / 1e3
+        ops[c] = {"records": recs[c], "ms": round(launch_ms[c], 4),
+                  "param_seeds_per_s": N * recs[c] / t_s,
+                  "alg_GBps": bytes_per_launch / t_s / 1e9,
+                  "hbm_frac": bytes_per_launch / t_s / 1e9 / HBM_PEAK_GBS,
+                  "alu_frac": N * recs[c] * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S}
+
+    out = {
+        "metric": "param-seed updates/sec (params x K per s)",
+        "value": value,
+        "unit": "param-seeds/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {N} {w.dtype} params in {w.n_tensors} tensors, "
+                               f"K={K}; step = perturb +eps,-2eps,+eps; quantize {K} grads; "
+                               f"update_multi K={K}; replay T={T_REPLAY}xK={K}",
+                   "params": N, "tensors": w.n_tensors, "K": K, "replay_T": T_REPLAY,
+                   "eps": eps, "lr": lr, "param_seeds_per_step": ps_per_step},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": peak,
+                     "unit": "Tinstr/s", "frac": achieved / peak,
+                     "traffic": measured_traffic(bytes_per_launch),
+                     "alg_bytes_per_launch": bytes_per_launch,
+                     "kernel": "engine_kernel<inline records, f32>",
+                     "instr_per_param_seed": INSTR_PER_PARAM_SEED,
+                     "param_seeds_per_launch": ps_per_launch,
+                     "avg_launch_ms": kernel_ms / n_launch,
+                     "issue_cycles_isolated": {k: round(v, 3) for k, v in costs.items()}},
+        "wall_s_timed": wall,
+        "ops": ops,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, recs, calls, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+def issue_costs() -> dict:
+    """SIMD cycles per wave instruction of each instruction of the inner loop in
+    isolation, measured now on this device by libisa_probe.so (8 waves per
+    SIMD, 8 independent chains per lane): context for the instruction mix."""
+    import ctypes
+    from paper_2306_10015_amd import build as b
+    if not b.PROBE_LIB.exists():
+        raise RuntimeError(f"{b.PROBE_LIB} is not built")
+    L = ctypes.CDLL(str(b.PROBE_LIB))
+    L.isa_probe_count.restype = ctypes.c_int
+    L.isa_probe_name.restype = ctypes.c_char_p
+    L.isa_probe_name.argtypes = [ctypes.c_int]
+    L.isa_probe_run.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_double]
+    n = L.isa_probe_count()
+    out = (ctypes.c_double * n)()
+    rc = L.isa_probe_run(out, CLOCK_GHZ)
+    if rc != 0:
+        raise RuntimeError(f"isa_probe_run failed ({rc})")
+    return {L.isa_probe_name(i).decode(): float(out[i]) for i in range(n)}
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(n_launch_bytes: float):
+    """HBM bytes per engine launch from the committed counter profile, or None
+    when there is none or the kernel sources changed since it was taken."""
+    try:
+        with open(TRAFFIC_PROFILE) as f:
+            prof = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if prof.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return prof["hbm_bytes_per_dispatch"]
+
+
+def copy_probe(torch, flat, args):
+    """A plain device-to-device copy of the whole parameter buffer: what HBM
+    delivers to a streaming read+write of the same size (context for the
+    bandwidth figures, and the reference for the traffic counters)."""
+    dst = torch.empty_like(flat)
+    for _ in range(args.warmup):
+        dst.copy_(flat)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(args.steps):
+        dst.copy_(flat)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    nbytes = 2 * flat.numel() * flat.element_size()
+    print(json.dumps({"probe": "copy", "bytes_per_copy": nbytes, "ms": ms,
+                      "GBps": nbytes / (ms / 1e3) / 1e9,
+                      "hbm_frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
+
+
+def cpu_baseline(w, recs, calls, target_s):
+    """The oracle, as it stands, on a bounded element sample of the same step:
+    all tensors' first elements, sized to about `target_s` of CPU time."""
+    import oracle
+    from paper_2306_10015_amd import synth
+    n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    n_threads = min(n_threads, 16)
+    oracle.set_threads(n_threads)
+    K = w.K
+    seeds = synth.seeds(w.machines, w.samples_per_machine, step=0)
+    q = synth.grads_int8(K, "uniform", seed=1)
+    log = [(synth.seeds(w.machines, w.samples_per_machine, step=10_000 + t),
+            synth.grads_int8(K, "uniform", seed=2000 + t), w.lr) for t in range(T_REPLAY)]
+    seeds_per_elem = sum(recs[c] for c in calls)
+
+    def run(n):
+        th = synth.theta0_tensor((n,), w.dtype, 0, 0)
+        t0 = time.perf_counter()
+        oracle.perturb(th, 0, (0, 0, 0), w.eps)
+        oracle.perturb(th, 0, (0, 0, 0), -2 * w.eps)
+        oracle.perturb(th, 0, (0, 0, 0), w.eps)
+        oracle.update(th, 0, seeds, q, w.lr)
+        oracle.replay(th, 0, log)
+        return time.perf_counter() - t0
+
+    n = 1 << 14
+    dt = run(n)
+    n_full = int(min(max(n * target_s / max(dt, 1e-6), n), w.numel))
+    dt = run(n_full)
+    return {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,
+            "kind": "oracle",
+            "sample": f"first {n_full} elements of tensor 0 through the same step "
+                      f"({seeds_per_elem} param-seeds per element), {dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,216 @@
+/*
+ * mezo.h — C ABI of libmezo, the MI355X (gfx950) seeded perturbation engine
+ * for shared-randomness SPSA fine-tuning ("Just One Byte (per gradient)",
+ * arXiv 2306.10015).
+ *
+ * The engine regenerates every Gaussian perturbation z from a seed instead of
+ * storing it, and applies it to a model's parameters in place:
+ *   - mezo_perturb       theta += scale * z(seed)          (Algorithm 1,
+ *                        PerturbParameters; called with +eps, -2eps, +eps
+ *                        around the two forward passes)
+ *   - mezo_update_multi  theta -= lr * sum_k g~_k z(seed_k) (Algorithm 1, the
+ *                        apply loop over (timestamp, sample_id) in order)
+ *   - mezo_replay        T logged updates one after another (Appendix B,
+ *                        late-joiner catch-up)
+ *   - quantize_projgrad  projected gradient -> one byte (Section 3)
+ *
+ * Plain C99: no HIP or torch types. Device pointers are plain pointers into
+ * memory of the current HIP device; a stream is a hipStream_t passed as void*
+ * (NULL = the null stream).
+ *
+ * What z is. For seed s = (machine, step, sample), tensor id t and element e
+ * of that tensor, the four 32-bit words w0..w3 of
+ *     Philox4x32-10(key = (lo32(machine), hi32(machine)),
+ *                   counter = (e >> 2, t, sample, step))
+ * are turned into four Gaussians by Box-Muller on 24-bit uniforms
+ *     u1 = ((w_a >> 8) + 1) * 2^-24,  u2 = (w_b >> 8) * 2^-24,
+ *     z = sqrt(-2 ln u1) * (cos 2 pi u2, sin 2 pi u2)
+ * with (w0, w1) giving elements 4b, 4b+1 and (w2, w3) giving 4b+2, 4b+3.
+ * z therefore depends only on (seed, t, e): not on the launch, the grouping
+ * of tensors or the storage type. RNG words are bit-exact with any other
+ * implementation of this definition; the Gaussians are computed in fp32 with
+ * the GPU's transcendental instructions (absolute error below 1e-6 * max|z|).
+ *
+ * Arithmetic. theta is loaded into fp32 (bf16 exactly), the perturbations are
+ * accumulated in fp32 as acc = fma(c_k, z_k, acc) for k ascending, and
+ * theta' = round(theta + acc) to the storage type, round-to-nearest-even;
+ * subnormals are kept.
+ *
+ * Errors. Every int-returning call returns MEZO_OK (0) or a negative MEZO_E*
+ * code. All argument checks run before anything is enqueued, so a failed call
+ * leaves the parameters untouched. Device faults surface at the caller's next
+ * synchronisation (HIP's convention). mezo_strerror() gives a description;
+ * for MEZO_EHIP, mezo_last_error() gives the HIP runtime's message of the last
+ * failure on the calling thread.
+ *
+ * Ownership. Parameter memory belongs to the caller (e.g. PyTorch): the
+ * library never allocates or frees it. The library owns a paramset's device
+ * tensor table and its seed-staging buffers, released by
+ * mezo_paramset_destroy. Host arrays passed to any call are read before the
+ * call returns and may be reused at once.
+ *
+ * Threads and streams. Calls on one paramset may come from several host
+ * threads (they serialise on a per-paramset lock). Work is ordered only by the
+ * stream it is enqueued on: two calls on different streams that touch the
+ * same parameters race unless the caller orders the streams.
+ */
+#ifndef MEZO_H
+#define MEZO_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define MEZO_API __attribute__((visibility("default")))
+#else
+#define MEZO_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ---------------------------------------------------- */
+#define MEZO_OK        0
+#define MEZO_EINVAL   -1  /* null/misaligned pointer, empty or oversized tensor,
+                             duplicated tensor_id, bad count                  */
+#define MEZO_EDTYPE   -2  /* unknown storage type                            */
+#define MEZO_EOVERLAP -3  /* two tensors of a paramset share memory          */
+#define MEZO_EORDER   -4  /* seeds of one update not strictly ascending      */
+#define MEZO_ERANGE   -5  /* q = -128, NaN gradient, non-finite lr/scale,
+                             codec parameters out of range                   */
+#define MEZO_EHIP     -6  /* HIP runtime failure (see mezo_last_error)       */
+
+/* ---- storage types and codecs ---------------------------------------- */
+#define MEZO_F32  0u      /* IEEE binary32                                    */
+#define MEZO_BF16 1u      /* bfloat16: top 16 bits of a binary32              */
+
+#define MEZO_CODEC_LINEAR     0u  /* q = clamp(rne(g / scale), -127, 127);
+                                     g~ = fl32(q * scale)                     */
+#define MEZO_CODEC_SIGNED_LOG 1u  /* q = sign(g) min(127, rne(alpha ln(1+|g|)));
+                                     g~ = fl32(sign(q) (exp(|q|/alpha) - 1)).
+                                     alpha = 1/ln 2 (a base-2 log) puts code
+                                     127 just inside fp32; an alpha for which
+                                     code 127 would decode past fp32 (alpha <
+                                     ~1.4314) is MEZO_ERANGE.                 */
+
+/* Largest number of elements of one tensor (the counter holds e >> 2 in 32
+ * bits). */
+#define MEZO_MAX_NUMEL (1ull << 34)
+
+/* A seed (Section 2: built from the machine's identifier/start time, the
+ * iteration and the sample index; Algorithm 1 writes it (self_time, t,
+ * sample)). A floating-point timestamp is passed as its bit pattern. */
+typedef struct {
+    uint64_t machine;
+    uint32_t step;    /* the iteration t / cur_iter */
+    uint32_t sample;  /* index of the projected gradient within its machine's step */
+} mezo_seed_t;
+
+/* One parameter tensor: `numel` contiguous elements at device address
+ * `data` (16-byte aligned), storage `dtype`. `tensor_id` selects the tensor's
+ * noise stream and must be unique within a paramset; keep it stable across
+ * machines (e.g. the registration order of the model's parameters). */
+typedef struct {
+    void*    data;
+    uint64_t numel;
+    uint32_t tensor_id;
+    uint32_t dtype;
+} mezo_tensor_t;
+
+/* One-byte gradient code (Section 3). `scale` is used by LINEAR, `alpha` by
+ * SIGNED_LOG. */
+typedef struct {
+    uint32_t kind;
+    float    scale;
+    float    alpha;
+} mezo_codec_t;
+
+/* One logged step of the apply loop (Appendix B): K seeds in ascending
+ * (machine, step, sample) order, their one-byte gradients, and the step's
+ * per-gradient learning rate (eta_t / numel(all_grads), Algorithm 1). */
+typedef struct {
+    const mezo_seed_t* seeds;
+    const int8_t*      q;
+    uint32_t           K;
+    float              lr;
+} mezo_step_t;
+
+typedef struct mezo_paramset* mezo_paramset_t;
+
+/* ---- parameter sets --------------------------------------------------- */
+
+/* Register n tensors (copied; the array may be reused). Checks: t and out
+ * non-null, n >= 1, every data non-null and 16-byte aligned, 1 <= numel <=
+ * MEZO_MAX_NUMEL (else MEZO_EINVAL), dtype known (MEZO_EDTYPE), tensor_ids
+ * unique (MEZO_EINVAL), no two tensors overlapping in memory (MEZO_EOVERLAP).
+ * Device resources are created on the current HIP device at the first launch;
+ * every later call must be made with that same device current (MEZO_EINVAL
+ * otherwise). */
+MEZO_API int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* out);
+
+/* Release the paramset's table and staging buffers after waiting for the
+ * work it enqueued. NULL is ignored. */
+MEZO_API void mezo_paramset_destroy(mezo_paramset_t ps);
+
+/* Total number of elements of a paramset (0 for NULL). */
+MEZO_API uint64_t mezo_paramset_numel(mezo_paramset_t ps);
+
+/* ---- the engine ------------------------------------------------------- */
+
+/* PerturbParameters(theta, scale, seed) — Algorithm 1: for every element of
+ * every tensor, theta <- round(theta + scale * z(seed)). One pass; one read
+ * and one write of each element. scale must be finite (MEZO_ERANGE);
+ * scale = 0 enqueues nothing. */
+MEZO_API int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream);
+
+/* The apply loop of one iteration — Algorithm 1 and Section 2: in
+ * machine-timestamp order, perturb by -grad_k * lr with seed_k. Fused: for
+ * every element, acc = sum_k c_k z(seed_k) with c_k = fl32(-lr * g~_k)
+ * (g~_k = the codec's decoding of q[k]), then theta <- round(theta + acc);
+ * each element is read and written once for all K seeds.
+ * seeds must be strictly ascending by (machine, step, sample) (MEZO_EORDER);
+ * the fixed order fixes the fp32 sum, so replicas stay bit-identical.
+ * q[k] = -128, non-finite lr or a bad codec give MEZO_ERANGE. Terms with
+ * c_k = 0 are dropped; K = 0, lr = 0 or all-zero q enqueue nothing. */
+MEZO_API int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t* q,
+                      uint32_t K, const mezo_codec_t* codec, float lr, void* stream);
+
+/* Late-joiner catch-up — Appendix B: apply T logged steps in order, each as
+ * mezo_update_multi would (rounding to storage after every step), in one pass
+ * over the parameters. Each step is checked as in mezo_update_multi; T = 0
+ * enqueues nothing. The result is bit-identical to T mezo_update_multi calls. */
+MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T,
+                const mezo_codec_t* codec, void* stream);
+
+/* ---- the one-byte gradient (host, pure) ------------------------------- */
+
+/* Projected gradient g = (l+ - l-) / (2 eps) -> q (Section 3). ±inf clip to
+ * ±127; NaN is MEZO_ERANGE. Rounding ties go to even. n may be 0. */
+MEZO_API int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t* codec);
+
+/* q -> g~ (the value every machine applies). q = -128 is MEZO_ERANGE. */
+MEZO_API int mezo_dequantize(const int8_t* q, float* g, uint32_t n, const mezo_codec_t* codec);
+
+/* ---- inspection -------------------------------------------------------- */
+
+/* Write the RNG word (words_dev[i] = word e & 3 of the block of element e)
+ * and/or the Gaussian z_dev[i] of elements e = first_elem + i, i < count, of
+ * tensor tensor_id under seed. Either device pointer may be NULL;
+ * first_elem + count <= MEZO_MAX_NUMEL (MEZO_EINVAL). */
+MEZO_API int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t first_elem,
+                        uint64_t count, uint32_t* words_dev, float* z_dev, void* stream);
+
+MEZO_API const char* mezo_strerror(int code);
+
+/* The HIP runtime's message of the last MEZO_EHIP failure on this thread
+ * ("" if none). */
+MEZO_API const char* mezo_last_error(void);
+
+/* Library version, major*10000 + minor*100 + patch. */
+MEZO_API int mezo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MEZO_H */

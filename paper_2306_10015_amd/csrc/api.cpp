@@ -1,0 +1,415 @@
+// api.cpp — the C ABI of libmezo (include/mezo.h): argument checks, the
+// paramset tensor table, the one-byte codec, seed records, staging and
+// launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/mezo.h"
+#include "launch.hpp"
+#include "records.hpp"
+
+namespace {
+
+thread_local std::string t_last_error;
+
+int hip_fail(hipError_t e, const char* where)
+{
+    t_last_error = std::string(where) + ": " + hipGetErrorString(e);
+    return MEZO_EHIP;
+}
+
+#define MEZO_HIP(call)                                  \
+    do {                                                \
+        hipError_t err_ = (call);                       \
+        if (err_ != hipSuccess) return hip_fail(err_, #call); \
+    } while (0)
+
+// ---- codec (Section 3: the projected gradient in one byte) -------------------
+
+bool codec_valid(const mezo_codec_t* c)
+{
+    if (!c) return false;
+    if (c->kind == MEZO_CODEC_LINEAR) return std::isfinite(c->scale) && c->scale > 0.0f;
+    if (c->kind == MEZO_CODEC_SIGNED_LOG) {
+        if (!(std::isfinite(c->alpha) && c->alpha > 0.0f)) return false;
+        // the largest code must decode to a finite fp32 value
+        return std::isfinite(static_cast<float>(std::expm1(127.0 / double(c->alpha))));
+    }
+    return false;
+}
+
+int8_t encode(float g, const mezo_codec_t& c)
+{
+    double r;
+    if (c.kind == MEZO_CODEC_LINEAR) {
+        r = double(std::rint(g / c.scale));  // fp32 quotient, ties to even
+    } else {
+        const double mag = std::rint(double(c.alpha) * std::log1p(std::fabs(double(g))));
+        r = std::signbit(g) ? -mag : mag;
+    }
+    r = std::min(127.0, std::max(-127.0, r));
+    return static_cast<int8_t>(r);
+}
+
+float decode(int8_t q, const mezo_codec_t& c)
+{
+    if (c.kind == MEZO_CODEC_LINEAR) return static_cast<float>(double(q) * double(c.scale));
+    const double mag = std::expm1(std::fabs(double(q)) / double(c.alpha));
+    return static_cast<float>(q < 0 ? -mag : mag);
+}
+
+// ---- seeds -----------------------------------------------------------------
+
+bool seed_less(const mezo_seed_t& a, const mezo_seed_t& b)
+{
+    if (a.machine != b.machine) return a.machine < b.machine;
+    if (a.step != b.step) return a.step < b.step;
+    return a.sample < b.sample;
+}
+
+mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last)
+{
+    mezo::SeedRec r;
+    r.key0 = static_cast<uint32_t>(s.machine);
+    r.key1 = static_cast<uint32_t>(s.machine >> 32);
+    r.step = s.step;
+    const uint64_t p = uint64_t(mezo::kMulB) * uint64_t(s.sample);
+    r.mb_hi = static_cast<uint32_t>(p >> 32);
+    r.mb_lo = static_cast<uint32_t>(p);
+    r.coef = coef;
+    r.last = last ? 1u : 0u;
+    r.sample = s.sample;
+    return r;
+}
+
+// Checks one step of the apply loop and appends its records (zero weights
+// dropped; the step's last kept record is flagged to round to storage).
+int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t* codec,
+                float lr, std::vector<mezo::SeedRec>& out)
+{
+    if (!codec) return MEZO_EINVAL;
+    if (!codec_valid(codec) || !std::isfinite(lr)) return MEZO_ERANGE;
+    if (K == 0) return MEZO_OK;
+    if (!seeds || !q) return MEZO_EINVAL;
+    for (uint32_t k = 0; k < K; ++k)
+        if (q[k] == -128) return MEZO_ERANGE;
+    for (uint32_t k = 1; k < K; ++k)
+        if (!seed_less(seeds[k - 1], seeds[k])) return MEZO_EORDER;
+    const size_t first = out.size();
+    for (uint32_t k = 0; k < K; ++k) {
+        // weight of perturbation k in the apply loop: -grad * lr (Algorithm 1)
+        const float c = static_cast<float>(-double(lr) * double(decode(q[k], *codec)));
+        if (c != 0.0f) out.push_back(make_rec(seeds[k], c, false));
+    }
+    if (out.size() > first) out.back().last = 1u;
+    return MEZO_OK;
+}
+
+}  // namespace
+
+// ---- paramset -----------------------------------------------------------------
+
+struct mezo_paramset {
+    std::mutex mu;
+    // One table per storage type (index = dtype), each in registration order
+    // with tile_begin ascending; the engine runs one launch per non-empty table.
+    std::vector<mezo::TensorDesc> table[2];
+    uint64_t total_tiles[2] = {0, 0};
+    uint64_t numel = 0;
+    int device = -1;
+    mezo::TensorDesc* d_table[2] = {nullptr, nullptr};
+    uint32_t* d_tile_tensor[2] = {nullptr, nullptr};  // tensor index of every tile
+    hipEvent_t last = nullptr;  // after the latest launch that reads a table
+
+    // Staging of record lists too long for the kernel arguments: a ring of
+    // slots, each reused only after the launch that read it has completed.
+    struct Slot {
+        mezo::SeedRec* host = nullptr;  // pinned
+        mezo::SeedRec* dev = nullptr;
+        size_t cap = 0;
+        hipEvent_t done = nullptr;
+    };
+    static constexpr int kSlots = 4;
+    Slot slots[kSlots];
+    unsigned next_slot = 0;
+};
+
+namespace {
+
+// Device resources are made on first use, on the device current then.
+int ensure_device(mezo_paramset* ps)
+{
+    int dev = -1;
+    MEZO_HIP(hipGetDevice(&dev));
+    if (ps->device >= 0) {
+        if (dev != ps->device) {
+            t_last_error = "paramset used on a device other than the one it was first used on";
+            return MEZO_EINVAL;
+        }
+        return MEZO_OK;
+    }
+    hipError_t e = hipSuccess;
+    for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
+        const std::vector<mezo::TensorDesc>& tab = ps->table[dt];
+        if (tab.empty()) continue;
+        const size_t bytes = tab.size() * sizeof(mezo::TensorDesc);
+        e = hipMalloc(reinterpret_cast<void**>(&ps->d_table[dt]), bytes);
+        if (e == hipSuccess) e = hipMemcpy(ps->d_table[dt], tab.data(), bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) break;
+        std::vector<uint32_t> owner(ps->total_tiles[dt]);
+        for (size_t i = 0; i < tab.size(); ++i) {
+            const uint64_t end = i + 1 < tab.size() ? tab[i + 1].tile_begin : ps->total_tiles[dt];
+            for (uint64_t tl = tab[i].tile_begin; tl < end; ++tl) owner[tl] = static_cast<uint32_t>(i);
+        }
+        e = hipMalloc(reinterpret_cast<void**>(&ps->d_tile_tensor[dt]), owner.size() * sizeof(uint32_t));
+        if (e == hipSuccess)
+            e = hipMemcpy(ps->d_tile_tensor[dt], owner.data(), owner.size() * sizeof(uint32_t),
+                          hipMemcpyHostToDevice);
+    }
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ps->last, hipEventDisableTiming);
+    if (e != hipSuccess) {
+        for (int dt = 0; dt < 2; ++dt) {
+            if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
+            if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
+            ps->d_table[dt] = nullptr;
+            ps->d_tile_tensor[dt] = nullptr;
+        }
+        return hip_fail(e, "paramset device table");
+    }
+    ps->device = dev;
+    return MEZO_OK;
+}
+
+int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hipStream_t stream)
+{
+    if (recs.empty()) return MEZO_OK;
+    int rc = ensure_device(ps);
+    if (rc) return rc;
+    mezo::EngineArgs args;
+    std::memset(&args, 0, sizeof(args));
+    args.n_rec = static_cast<uint32_t>(recs.size());
+    mezo_paramset::Slot* slot = nullptr;
+    if (recs.size() <= mezo::kInlineRecs) {
+        std::copy(recs.begin(), recs.end(), args.inl);
+    } else {
+        slot = &ps->slots[ps->next_slot++ % mezo_paramset::kSlots];
+        if (slot->done)
+            MEZO_HIP(hipEventSynchronize(slot->done));
+        else
+            MEZO_HIP(hipEventCreateWithFlags(&slot->done, hipEventDisableTiming));
+        if (slot->cap < recs.size()) {
+            size_t cap = std::max<size_t>(recs.size(), 2 * slot->cap);
+            if (slot->host) MEZO_HIP(hipHostFree(slot->host));
+            if (slot->dev) MEZO_HIP(hipFree(slot->dev));
+            slot->host = nullptr;
+            slot->dev = nullptr;
+            slot->cap = 0;
+            MEZO_HIP(hipHostMalloc(reinterpret_cast<void**>(&slot->host), cap * sizeof(mezo::SeedRec)));
+            MEZO_HIP(hipMalloc(reinterpret_cast<void**>(&slot->dev), cap * sizeof(mezo::SeedRec)));
+            slot->cap = cap;
+        }
+        std::memcpy(slot->host, recs.data(), recs.size() * sizeof(mezo::SeedRec));
+        MEZO_HIP(hipMemcpyAsync(slot->dev, slot->host, recs.size() * sizeof(mezo::SeedRec),
+                                hipMemcpyHostToDevice, stream));
+        args.ext = slot->dev;
+    }
+    for (uint32_t dt = 0; dt < 2; ++dt) {
+        if (ps->table[dt].empty()) continue;
+        args.tensors = ps->d_table[dt];
+        args.tile_tensor = ps->d_tile_tensor[dt];
+        args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
+        args.total_tiles = ps->total_tiles[dt];
+        MEZO_HIP(mezo::launch_engine(args, dt, stream));
+    }
+    if (slot) MEZO_HIP(hipEventRecord(slot->done, stream));
+    MEZO_HIP(hipEventRecord(ps->last, stream));
+    return MEZO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* out)
+{
+    if (!t || !out || n == 0) return MEZO_EINVAL;
+    std::vector<std::pair<uintptr_t, uintptr_t>> spans;
+    std::vector<uint32_t> ids;
+    spans.reserve(n);
+    ids.reserve(n);
+    for (uint32_t i = 0; i < n; ++i) {
+        if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16) return MEZO_EDTYPE;
+        if (!t[i].data || (reinterpret_cast<uintptr_t>(t[i].data) & 15u)) return MEZO_EINVAL;
+        if (t[i].numel == 0 || t[i].numel > MEZO_MAX_NUMEL) return MEZO_EINVAL;
+        const uintptr_t b = reinterpret_cast<uintptr_t>(t[i].data);
+        const uint64_t esz = t[i].dtype == MEZO_F32 ? 4 : 2;
+        spans.emplace_back(b, b + t[i].numel * esz);
+        ids.push_back(t[i].tensor_id);
+    }
+    std::sort(ids.begin(), ids.end());
+    if (std::adjacent_find(ids.begin(), ids.end()) != ids.end()) return MEZO_EINVAL;
+    std::sort(spans.begin(), spans.end());
+    for (size_t i = 1; i < spans.size(); ++i)
+        if (spans[i].first < spans[i - 1].second) return MEZO_EOVERLAP;
+
+    mezo_paramset* ps = new (std::nothrow) mezo_paramset;
+    if (!ps) return MEZO_EINVAL;
+    uint64_t numel = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        const uint32_t dt = t[i].dtype;
+        mezo::TensorDesc d;
+        d.data = reinterpret_cast<uint64_t>(t[i].data);
+        d.numel = t[i].numel;
+        d.tensor_id = t[i].tensor_id;
+        d.dtype = dt;
+        d.tile_begin = ps->total_tiles[dt];
+        const uint64_t per = dt == MEZO_F32 ? mezo::kTileF32 : mezo::kTileBF16;
+        ps->total_tiles[dt] += (t[i].numel + per - 1) / per;
+        ps->table[dt].push_back(d);
+        numel += t[i].numel;
+    }
+    ps->numel = numel;
+    if (ps->total_tiles[0] > 0x7FFFFFFFull || ps->total_tiles[1] > 0x7FFFFFFFull) {
+        delete ps;  // more tiles than one launch can address
+        return MEZO_EINVAL;
+    }
+    *out = ps;
+    return MEZO_OK;
+}
+
+void mezo_paramset_destroy(mezo_paramset_t ps)
+{
+    if (!ps) return;
+    {
+        std::lock_guard<std::mutex> lock(ps->mu);
+        if (ps->last) {
+            (void)hipEventSynchronize(ps->last);
+            (void)hipEventDestroy(ps->last);
+        }
+        for (auto& s : ps->slots) {
+            if (s.done) {
+                (void)hipEventSynchronize(s.done);
+                (void)hipEventDestroy(s.done);
+            }
+            if (s.host) (void)hipHostFree(s.host);
+            if (s.dev) (void)hipFree(s.dev);
+        }
+        for (int dt = 0; dt < 2; ++dt) {
+            if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
+            if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
+        }
+    }
+    delete ps;
+}
+
+uint64_t mezo_paramset_numel(mezo_paramset_t ps) { return ps ? ps->numel : 0; }
+
+int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream)
+{
+    if (!ps) return MEZO_EINVAL;
+    if (!std::isfinite(scale)) return MEZO_ERANGE;
+    if (scale == 0.0f) return MEZO_OK;
+    std::vector<mezo::SeedRec> recs(1, make_rec(seed, scale, true));
+    std::lock_guard<std::mutex> lock(ps->mu);
+    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+}
+
+int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t* q, uint32_t K,
+                      const mezo_codec_t* codec, float lr, void* stream)
+{
+    if (!ps) return MEZO_EINVAL;
+    std::vector<mezo::SeedRec> recs;
+    recs.reserve(K);
+    int rc = append_step(seeds, q, K, codec, lr, recs);
+    if (rc) return rc;
+    std::lock_guard<std::mutex> lock(ps->mu);
+    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+}
+
+int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const mezo_codec_t* codec,
+                void* stream)
+{
+    if (!ps || !codec) return MEZO_EINVAL;
+    if (!codec_valid(codec)) return MEZO_ERANGE;
+    if (T == 0) return MEZO_OK;
+    if (!steps) return MEZO_EINVAL;
+    std::vector<mezo::SeedRec> recs;
+    size_t total = 0;
+    for (uint32_t t = 0; t < T; ++t) total += steps[t].K;
+    recs.reserve(total);
+    for (uint32_t t = 0; t < T; ++t) {
+        int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, recs);
+        if (rc) return rc;
+    }
+    std::lock_guard<std::mutex> lock(ps->mu);
+    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+}
+
+int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t* codec)
+{
+    if (!codec) return MEZO_EINVAL;
+    if (!codec_valid(codec)) return MEZO_ERANGE;
+    if (n == 0) return MEZO_OK;
+    if (!g || !q) return MEZO_EINVAL;
+    for (uint32_t i = 0; i < n; ++i)
+        if (std::isnan(g[i])) return MEZO_ERANGE;
+    for (uint32_t i = 0; i < n; ++i) q[i] = encode(g[i], *codec);
+    return MEZO_OK;
+}
+
+int mezo_dequantize(const int8_t* q, float* g, uint32_t n, const mezo_codec_t* codec)
+{
+    if (!codec) return MEZO_EINVAL;
+    if (!codec_valid(codec)) return MEZO_ERANGE;
+    if (n == 0) return MEZO_OK;
+    if (!g || !q) return MEZO_EINVAL;
+    for (uint32_t i = 0; i < n; ++i)
+        if (q[i] == -128) return MEZO_ERANGE;
+    for (uint32_t i = 0; i < n; ++i) g[i] = decode(q[i], *codec);
+    return MEZO_OK;
+}
+
+int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t first_elem, uint64_t count,
+                        uint32_t* words_dev, float* z_dev, void* stream)
+{
+    if (first_elem > MEZO_MAX_NUMEL || count > MEZO_MAX_NUMEL - first_elem) return MEZO_EINVAL;
+    if (count == 0 || (!words_dev && !z_dev)) return MEZO_OK;
+    mezo::GenArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.rec = make_rec(seed, 0.0f, false);
+    a.tensor_id = tensor_id;
+    a.first = first_elem;
+    a.count = count;
+    a.words = words_dev;
+    a.z = z_dev;
+    MEZO_HIP(mezo::launch_generate(a, static_cast<hipStream_t>(stream)));
+    return MEZO_OK;
+}
+
+const char* mezo_strerror(int code)
+{
+    switch (code) {
+    case MEZO_OK: return "success";
+    case MEZO_EINVAL: return "invalid argument (null/misaligned pointer, bad size or duplicate tensor id)";
+    case MEZO_EDTYPE: return "unknown storage type";
+    case MEZO_EOVERLAP: return "tensors overlap in memory";
+    case MEZO_EORDER: return "seeds not strictly ascending by (machine, step, sample)";
+    case MEZO_ERANGE: return "value out of range (q = -128, NaN gradient, non-finite lr/scale, bad codec)";
+    case MEZO_EHIP: return "HIP runtime failure";
+    default: return "unknown error code";
+    }
+}
+
+const char* mezo_last_error(void) { return t_last_error.c_str(); }
+
+int mezo_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,158 @@
+// engine.hpp — device-side building blocks of the seeded perturbation engine
+// for gfx950 (MI355X): the Philox generator, the Gaussian transform and the
+// storage conversions.
+//
+// z for (seed, tensor t, element e) is defined in include/mezo.h: Philox4x32-10
+// with key = machine id and counter = (e >> 2, t, sample, step), then
+// Box-Muller on 24-bit uniforms. The paper only requires an RNG that every
+// machine can reset to the same seed and replay (Algorithm 1,
+// PerturbParameters; Appendix B on reproducing noise across devices); a
+// counter-based generator lets every lane compute its own elements' noise in
+// registers, so z is never stored.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "records.hpp"
+
+namespace mezo {
+
+__device__ __forceinline__ void mul_wide(uint32_t m, uint32_t x, uint32_t& hi, uint32_t& lo)
+{
+    uint64_t p = uint64_t(m) * uint64_t(x);
+    hi = uint32_t(p >> 32);
+    lo = uint32_t(p);
+}
+
+// a ^ b ^ c in one gfx950 v_bitop3_b32 (truth table 0x96 = three-way xor).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+// Per-call values that are the same for every element of one tensor: the
+// round-1 words that do not depend on the element, and the round-2 product
+// of the (element-independent) word 0. All scalar.
+struct SeedUniform {
+    uint32_t y1;        // round-1 output word 1
+    uint32_t kx;        // step ^ key1: folded into round-1 output word 2
+    uint32_t r2_hi;     // round 2: high word of kMulA * y0
+    uint32_t r2_lo;     // round 2: low  word of kMulA * y0 (= output word 3)
+    uint32_t k0, k1;    // round-2 key
+};
+
+__device__ __forceinline__ SeedUniform seed_uniform(const SeedRec& r, uint32_t tensor_id)
+{
+    SeedUniform u;
+    // Round 1 on counter (blk, t, sample, step) with key (key0, key1):
+    //   word 0 = hi(kMulB*sample) ^ t ^ key0   (element-independent)
+    //   word 1 = lo(kMulB*sample)              (element-independent)
+    //   word 2 = hi(kMulA*blk) ^ step ^ key1   (per element)
+    //   word 3 = lo(kMulA*blk)                 (per element, seed-independent)
+    uint32_t y0 = r.mb_hi ^ tensor_id ^ r.key0;
+    u.y1 = r.mb_lo;
+    u.kx = r.step ^ r.key1;
+    u.k0 = r.key0 + kWeylA;
+    u.k1 = r.key1 + kWeylB;
+    mul_wide(kMulA, y0, u.r2_hi, u.r2_lo);
+    return u;
+}
+
+// Seed-independent part of round 1 for block blk: kMulA * blk.
+struct BlockPre {
+    uint32_t hi, lo;
+};
+
+__device__ __forceinline__ BlockPre block_pre(uint32_t blk)
+{
+    BlockPre b;
+    mul_wide(kMulA, blk, b.hi, b.lo);
+    return b;
+}
+
+// The four Philox4x32-10 output words of one block, from the hoisted round-1
+// values: rounds 2..10 with the per-element products on the vector unit.
+__device__ __forceinline__ void philox_words(const SeedUniform& u, BlockPre b, uint32_t& x0,
+                                             uint32_t& x1, uint32_t& x2, uint32_t& x3)
+{
+    // end of round 1
+    uint32_t y2 = b.hi ^ u.kx;
+    uint32_t y3 = b.lo;
+    // round 2 (key k0, k1): products kMulA*y0 (scalar, precomputed) and kMulB*y2
+    uint32_t hb, lb;
+    mul_wide(kMulB, y2, hb, lb);
+    x0 = hb ^ u.y1 ^ u.k0;
+    x1 = lb;
+    x2 = u.r2_hi ^ y3 ^ u.k1;
+    x3 = u.r2_lo;
+    uint32_t k0 = u.k0, k1 = u.k1;
+#pragma unroll
+    for (int round = 3; round <= 10; ++round) {
+        k0 += kWeylA;
+        k1 += kWeylB;
+        uint32_t ha, la;
+        mul_wide(kMulA, x0, ha, la);
+        mul_wide(kMulB, x2, hb, lb);
+        const uint32_t n0 = xor3(hb, x1, k0);
+        const uint32_t n2 = xor3(ha, x3, k1);
+        x0 = n0;
+        x1 = lb;
+        x2 = n2;
+        x3 = la;
+    }
+}
+
+// ---- Box-Muller -----------------------------------------------------------
+// Box & Muller (1958). u1 = ((w_a >> 8) + 1) 2^-24 in (0, 1] and
+// u2 = (w_b >> 8) 2^-24 in [0, 1) are exact in fp32. v_log_f32 is log2, so
+// -2 ln u1 = (-2 ln 2) log2 u1; v_sin_f32 / v_cos_f32 take revolutions, so
+// sin(2 pi u2) needs no multiply by 2 pi.
+struct Z4 {
+    float z0, z1, z2, z3;
+};
+
+__device__ __forceinline__ void box_muller_pair(uint32_t wa, uint32_t wb, float& zc, float& zs)
+{
+    constexpr float kTwoM24 = 0x1p-24f;
+    constexpr float kMinusTwoLn2 = -1.38629436111989061883f;
+    // (t + 1) 2^-24 as one fma: t < 2^24, so the product, the sum and the
+    // result are exact.
+    float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
+    float u2 = float(wb >> 8) * kTwoM24;
+    float r = __builtin_amdgcn_sqrtf(kMinusTwoLn2 * __builtin_amdgcn_logf(u1));
+    zc = r * __builtin_amdgcn_cosf(u2);
+    zs = r * __builtin_amdgcn_sinf(u2);
+}
+
+__device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+{
+    Z4 z;
+    box_muller_pair(w0, w1, z.z0, z.z1);
+    box_muller_pair(w2, w3, z.z2, z.z3);
+    return z;
+}
+
+// ---- storage conversions ---------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t packed) { return __uint_as_float(packed & 0xFFFF0000u); }
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> two bf16 (round to nearest even, one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
+{
+    f32x2_t v = {lo, hi};
+    bf16x2_t b = __builtin_convertvector(v, bf16x2_t);
+    return __builtin_bit_cast(uint32_t, b);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float x)
+{
+    __bf16 b = static_cast<__bf16>(x);
+    return __builtin_bit_cast(uint16_t, b);
+}
+
+}  // namespace mezo

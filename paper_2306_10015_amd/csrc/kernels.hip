@@ -1,0 +1,335 @@
+// kernels.hip — HIP kernels of the seeded perturbation engine (gfx950).
+//
+// One kernel applies any sequence of seeded perturbations to a whole parameter
+// set in one pass: PerturbParameters (one record), the fused apply loop of one
+// iteration (K records, the last flagged) and the late-joiner replay (T steps
+// of records, each step's last flagged). Every element is read once and
+// written once; its noise is regenerated in registers for every record.
+//
+// Launch shape: one launch per storage type, one workgroup per 2048-element
+// tile; the workgroup finds its tensor with two scalar loads (tile -> tensor
+// index -> descriptor). theta streams through with non-temporal 16-byte loads
+// and stores (it is touched once per call, so it should not displace anything
+// in the caches). Per lane, the seed-independent round-1 Philox product of each
+// owned block is computed once and reused by every record; seed words, tensor
+// id and coefficient are wave-uniform and live in SGPRs (scalar loads from the
+// kernel arguments or from the staged record buffer).
+#include "engine.hpp"
+#include "launch.hpp"
+
+namespace mezo {
+
+template <bool kInline>
+__device__ __forceinline__ const SeedRec& rec_at(const EngineArgs& a, uint32_t r)
+{
+    if constexpr (kInline)
+        return a.inl[r];
+    else
+        return a.ext[r];
+}
+
+template <uint32_t kDtype>
+struct Layout;
+template <>
+struct Layout<kF32> {
+    static constexpr int kGroups = kGroupsF32;
+    static constexpr uint64_t kPerGroup = 4;  // elements per 16-byte group
+};
+template <>
+struct Layout<kBF16> {
+    static constexpr int kGroups = kGroupsBF16;
+    static constexpr uint64_t kPerGroup = 8;
+};
+
+// The 16-byte groups a lane owns in one tile, as loaded from memory. A group
+// that runs past the end of its tensor is not loaded here (it stays zero) and
+// is read element by element when the tile is processed.
+template <int kGroups>
+struct TileRaw {
+    uint4 g[kGroups];
+};
+
+template <int kGroups>
+__device__ __forceinline__ uint64_t group_index(uint64_t tile, int g)
+{
+    return tile * (kThreads * kGroups) + uint64_t(g) * kThreads + threadIdx.x;
+}
+
+// Parameter memory is global memory; saying so lets the compiler use global_*
+// instead of flat_* instructions for addresses read from the tensor table.
+#define MEZO_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef MEZO_GLOBAL u32x4_t gu32x4_t;
+typedef MEZO_GLOBAL float gfloat_t;
+typedef MEZO_GLOBAL uint16_t gu16_t;
+
+__device__ __forceinline__ uint4 load_stream(uint64_t addr)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const gu32x4_t*>(addr));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store_stream(uint64_t addr, uint4 v)
+{
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<gu32x4_t*>(addr));
+}
+
+template <uint32_t kDtype>
+__device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t tile,
+                                          TileRaw<Layout<kDtype>::kGroups>& raw)
+{
+    constexpr int kGroups = Layout<kDtype>::kGroups;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const uint64_t grp = group_index<kGroups>(tile, g);
+        if ((grp + 1) * Layout<kDtype>::kPerGroup <= d.numel)
+            raw.g[g] = load_stream(d.data + grp * 16);
+        else
+            raw.g[g] = make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+// One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
+// (one Philox block each).
+template <bool kInline>
+__device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& d, uint64_t tile,
+                                         const TileRaw<kGroupsF32>& raw)
+{
+    constexpr int kGroups = kGroupsF32;
+    gfloat_t* __restrict__ base = reinterpret_cast<gfloat_t*>(d.data);
+    const uint64_t numel = d.numel;
+    float th[kGroups][4];
+    float acc[kGroups][4];
+    BlockPre pre[kGroups];
+    uint64_t e0[kGroups];
+
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const uint64_t grp = group_index<kGroups>(tile, g);
+        e0[g] = grp * 4;
+        if (e0[g] + 4 <= numel) {
+            th[g][0] = __uint_as_float(raw.g[g].x);
+            th[g][1] = __uint_as_float(raw.g[g].y);
+            th[g][2] = __uint_as_float(raw.g[g].z);
+            th[g][3] = __uint_as_float(raw.g[g].w);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) th[g][j] = (e0[g] + j < numel) ? base[e0[g] + j] : 0.0f;
+        }
+        pre[g] = block_pre(uint32_t(grp));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[g][j] = 0.0f;
+    }
+
+    for (uint32_t r = 0; r < a.n_rec; ++r) {
+        const SeedRec& rec = rec_at<kInline>(a, r);
+        const SeedUniform u = seed_uniform(rec, d.tensor_id);
+        const float c = rec.coef;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            uint32_t w0, w1, w2, w3;
+            philox_words(u, pre[g], w0, w1, w2, w3);
+            const Z4 z = gauss4(w0, w1, w2, w3);
+            acc[g][0] = __builtin_fmaf(c, z.z0, acc[g][0]);
+            acc[g][1] = __builtin_fmaf(c, z.z1, acc[g][1]);
+            acc[g][2] = __builtin_fmaf(c, z.z2, acc[g][2]);
+            acc[g][3] = __builtin_fmaf(c, z.z3, acc[g][3]);
+        }
+        if (rec.last) {
+#pragma unroll
+            for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    th[g][j] = th[g][j] + acc[g][j];
+                    acc[g][j] = 0.0f;
+                }
+        }
+    }
+
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        if (e0[g] + 4 <= numel) {
+            store_stream(d.data + e0[g] * 4, make_uint4(__float_as_uint(th[g][0]), __float_as_uint(th[g][1]),
+                                                        __float_as_uint(th[g][2]), __float_as_uint(th[g][3])));
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (e0[g] + j < numel) base[e0[g] + j] = th[g][j];
+        }
+    }
+}
+
+// One tile of a bf16 tensor: each lane owns kGroups groups of 8 elements (two
+// Philox blocks each). theta is held as fp32 holding a bf16 value; a step ends
+// with one RNE rounding back to bf16.
+template <bool kInline>
+__device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t tile,
+                                          const TileRaw<kGroupsBF16>& raw)
+{
+    constexpr int kGroups = kGroupsBF16;
+    gu16_t* __restrict__ base = reinterpret_cast<gu16_t*>(d.data);
+    const uint64_t numel = d.numel;
+    float th[kGroups][8];
+    float acc[kGroups][8];
+    BlockPre pre[kGroups][2];
+    uint64_t e0[kGroups];
+
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const uint64_t grp = group_index<kGroups>(tile, g);
+        e0[g] = grp * 8;
+        if (e0[g] + 8 <= numel) {
+            const uint4 v = raw.g[g];
+            th[g][0] = bf16_lo(v.x);
+            th[g][1] = bf16_hi(v.x);
+            th[g][2] = bf16_lo(v.y);
+            th[g][3] = bf16_hi(v.y);
+            th[g][4] = bf16_lo(v.z);
+            th[g][5] = bf16_hi(v.z);
+            th[g][6] = bf16_lo(v.w);
+            th[g][7] = bf16_hi(v.w);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                th[g][j] = (e0[g] + j < numel) ? __uint_as_float(uint32_t(base[e0[g] + j]) << 16) : 0.0f;
+        }
+        pre[g][0] = block_pre(uint32_t(2 * grp));
+        pre[g][1] = block_pre(uint32_t(2 * grp + 1));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[g][j] = 0.0f;
+    }
+
+    for (uint32_t r = 0; r < a.n_rec; ++r) {
+        const SeedRec& rec = rec_at<kInline>(a, r);
+        const SeedUniform u = seed_uniform(rec, d.tensor_id);
+        const float c = rec.coef;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                uint32_t w0, w1, w2, w3;
+                philox_words(u, pre[g][h], w0, w1, w2, w3);
+                const Z4 z = gauss4(w0, w1, w2, w3);
+                acc[g][4 * h + 0] = __builtin_fmaf(c, z.z0, acc[g][4 * h + 0]);
+                acc[g][4 * h + 1] = __builtin_fmaf(c, z.z1, acc[g][4 * h + 1]);
+                acc[g][4 * h + 2] = __builtin_fmaf(c, z.z2, acc[g][4 * h + 2]);
+                acc[g][4 * h + 3] = __builtin_fmaf(c, z.z3, acc[g][4 * h + 3]);
+            }
+        if (rec.last) {
+#pragma unroll
+            for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+                for (int j = 0; j < 8; j += 2) {
+                    const uint32_t p = pack_bf16(th[g][j] + acc[g][j], th[g][j + 1] + acc[g][j + 1]);
+                    th[g][j] = bf16_lo(p);
+                    th[g][j + 1] = bf16_hi(p);
+                    acc[g][j] = 0.0f;
+                    acc[g][j + 1] = 0.0f;
+                }
+        }
+    }
+
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        if (e0[g] + 8 <= numel) {
+            uint4 v;
+            v.x = pack_bf16(th[g][0], th[g][1]);
+            v.y = pack_bf16(th[g][2], th[g][3]);
+            v.z = pack_bf16(th[g][4], th[g][5]);
+            v.w = pack_bf16(th[g][6], th[g][7]);
+            store_stream(d.data + e0[g] * 2, v);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (e0[g] + j < numel) base[e0[g] + j] = to_bf16(th[g][j]);
+        }
+    }
+}
+
+template <bool kInline, uint32_t kDtype>
+__global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
+{
+    const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
+    const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+    TileRaw<Layout<kDtype>::kGroups> raw;
+    load_tile<kDtype>(d, tile - d.tile_begin, raw);
+    if constexpr (kDtype == kF32)
+        tile_f32<kInline>(a, d, tile - d.tile_begin, raw);
+    else
+        tile_bf16<kInline>(a, d, tile - d.tile_begin, raw);
+}
+
+// Inspection: RNG words and Gaussians of a range of elements, one Philox
+// block per lane, through the same generator functions as the engine.
+__global__ __launch_bounds__(kThreads) void generate_kernel(GenArgs a)
+{
+    const uint64_t blk = (a.first >> 2) + uint64_t(blockIdx.x) * kThreads + threadIdx.x;
+    const uint64_t end = a.first + a.count;
+    const uint64_t eb = blk * 4;
+    if (eb >= end) return;
+    const SeedUniform u = seed_uniform(a.rec, a.tensor_id);
+    uint32_t w[4];
+    philox_words(u, block_pre(uint32_t(blk)), w[0], w[1], w[2], w[3]);
+    const Z4 z4 = gauss4(w[0], w[1], w[2], w[3]);
+    const float z[4] = {z4.z0, z4.z1, z4.z2, z4.z3};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint64_t e = eb + j;
+        if (e < a.first || e >= end) continue;
+        const uint64_t i = e - a.first;
+        if (a.words) a.words[i] = w[j];
+        if (a.z) a.z[i] = z[j];
+    }
+}
+
+// ---- host-side launchers ----------------------------------------------------
+
+hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream)
+{
+    if (args.total_tiles == 0) return hipSuccess;
+    if (args.total_tiles > uint64_t(0x7FFFFFFF) || dtype > kBF16) return hipErrorInvalidValue;
+    const bool inl = args.n_rec <= kInlineRecs;
+    const dim3 g{uint32_t(args.total_tiles)};
+    const dim3 b{uint32_t(kThreads)};
+    if (inl) {
+        if (dtype == kF32)
+            hipLaunchKernelGGL((engine_kernel<true, kF32>), g, b, 0, stream, args);
+        else
+            hipLaunchKernelGGL((engine_kernel<true, kBF16>), g, b, 0, stream, args);
+    } else {
+        if (dtype == kF32)
+            hipLaunchKernelGGL((engine_kernel<false, kF32>), g, b, 0, stream, args);
+        else
+            hipLaunchKernelGGL((engine_kernel<false, kBF16>), g, b, 0, stream, args);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_generate(const GenArgs& args, hipStream_t stream)
+{
+    // At most 2^26 blocks (2^28 elements) per launch keeps the grid small.
+    const uint64_t kChunk = uint64_t(1) << 28;
+    GenArgs a = args;
+    uint64_t left = args.count;
+    uint64_t first = args.first;
+    uint64_t done = 0;
+    while (left > 0) {
+        const uint64_t n = left < kChunk ? left : kChunk;
+        a.first = first;
+        a.count = n;
+        a.words = args.words ? args.words + done : nullptr;
+        a.z = args.z ? args.z + done : nullptr;
+        const uint64_t nblk = ((first + n - 1) >> 2) - (first >> 2) + 1;
+        const uint64_t grid = (nblk + kThreads - 1) / kThreads;
+        hipLaunchKernelGGL(generate_kernel, dim3(uint32_t(grid)), dim3(kThreads), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        left -= n;
+        first += n;
+        done += n;
+    }
+    return hipSuccess;
+}
+
+}  // namespace mezo

@@ -1,0 +1,39 @@
+// launch.hpp — interface between the C-ABI host code (api.cpp) and the
+// kernels (kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "records.hpp"
+
+namespace mezo {
+
+// Kernel arguments of the engine kernel, one launch per storage type. Up to
+// kInlineRecs records travel in the arguments themselves; longer lists are
+// staged in device memory (ext).
+struct EngineArgs {
+    const TensorDesc* tensors;     // device table of one storage type, tile_begin ascending
+    const uint32_t* tile_tensor;   // device: index into tensors of every tile
+    uint64_t total_tiles;
+    const SeedRec* ext;         // device records when n_rec > kInlineRecs
+    uint32_t n_tensors;
+    uint32_t n_rec;
+    SeedRec inl[kInlineRecs];
+};
+
+struct GenArgs {
+    SeedRec rec;
+    uint64_t first;
+    uint64_t count;
+    uint32_t* words;
+    float* z;
+    uint32_t tensor_id;
+};
+
+// Launch the engine over the tensors of one storage type (dtype): one
+// workgroup per tile (at most 2^31 - 1 tiles).
+hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream);
+hipError_t launch_generate(const GenArgs& args, hipStream_t stream);
+
+}  // namespace mezo

@@ -1,0 +1,59 @@
+// records.hpp — structures and constants shared by the host code (api.cpp)
+// and the kernels (kernels.hip): the seed record, the tensor table entry, the
+// work decomposition and the Philox4x32-10 constants.
+#pragma once
+
+#include <stdint.h>
+
+namespace mezo {
+
+// One perturbation to apply: seed-derived Philox inputs and its weight.
+// 32 bytes, read by every wave with one scalar load.
+struct alignas(16) SeedRec {
+    uint32_t key0;    // Philox key, low word  = low 32 bits of the machine id
+    uint32_t key1;    // Philox key, high word = high 32 bits of the machine id
+    uint32_t step;    // counter word 3
+    uint32_t mb_hi;   // high word of kMulB * sample (round 1, counter word 2)
+    uint32_t mb_lo;   // low word  of kMulB * sample
+    float    coef;    // weight c of z in theta += c * z
+    uint32_t last;    // 1: round to storage after this record (end of a step)
+    uint32_t sample;  // counter word 2 (inspection only)
+};
+
+// One registered tensor as the kernels see it.
+struct alignas(16) TensorDesc {
+    uint64_t data;        // device address, 16-byte aligned
+    uint64_t numel;
+    uint64_t tile_begin;  // first global tile of this tensor
+    uint32_t tensor_id;
+    uint32_t dtype;       // 0 = fp32, 1 = bf16
+};
+
+constexpr uint32_t kF32 = 0u;
+constexpr uint32_t kBF16 = 1u;
+
+// Work decomposition: a workgroup of kThreads lanes handles one tile per
+// iteration; each lane owns a few 16-byte groups of the tile, strided by
+// kThreads groups so that every wave touches one contiguous 1 KiB run per
+// group. A 16-byte group is 4 fp32 elements (one Philox block) or 8 bf16
+// elements (two blocks), so both storage types give every lane two
+// independent Philox blocks per record and 2048-element tiles.
+constexpr int kThreads = 256;
+constexpr int kGroupsF32 = 2;
+constexpr int kGroupsBF16 = 1;
+constexpr uint64_t kTileF32 = uint64_t(kThreads) * kGroupsF32 * 4;
+constexpr uint64_t kTileBF16 = uint64_t(kThreads) * kGroupsBF16 * 8;
+
+// Records that travel inside the kernel arguments (above this they are staged
+// in device memory).
+constexpr uint32_t kInlineRecs = 32;
+
+// ---- Philox4x32-10 ---------------------------------------------------------
+// Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3"
+// (SC'11): multipliers and Weyl key increments of the 4x32 variant.
+constexpr uint32_t kMulA = 0xD2511F53u;
+constexpr uint32_t kMulB = 0xCD9E8D57u;
+constexpr uint32_t kWeylA = 0x9E3779B9u;
+constexpr uint32_t kWeylB = 0xBB67AE85u;
+
+}  // namespace mezo

@@ -1,0 +1,265 @@
+"""Python binding of libmezo (include/mezo.h): argument marshalling only.
+
+Every step of the engine runs in the library's HIP kernels; PyTorch supplies
+device memory and the current stream. Importing this module loads
+``libmezo.so`` from this directory and raises if it is not built (build it
+with ``python -m paper_2306_10015_amd.build``); there is no fallback.
+
+    import torch
+    from paper_2306_10015_amd import mezo
+    params = [torch.randn(1024, 1024, device="cuda") * 0.02 for _ in range(4)]
+    ps = mezo.ParamSet(params)                       # tensor_id = position
+    s = (machine_id, step, sample)
+    ps.perturb(s, +eps); ...; ps.perturb(s, -2 * eps); ...; ps.perturb(s, +eps)
+    q = mezo.quantize_projgrad([(l_plus - l_minus) / (2 * eps)])
+    ps.update_multi(seeds, q_all, lr=eta / n_grads)  # Algorithm 1 apply loop
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from pathlib import Path
+from typing import Iterable, Sequence
+
+import numpy as np
+
+LIB_PATH = Path(__file__).resolve().parent / "libmezo.so"
+
+OK, EINVAL, EDTYPE, EOVERLAP, EORDER, ERANGE, EHIP = 0, -1, -2, -3, -4, -5, -6
+F32, BF16 = 0, 1
+LINEAR, SIGNED_LOG = 0, 1
+#: Signed-log slope of a base-2 log: code 127 decodes just inside fp32.
+LOG2_ALPHA = 1.0 / math.log(2.0)
+MAX_NUMEL = 1 << 34
+
+#: Layout of mezo_seed_t: (machine u64, step u32, sample u32), 16 bytes.
+SEED_DTYPE = np.dtype([("machine", "<u8"), ("step", "<u4"), ("sample", "<u4")])
+
+
+class Seed(ctypes.Structure):
+    _fields_ = [("machine", ctypes.c_uint64), ("step", ctypes.c_uint32),
+                ("sample", ctypes.c_uint32)]
+
+
+class Tensor(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("numel", ctypes.c_uint64),
+                ("tensor_id", ctypes.c_uint32), ("dtype", ctypes.c_uint32)]
+
+
+class Codec(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_uint32), ("scale", ctypes.c_float), ("alpha", ctypes.c_float)]
+
+
+class Step(ctypes.Structure):
+    _fields_ = [("seeds", ctypes.c_void_p), ("q", ctypes.c_void_p), ("K", ctypes.c_uint32),
+                ("lr", ctypes.c_float)]
+
+
+#: Every symbol include/mezo.h declares.
+EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
+           "mezo_perturb", "mezo_update_multi", "mezo_replay", "quantize_projgrad",
+           "mezo_dequantize", "mezo_debug_generate", "mezo_strerror", "mezo_last_error",
+           "mezo_version")
+
+
+def _load() -> ctypes.CDLL:
+    # libmezo must run on the same HIP runtime as torch: the streams and device
+    # pointers it receives belong to that runtime. torch carries its own copy
+    # (same SONAME); importing torch first makes the dynamic loader bind
+    # libmezo to it instead of loading a second runtime.
+    import torch  # noqa: F401
+    if not LIB_PATH.exists():
+        raise ImportError(f"{LIB_PATH} is not built: run python -m paper_2306_10015_amd.build")
+    L = ctypes.CDLL(str(LIB_PATH))
+    vp, u32, u64, i32, f32 = (ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int,
+                               ctypes.c_float)
+    L.mezo_paramset_create.argtypes = [ctypes.POINTER(Tensor), u32, ctypes.POINTER(vp)]
+    L.mezo_paramset_create.restype = i32
+    L.mezo_paramset_destroy.argtypes = [vp]
+    L.mezo_paramset_destroy.restype = None
+    L.mezo_paramset_numel.argtypes = [vp]
+    L.mezo_paramset_numel.restype = u64
+    L.mezo_perturb.argtypes = [vp, Seed, f32, vp]
+    L.mezo_perturb.restype = i32
+    L.mezo_update_multi.argtypes = [vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
+    L.mezo_update_multi.restype = i32
+    L.mezo_replay.argtypes = [vp, ctypes.POINTER(Step), u32, ctypes.POINTER(Codec), vp]
+    L.mezo_replay.restype = i32
+    L.quantize_projgrad.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
+    L.quantize_projgrad.restype = i32
+    L.mezo_dequantize.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
+    L.mezo_dequantize.restype = i32
+    L.mezo_debug_generate.argtypes = [Seed, u32, u64, u64, vp, vp, vp]
+    L.mezo_debug_generate.restype = i32
+    L.mezo_strerror.argtypes = [i32]
+    L.mezo_strerror.restype = ctypes.c_char_p
+    L.mezo_last_error.argtypes = []
+    L.mezo_last_error.restype = ctypes.c_char_p
+    L.mezo_version.argtypes = []
+    L.mezo_version.restype = i32
+    return L
+
+
+lib = _load()
+
+
+class MezoError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        msg = lib.mezo_strerror(code).decode()
+        if code == EHIP:
+            msg += f" ({lib.mezo_last_error().decode()})"
+        super().__init__(f"{what}: {msg} [code {code}]")
+        self.code = code
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != OK:
+        raise MezoError(rc, what)
+
+
+def codec(kind: int = LINEAR, scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA) -> Codec:
+    return Codec(kind, scale, alpha)
+
+
+DEFAULT_CODEC = codec()
+
+
+def _seed(s) -> Seed:
+    if isinstance(s, Seed):
+        return s
+    if isinstance(s, np.void):
+        return Seed(int(s["machine"]), int(s["step"]), int(s["sample"]))
+    m, t, j = s
+    return Seed(int(m), int(t), int(j))
+
+
+def seeds_array(seeds) -> np.ndarray:
+    """Any sequence of (machine, step, sample) -> contiguous SEED_DTYPE array."""
+    if isinstance(seeds, np.ndarray) and seeds.dtype == SEED_DTYPE:
+        return np.ascontiguousarray(seeds)
+    out = np.zeros(len(seeds), dtype=SEED_DTYPE)
+    for i, s in enumerate(seeds):
+        out[i] = s if isinstance(s, np.void) else (int(s[0]), int(s[1]), int(s[2]))
+    return out
+
+
+def _stream_ptr(stream) -> int | None:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported parameter dtype {t.dtype}")
+
+
+class ParamSet:
+    """A registered set of parameter tensors (device memory owned by torch).
+
+    ``tensor_ids`` default to the position in ``tensors``; they select each
+    tensor's noise stream and must be the same on every machine.
+    """
+
+    def __init__(self, tensors: Sequence, tensor_ids: Iterable[int] | None = None):
+        self.tensors = list(tensors)
+        ids = list(range(len(self.tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
+        if len(ids) != len(self.tensors):
+            raise ValueError("one tensor_id per tensor")
+        arr = (Tensor * max(1, len(self.tensors)))()
+        for i, (t, tid) in enumerate(zip(self.tensors, ids)):
+            if not t.is_cuda or not t.is_contiguous():
+                raise ValueError("parameters must be contiguous CUDA tensors")
+            arr[i] = Tensor(t.data_ptr(), t.numel(), tid, _dtype_code(t))
+        h = ctypes.c_void_p()
+        _check(lib.mezo_paramset_create(arr, len(self.tensors), ctypes.byref(h)),
+               "mezo_paramset_create")
+        self._h = h
+        self.tensor_ids = ids
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        return self._h
+
+    @property
+    def numel(self) -> int:
+        return int(lib.mezo_paramset_numel(self._h))
+
+    def close(self) -> None:
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib.mezo_paramset_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def perturb(self, seed, scale: float, stream=None) -> None:
+        """PerturbParameters: theta += scale * z(seed)."""
+        _check(lib.mezo_perturb(self._h, _seed(seed), float(scale), _stream_ptr(stream)),
+               "mezo_perturb")
+
+    def update_multi(self, seeds, q, lr: float, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
+        """Apply loop of one iteration: theta -= lr * sum_k deq(q_k) z(seed_k)."""
+        sa = seeds_array(seeds)
+        qa = np.ascontiguousarray(q, dtype=np.int8)
+        if sa.size != qa.size:
+            raise ValueError("seeds and q differ in length")
+        _check(lib.mezo_update_multi(self._h, sa.ctypes.data, qa.ctypes.data, sa.size,
+                                     ctypes.byref(codec_), float(lr), _stream_ptr(stream)),
+               "mezo_update_multi")
+
+    def replay(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
+        """Late-joiner catch-up: steps = [(seeds, q, lr), ...] in order."""
+        keep = []
+        arr = (Step * max(1, len(steps)))()
+        for i, (s, q, lr) in enumerate(steps):
+            sa = seeds_array(s)
+            qa = np.ascontiguousarray(q, dtype=np.int8)
+            if sa.size != qa.size:
+                raise ValueError(f"step {i}: seeds and q differ in length")
+            keep.append((sa, qa))
+            arr[i] = Step(sa.ctypes.data, qa.ctypes.data, sa.size, float(lr))
+        _check(lib.mezo_replay(self._h, arr, len(steps), ctypes.byref(codec_),
+                               _stream_ptr(stream)), "mezo_replay")
+
+
+def quantize_projgrad(g, codec_: Codec = DEFAULT_CODEC) -> np.ndarray:
+    ga = np.ascontiguousarray(g, dtype=np.float32)
+    q = np.zeros(ga.size, dtype=np.int8)
+    _check(lib.quantize_projgrad(ga.ctypes.data, q.ctypes.data, ga.size, ctypes.byref(codec_)),
+           "quantize_projgrad")
+    return q
+
+
+def dequantize(q, codec_: Codec = DEFAULT_CODEC) -> np.ndarray:
+    qa = np.ascontiguousarray(q, dtype=np.int8)
+    g = np.zeros(qa.size, dtype=np.float32)
+    _check(lib.mezo_dequantize(qa.ctypes.data, g.ctypes.data, qa.size, ctypes.byref(codec_)),
+           "mezo_dequantize")
+    return g
+
+
+def debug_generate(seed, tensor_id: int, first: int, count: int, words=True, z=True,
+                   stream=None):
+    """Device tensors (words uint32 as int32 bits, z float32) of elements
+    first .. first+count-1 of tensor tensor_id under seed."""
+    import torch
+    w = torch.empty(count, dtype=torch.int32, device="cuda") if words else None
+    zz = torch.empty(count, dtype=torch.float32, device="cuda") if z else None
+    _check(lib.mezo_debug_generate(_seed(seed), int(tensor_id), int(first), int(count),
+                                   None if w is None else w.data_ptr(),
+                                   None if zz is None else zz.data_ptr(), _stream_ptr(stream)),
+           "mezo_debug_generate")
+    return w, zz
+
+
+def version() -> int:
+    return int(lib.mezo_version())

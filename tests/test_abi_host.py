@@ -1,0 +1,198 @@
+"""Host-side tests of libmezo that need no GPU: the library loads and exports
+every symbol include/mezo.h declares; the one-byte codec (Section 3) matches
+the oracle bit for bit; argument checks return the documented codes before
+anything touches a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2306_10015_amd import mezo
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "mezo.h")).read()
+    return sorted(set(re.findall(r"^MEZO_API\s+[\w\s\*]*?\b(\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary_calls():
+    names = declared_symbols()
+    for required in ("mezo_perturb", "mezo_update_multi", "mezo_replay", "quantize_projgrad"):
+        assert required in names
+    assert sorted(mezo.EXPORTS) == names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(str(mezo.LIB_PATH))
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def test_no_cpu_fallback_in_the_binding():
+    """The binding only marshals arguments: it never imports the oracle."""
+    src = open(mezo.__file__).read()
+    assert "oracle" not in src.replace("oracle.", "")  # no import or call
+    assert "import oracle" not in src
+
+
+# ---- codec parity with the oracle -----------------------------------------
+
+CODECS = [(mezo.LINEAR, 1 / 127, 1.0), (mezo.LINEAR, 0.25, 1.0), (mezo.LINEAR, 3e-4, 1.0),
+          (mezo.SIGNED_LOG, 1.0, mezo.LOG2_ALPHA), (mezo.SIGNED_LOG, 1.0, 3.0),
+          (mezo.SIGNED_LOG, 1.0, 17.5)]
+
+
+@pytest.mark.parametrize("kind,scale,alpha", CODECS)
+def test_quantize_matches_oracle_bit_exact(kind, scale, alpha):
+    rng = np.random.Generator(np.random.PCG64(31))
+    g = np.concatenate([
+        rng.normal(0, 1, 20000), rng.normal(0, 1e3, 20000), rng.uniform(-2, 2, 20000),
+        (np.arange(-300, 301) * 0.5) * scale,            # exact ties of the linear code
+        np.array([0.0, -0.0, np.inf, -np.inf, 3.4e38, -3.4e38, 1e-45]),
+    ]).astype(np.float32)
+    got = mezo.quantize_projgrad(g, mezo.codec(kind, scale, alpha))
+    want = oracle.quantize(g, kind, scale, alpha)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("kind,scale,alpha", CODECS)
+def test_dequantize_matches_oracle_bit_exact(kind, scale, alpha):
+    q = np.arange(-127, 128, dtype=np.int8)
+    got = mezo.dequantize(q, mezo.codec(kind, scale, alpha))
+    want = oracle.dequantize(q, kind, scale, alpha)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_codec_errors():
+    with pytest.raises(mezo.MezoError) as e:
+        mezo.quantize_projgrad([np.nan])
+    assert e.value.code == mezo.ERANGE
+    with pytest.raises(mezo.MezoError) as e:
+        mezo.dequantize([-128])
+    assert e.value.code == mezo.ERANGE
+    for bad in (mezo.codec(mezo.LINEAR, 0.0), mezo.codec(mezo.LINEAR, float("inf")),
+                mezo.codec(mezo.SIGNED_LOG, 1.0, 1.0), mezo.codec(7, 1.0, 1.0)):
+        with pytest.raises(mezo.MezoError) as e:
+            mezo.quantize_projgrad([1.0], bad)
+        assert e.value.code == mezo.ERANGE
+    assert mezo.quantize_projgrad(np.zeros(0, dtype=np.float32)).size == 0
+
+
+# ---- argument checks (no device is touched) -------------------------------
+
+def create(entries):
+    arr = (mezo.Tensor * max(1, len(entries)))()
+    for i, (ptr, n, tid, dt) in enumerate(entries):
+        arr[i] = mezo.Tensor(ptr, n, tid, dt)
+    h = ctypes.c_void_p()
+    rc = mezo.lib.mezo_paramset_create(arr, len(entries), ctypes.byref(h))
+    return rc, h
+
+
+@pytest.mark.parametrize("entries,code", [
+    ([], mezo.EINVAL),
+    ([(0, 16, 0, mezo.F32)], mezo.EINVAL),                         # null data
+    ([(0x1004, 16, 0, mezo.F32)], mezo.EINVAL),                    # not 16-byte aligned
+    ([(0x1000, 0, 0, mezo.F32)], mezo.EINVAL),                     # empty tensor
+    ([(0x1000, (1 << 34) + 1, 0, mezo.F32)], mezo.EINVAL),         # too many elements
+    ([(0x1000, 16, 0, 5)], mezo.EDTYPE),
+    ([(0x1000, 16, 3, mezo.F32), (0x2000, 16, 3, mezo.F32)], mezo.EINVAL),   # duplicate id
+    ([(0x1000, 16, 0, mezo.F32), (0x1030, 16, 1, mezo.F32)], mezo.EOVERLAP),
+    ([(0x1000, 16, 0, mezo.BF16), (0x1010, 16, 1, mezo.F32)], mezo.EOVERLAP),
+])
+def test_paramset_create_rejects(entries, code):
+    rc, h = create(entries)
+    assert rc == code
+    assert not h.value
+
+
+def test_paramset_create_accepts_adjacent_and_reports_numel():
+    rc, h = create([(0x1000, 16, 0, mezo.F32), (0x1040, 24, 1, mezo.BF16)])
+    assert rc == mezo.OK
+    assert mezo.lib.mezo_paramset_numel(h) == 40
+    mezo.lib.mezo_paramset_destroy(h)
+    mezo.lib.mezo_paramset_destroy(None)
+
+
+@pytest.fixture
+def fake_ps():
+    rc, h = create([(0x10000, 1024, 0, mezo.F32)])
+    assert rc == mezo.OK
+    yield h
+    mezo.lib.mezo_paramset_destroy(h)
+
+
+def seeds_of(*triples):
+    return mezo.seeds_array(list(triples))
+
+
+def test_update_argument_checks(fake_ps):
+    lib = mezo.lib
+    c = mezo.codec()
+    s = seeds_of((0, 0, 0), (1, 0, 0))
+    q = np.array([3, 4], dtype=np.int8)
+    assert lib.mezo_update_multi(None, s.ctypes.data, q.ctypes.data, 2, c, 1e-3, None) == mezo.EINVAL
+    assert lib.mezo_update_multi(fake_ps, None, q.ctypes.data, 2, c, 1e-3, None) == mezo.EINVAL
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, q.ctypes.data, 2, None, 1e-3, None) == mezo.EINVAL
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, q.ctypes.data, 2, c, float("nan"), None) == mezo.ERANGE
+    bad_q = np.array([3, -128], dtype=np.int8)
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, bad_q.ctypes.data, 2, c, 1e-3, None) == mezo.ERANGE
+    for order in [((1, 0, 0), (0, 0, 0)), ((0, 0, 0), (0, 0, 0)), ((0, 1, 0), (0, 0, 5)),
+                  ((0, 0, 2), (0, 0, 1))]:
+        so = seeds_of(*order)
+        assert lib.mezo_update_multi(fake_ps, so.ctypes.data, q.ctypes.data, 2, c, 1e-3, None) == mezo.EORDER
+    # no-ops return OK without touching a device
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, q.ctypes.data, 0, c, 1e-3, None) == mezo.OK
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, q.ctypes.data, 2, c, 0.0, None) == mezo.OK
+    z = np.zeros(2, dtype=np.int8)
+    assert lib.mezo_update_multi(fake_ps, s.ctypes.data, z.ctypes.data, 2, c, 1e-3, None) == mezo.OK
+
+
+def test_perturb_and_replay_argument_checks(fake_ps):
+    lib = mezo.lib
+    assert lib.mezo_perturb(fake_ps, mezo.Seed(0, 0, 0), float("inf"), None) == mezo.ERANGE
+    assert lib.mezo_perturb(None, mezo.Seed(0, 0, 0), 1.0, None) == mezo.EINVAL
+    assert lib.mezo_perturb(fake_ps, mezo.Seed(0, 0, 0), 0.0, None) == mezo.OK
+    c = mezo.codec()
+    steps = (mezo.Step * 2)()
+    s0 = seeds_of((0, 0, 0), (1, 0, 0))
+    s1 = seeds_of((1, 1, 0), (0, 1, 0))          # unsorted
+    q = np.array([1, 2], dtype=np.int8)
+    steps[0] = mezo.Step(s0.ctypes.data, q.ctypes.data, 2, 1e-3)
+    steps[1] = mezo.Step(s1.ctypes.data, q.ctypes.data, 2, 1e-3)
+    assert lib.mezo_replay(fake_ps, steps, 2, c, None) == mezo.EORDER
+    assert lib.mezo_replay(fake_ps, steps, 0, c, None) == mezo.OK
+    assert lib.mezo_replay(fake_ps, None, 2, c, None) == mezo.EINVAL
+    steps[1] = mezo.Step(s0.ctypes.data, q.ctypes.data, 2, float("nan"))
+    assert lib.mezo_replay(fake_ps, steps, 2, c, None) == mezo.ERANGE
+
+
+def test_debug_generate_range_check():
+    lib = mezo.lib
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, (1 << 34) - 4, 8, 0x1000, None, None) == mezo.EINVAL
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 0, 0x1000, None, None) == mezo.OK
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 16, None, None, None) == mezo.OK
+
+
+def test_strerror_covers_every_code():
+    for code in (mezo.OK, mezo.EINVAL, mezo.EDTYPE, mezo.EOVERLAP, mezo.EORDER, mezo.ERANGE,
+                 mezo.EHIP):
+        assert mezo.lib.mezo_strerror(code).decode() not in ("", "unknown error code")
+    assert mezo.lib.mezo_strerror(-99).decode() == "unknown error code"
+
+
+def test_one_hip_runtime_in_the_process():
+    """libmezo binds to the HIP runtime torch loaded (torch's streams and
+    pointers are only valid there); no second copy is mapped."""
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            p = line.split()[-1]
+            if "libamdhip64" in p:
+                paths.add(p)
+    assert len(paths) == 1, paths
