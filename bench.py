@@ -62,7 +62,7 @@ INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
 #: counter profile of the engine kernel on this workload (FETCH_SIZE /
 #: WRITE_SIZE per dispatch, calibrated against a plain copy); its traffic is
 #: reported only while the kernel sources it was taken on are unchanged.
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_opt125m_f32_traffic.json")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_{workload}_traffic.json")
 KERNEL_SOURCES = ["paper_2306_10015_amd/csrc/kernels.hip", "paper_2306_10015_amd/csrc/engine.hpp",
                   "paper_2306_10015_amd/csrc/records.hpp"]
 
@@ -119,12 +119,23 @@ def main():
 
     # ---- inputs resident in HBM before timing -------------------------------
     flat, views, offs = flat_views(torch, w, dev)
-    for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
-        h = synth.theta0_tensor(shape, w.dtype, i, 0)
-        if w.dtype == "f32":
-            v.copy_(torch.from_numpy(h))
-        else:
-            v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+    if N <= 200_000_000:
+        # numpy PCG64 per tensor (the same theta0 the tests and the oracle use)
+        for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
+            h = synth.theta0_tensor(shape, w.dtype, i, 0)
+            if w.dtype == "f32":
+                v.copy_(torch.from_numpy(h))
+            else:
+                v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+    else:
+        # billions of elements: N(0, 0.02) drawn in HBM by torch's seeded generator
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        for v in views:
+            tmp = torch.empty(v.numel(), dtype=torch.float32, device=dev)
+            tmp.normal_(0.0, 0.02, generator=g)
+            v.copy_(tmp)
+            del tmp
     if args.probe == "copy":
         copy_probe(torch, flat, args)
         return
@@ -134,10 +145,13 @@ def main():
     total_steps = args.warmup + args.steps
     proj = [synth.projected_grads(K, seed=1000 + t) for t in range(total_steps)]
     seeds_t = [synth.seeds(w.machines, w.samples_per_machine, step=t) for t in range(total_steps)]
+    t_log = w.T if w.T > 0 else T_REPLAY
     log = [(synth.seeds(w.machines, w.samples_per_machine, step=10_000 + t),
-            synth.grads_int8(K, "uniform", seed=2000 + t), lr) for t in range(T_REPLAY)]
-    recs = {"perturb": 1, "update": K, "replay": T_REPLAY * K}
-    calls = ["perturb", "perturb", "perturb", "update", "replay"]
+            synth.grads_int8(K, "uniform", seed=2000 + t), lr) for t in range(t_log)]
+    recs = {"perturb": 1, "update": K, "replay": t_log * K}
+    # a replay workload's step is the catch-up alone; otherwise one iteration
+    # of Algorithm 1 on this machine plus a short catch-up
+    calls = ["replay"] if w.T > 0 else ["perturb", "perturb", "perturb", "update", "replay"]
     ps_per_step = N * sum(recs[c] for c in calls)
 
     stream = torch.cuda.current_stream()
@@ -153,15 +167,16 @@ def main():
                 marks.append(e)
 
         mark()
-        ps.perturb(s, eps)
-        mark()
-        ps.perturb(s, -2 * eps)
-        mark()
-        ps.perturb(s, eps)
-        mark()
-        q = mezo.quantize_projgrad(proj[t])
-        ps.update_multi(seeds_t[t], q, lr)
-        mark()
+        if w.T == 0:
+            ps.perturb(s, eps)
+            mark()
+            ps.perturb(s, -2 * eps)
+            mark()
+            ps.perturb(s, eps)
+            mark()
+            q = mezo.quantize_projgrad(proj[t])
+            ps.update_multi(seeds_t[t], q, lr)
+            mark()
         ps.replay(log)
         mark()
         if ev is not None:
@@ -191,7 +206,7 @@ def main():
     for t in range(args.warmup, total_steps):
         step(t, marks_all)
     torch.cuda.synchronize()
-    per_call = {c: [] for c in recs}
+    per_call = {c: [] for c in calls}
     for marks in marks_all:
         for c, a, b in zip(calls, marks[:-1], marks[1:]):
             per_call[c].append(a.elapsed_time(b))
@@ -211,7 +226,7 @@ def main():
     peak = VALU_LANE_INSTR_PER_S / 1e12
     costs = issue_costs()
     ops = {}
-    for c in recs:
+    for c in launch_ms:
         t_s = launch_ms[c] / 1e3
         ops[c] = {"records": recs[c], "ms": round(launch_ms[c], 4),
                   "param_seeds_per_s": N * recs[c] / t_s,
@@ -232,16 +247,18 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if w.dtype == "f32" else "bf16",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {N} {w.dtype} params in {w.n_tensors} tensors, "
-                               f"K={K}; step = perturb +eps,-2eps,+eps; quantize {K} grads; "
-                               f"update_multi K={K}; replay T={T_REPLAY}xK={K}",
-                   "params": N, "tensors": w.n_tensors, "K": K, "replay_T": T_REPLAY,
+        "config": {"workload": f"{w.name}: {N} {w.dtype} params in {w.n_tensors} tensors, K={K}; "
+                               + (f"step = replay T={t_log}xK={K}" if w.T > 0 else
+                                  f"step = perturb +eps,-2eps,+eps; quantize {K} grads; "
+                                  f"update_multi K={K}; replay T={t_log}xK={K}"),
+                   "params": N, "tensors": w.n_tensors, "K": K, "replay_T": t_log,
                    "eps": eps, "lr": lr, "param_seeds_per_step": ps_per_step},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak,
                      "unit": "Tinstr/s", "frac": achieved / peak,
-                     "traffic": measured_traffic(bytes_per_launch),
+                     "traffic": measured_traffic(w.name),
                      "alg_bytes_per_launch": bytes_per_launch,
-                     "kernel": "engine_kernel<inline records, f32>",
+                     "kernel": f"engine_kernel<{'inline' if max(recs[c] for c in calls) <= 32 else 'staged'}"
+                               f" records, {w.dtype}>",
                      "instr_per_param_seed": INSTR_PER_PARAM_SEED,
                      "param_seeds_per_launch": ps_per_launch,
                      "avg_launch_ms": kernel_ms / n_launch,
@@ -250,7 +267,7 @@ def main():
         "ops": ops,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, recs, calls, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, recs, calls, log, args.cpu_seconds)
     print(json.dumps(out))
 
 
@@ -284,11 +301,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(n_launch_bytes: float):
-    """HBM bytes per engine launch from the committed counter profile, or None
-    when there is none or the kernel sources changed since it was taken."""
+def measured_traffic(workload: str):
+    """HBM bytes per engine launch from the committed counter profile of this
+    workload, or None when there is none or the kernel sources changed since
+    it was taken."""
     try:
-        with open(TRAFFIC_PROFILE) as f:
+        with open(TRAFFIC_PROFILE.format(workload=workload)) as f:
             prof = json.load(f)
     except (OSError, ValueError):
         return None
@@ -319,33 +337,34 @@ def copy_probe(torch, flat, args):
                       "hbm_frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 
 
-def cpu_baseline(w, recs, calls, target_s):
+def cpu_baseline(w, recs, calls, log, target_s):
     """The oracle, as it stands, on a bounded element sample of the same step:
-    all tensors' first elements, sized to about `target_s` of CPU time."""
+    the first elements of tensor 0, sized to about `target_s` of CPU time."""
     import oracle
     from paper_2306_10015_amd import synth
     n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     n_threads = min(n_threads, 16)
     oracle.set_threads(n_threads)
-    K = w.K
     seeds = synth.seeds(w.machines, w.samples_per_machine, step=0)
-    q = synth.grads_int8(K, "uniform", seed=1)
-    log = [(synth.seeds(w.machines, w.samples_per_machine, step=10_000 + t),
-            synth.grads_int8(K, "uniform", seed=2000 + t), w.lr) for t in range(T_REPLAY)]
+    q = synth.grads_int8(w.K, "uniform", seed=1)
     seeds_per_elem = sum(recs[c] for c in calls)
 
     def run(n):
         th = synth.theta0_tensor((n,), w.dtype, 0, 0)
         t0 = time.perf_counter()
-        oracle.perturb(th, 0, (0, 0, 0), w.eps)
-        oracle.perturb(th, 0, (0, 0, 0), -2 * w.eps)
-        oracle.perturb(th, 0, (0, 0, 0), w.eps)
-        oracle.update(th, 0, seeds, q, w.lr)
+        if w.T == 0:
+            oracle.perturb(th, 0, (0, 0, 0), w.eps)
+            oracle.perturb(th, 0, (0, 0, 0), -2 * w.eps)
+            oracle.perturb(th, 0, (0, 0, 0), w.eps)
+            oracle.update(th, 0, seeds, q, w.lr)
         oracle.replay(th, 0, log)
         return time.perf_counter() - t0
 
-    n = 1 << 14
+    n = 1 << 10
     dt = run(n)
+    while dt < 0.5 and n < w.numel:
+        n *= 4
+        dt = run(n)
     n_full = int(min(max(n * target_s / max(dt, 1e-6), n), w.numel))
     dt = run(n_full)
     return {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,

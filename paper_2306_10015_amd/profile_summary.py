@@ -1,7 +1,7 @@
 """Summarise rocprofv3 CSV output of the engine into the short text files kept
 under profiles/ (measurement tooling; not used by the engine).
 
-    python -m paper_2306_10015_amd.profile_summary --name engine_kernel_opt125m_f32 \\
+    python -m paper_2306_10015_amd.profile_summary --name engine_kernel_opt125m \\
         --trace gpurun_out/prof_trace --fetch gpurun_out/prof_fetch \\
         --write gpurun_out/prof_write --copy-fetch gpurun_out/prof_copy_fetch \\
         --copy-write gpurun_out/prof_copy_write --valu gpurun_out/prof_valu \\

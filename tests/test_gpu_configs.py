@@ -1,0 +1,112 @@
+"""GPU parity at full size, in the launch configuration bench.py times, on
+sampled outputs the oracle computes one by one: the first and last elements of
+every tensor plus random 4-aligned blocks. Workloads: the OPT-125m-shaped fp32
+set (K = 8), the 1.3B-shaped bf16 set (K = 16), the 6.7B-shaped bf16 set
+(K = 64) and the late-joiner replay on the 1.3B set (T = 200 steps of K = 32).
+theta0 is N(0, 0.02), drawn in HBM by torch's seeded device generator; the
+oracle is fed the values read back at the sampled elements.
+"""
+import numpy as np
+import pytest
+
+from paper_2306_10015_amd import synth
+from gpu_util import assert_theta_close, bf16_ulp_distance, theta_on_device, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def mz():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    from paper_2306_10015_amd import mezo
+    return mezo
+
+
+def gather(torch, tensors, idx):
+    out = []
+    for t, ix in zip(tensors, idx):
+        sel = t.index_select(0, torch.from_numpy(ix.astype(np.int64)).cuda())
+        out.append(to_host(sel))
+    return out
+
+
+def sample_all(w, edge, blocks, seed=2):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return [synth.sample_indices(int(np.prod(s)), rng, edge=edge, blocks=blocks) for _, s in w.shapes]
+
+
+def check_op(torch, orc, tensors, idx, gpu_op, oracle_op, what):
+    before = gather(torch, tensors, idx)
+    gpu_op()
+    torch.cuda.synchronize()
+    after = gather(torch, tensors, idx)
+    worst, n_cancel = None, 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        ref = oracle_op(b.copy(), tid, ix)
+        s = assert_theta_close(a, ref, f"{what} tensor {tid}", inp=b)
+        n_cancel += s.get("cancelled_gt1ulp", 0)
+        worst = s
+    print(f"{what}: last tensor {worst}, cancellations beyond 1 ulp: {n_cancel}")
+
+
+def workload_q(w, step=0):
+    return synth.grads_int8(w.K, w.grad_kind, seed=1 + step)
+
+
+@pytest.mark.parametrize("name", ["opt125m", "opt1.3b", "opt6.7b"])
+def test_full_size_perturb_and_update(mz, orc, name):
+    import torch
+    w = synth.WORKLOADS[name]
+    tensors = theta_on_device(w, seed=0, device_rng=True)
+    ps = mz.ParamSet(tensors)
+    idx = sample_all(w, edge=1024, blocks=32)
+    s = (0, 0, 0)
+    check_op(torch, orc, tensors, idx, lambda: ps.perturb(s, w.eps),
+             lambda th, tid, ix: orc.perturb(th, tid, s, w.eps, idx=ix), f"{name} perturb +eps")
+    seeds = synth.workload_seeds(w)
+    q = workload_q(w)
+    check_op(torch, orc, tensors, idx, lambda: ps.update_multi(seeds, q, w.lr),
+             lambda th, tid, ix: orc.update(th, tid, seeds, q, w.lr, idx=ix), f"{name} update K={w.K}")
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
+
+
+def test_full_size_replay_1p3b(mz, orc):
+    """T = 200 logged steps of K = 32 seeds (4 machines x 8 samples) on the
+    1.3B bf16 set, against the oracle's step-by-step replay."""
+    import torch
+    w = synth.WORKLOADS["replay1.3b"]
+    tensors = theta_on_device(w, seed=0, device_rng=True)
+    ps = mz.ParamSet(tensors)
+    idx = sample_all(w, edge=48, blocks=8)
+    before = gather(torch, tensors, idx)
+    steps = [(synth.seeds(w.machines, w.samples_per_machine, step=t),
+              synth.grads_int8(w.K, "uniform", seed=500 + t), w.lr) for t in range(w.T)]
+    ps.replay(steps)
+    torch.cuda.synchronize()
+    after = gather(torch, tensors, idx)
+    hist = np.zeros(8, dtype=np.int64)
+    changed = 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        ref = orc.replay(b.copy(), tid, steps, idx=ix)
+        d = bf16_ulp_distance(a, ref)
+        hist += np.bincount(np.minimum(d, 7), minlength=8)
+        changed += int(np.sum(ref != b))
+        far = d > 1
+        if far.any():
+            # only where the value passed through zero (cancellation) may the
+            # distance exceed one ulp of the result; bound it at operand scale
+            from gpu_util import bf16_ulp_of
+            g = synth.bf16_bits_to_fp32(a[far]).astype(np.float64)
+            r = synth.bf16_bits_to_fp32(ref[far]).astype(np.float64)
+            i = synth.bf16_bits_to_fp32(b[far]).astype(np.float64)
+            assert np.all(np.abs(g - r) <= bf16_ulp_of(np.maximum(np.abs(i), np.abs(r)))), \
+                f"tensor {tid}: replay off by more than an operand-scale ulp"
+    print(f"replay T={w.T} K={w.K}: sampled {hist.sum()} elements, {changed} changed by the "
+          f"oracle's replay; ulp distance histogram {hist.tolist()}")
+    assert hist[0] / hist.sum() > 0.999
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
