@@ -48,15 +48,16 @@ HBM_PEAK_GBS = 8000.0
 #: inner loop, the method's minimal sequence on gfx950: round 1 and the
 #: element-independent half of round 2 hoisted out of the seed loop; rounds
 #: 2..10 cost 17 wide multiplies (v_mad_u64_u32), 16 three-way xors
-#: (v_bitop3_b32) and 3 xors; Box-Muller per pair of Gaussians: 2 shifts, 2
-#: int->float conversions, one fma forming u1, 4 muls, log2, sqrt, sin, cos;
-#: and one fma per Gaussian accumulating c_k * z.
+#: (v_bitop3_b32) and 3 xors; Box-Muller per pair of Gaussians (radius factor
+#: sqrt(2 ln 2) folded into the coefficient): 2 shifts, 2 int->float
+#: conversions, one fma forming u1, 3 muls, log2, sqrt, sin, cos; and one fma
+#: per Gaussian accumulating c_k * z.
 INNER_LOOP_MIX = {
     "v_mad_u64_u32": 17, "v_bitop3_b32": 16, "v_xor_b32": 3, "v_lshrrev_b32": 4,
-    "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 8, "v_log_f32": 2, "v_sqrt_f32": 2,
+    "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 6, "v_log_f32": 2, "v_sqrt_f32": 2,
     "v_sin_f32": 2, "v_cos_f32": 2, "v_fmac_f32": 4,
 }
-#: lane-instructions per param-seed (= 66 / 4)
+#: lane-instructions per param-seed (= 64 / 4)
 INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
 
 #: counter profile of the engine kernel on this workload (FETCH_SIZE /

@@ -32,8 +32,10 @@
  * the GPU's transcendental instructions (absolute error below 1e-6 * max|z|).
  *
  * Arithmetic. theta is loaded into fp32 (bf16 exactly), the perturbations are
- * accumulated in fp32 as acc = fma(c_k, z_k, acc) for k ascending, and
- * theta' = round(theta + acc) to the storage type, round-to-nearest-even;
+ * accumulated in fp32 for k ascending as acc = fma(c'_k, y_k, acc), where
+ * y_k = z_k / sqrt(2 ln 2) (the constant factor of Box-Muller's radius is
+ * taken out of the per-element work) and c'_k = fl32(c_k * sqrt(2 ln 2));
+ * then theta' = round(theta + acc) to the storage type, round-to-nearest-even;
  * subnormals are kept.
  *
  * Errors. Every int-returning call returns MEZO_OK (0) or a negative MEZO_E*
@@ -164,7 +166,7 @@ MEZO_API uint64_t mezo_paramset_numel(mezo_paramset_t ps);
 MEZO_API int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream);
 
 /* The apply loop of one iteration — Algorithm 1 and Section 2: in
- * machine-timestamp order, perturb by -grad_k * lr with seed_k. Fused: for
+ * machine/timestamp order, perturb by -grad_k * lr with seed_k. Fused: for
  * every element, acc = sum_k c_k z(seed_k) with c_k = fl32(-lr * g~_k)
  * (g~_k = the codec's decoding of q[k]), then theta <- round(theta + acc);
  * each element is read and written once for all K seeds.

@@ -186,8 +186,8 @@ static void store_theta(void* theta, int dtype, uint64_t i, double v)
 }
 
 /* ------------------------------------------------------------------------ */
-/* One-byte projected gradient (Section 3, "Training Speed": the signed log  */
-/* of the gradient clipped to +-127; the linear int8 code is the other      */
+/* One-byte projected gradient (Section 3: a signed log of the gradient,    */
+/* clipped to +-127; the linear int8 code is the other                      */
 /* codec the engine accepts). The range is the closed [-127, 127]; -128 is  */
 /* never produced and rejected on input; rounding ties go to even.          */
 /* ------------------------------------------------------------------------ */
@@ -195,7 +195,7 @@ static void store_theta(void* theta, int dtype, uint64_t i, double v)
 /* The signed-log code must decode every q to a finite fp32 value: the largest
  * code, 127, decodes to exp(127/alpha) - 1, which needs alpha >= ~1.4314. The
  * default alpha = 1/ln 2 (a base-2 log) puts the clip at 127 just inside the
- * fp32 range, the reading taken of "clipped to (-127, 127)". */
+ * fp32 range: the reading taken of the paper's clip at +-127. */
 static int codec_ok(int kind, float scale, float alpha)
 {
     if (kind == ORC_CODEC_LINEAR) return isfinite(scale) && scale > 0.0f;

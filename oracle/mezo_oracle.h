@@ -13,11 +13,10 @@
  *    add eps*z to it.
  *  - the perturb / evaluate triple +eps, -2eps, +eps (Algorithm 1, inner
  *    inference loop);
- *  - the apply loop (Algorithm 1, after GetGradients; Section 2 "Applying
- *    collected scalar projected gradients"): in machine-timestamp order,
- *    perturb with weight -grad * eta / numel(all_grads) and the same seed;
- *  - the one-byte gradient (Section 3, "Training Speed": signed log clipped to
- *    +-127);
+ *  - the apply loop (Algorithm 1, after GetGradients; Section 2): ordered by
+ *    machine timestamp, perturb with weight -grad * eta / numel(all_grads)
+ *    and the same seed;
+ *  - the one-byte gradient (Section 3: a signed log, clipped to +-127);
  *  - late-joiner catch-up (Appendix B): apply every logged projected gradient
  *    of the missed iterations.
  *

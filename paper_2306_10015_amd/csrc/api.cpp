@@ -84,7 +84,7 @@ mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last)
     const uint64_t p = uint64_t(mezo::kMulB) * uint64_t(s.sample);
     r.mb_hi = static_cast<uint32_t>(p >> 32);
     r.mb_lo = static_cast<uint32_t>(p);
-    r.coef = coef;
+    r.coef = static_cast<float>(double(coef) * mezo::kZScaleF64);
     r.last = last ? 1u : 0u;
     r.sample = s.sample;
     return r;

@@ -106,30 +106,47 @@ __device__ __forceinline__ void philox_words(const SeedUniform& u, BlockPre b, u
 // ---- Box-Muller -----------------------------------------------------------
 // Box & Muller (1958). u1 = ((w_a >> 8) + 1) 2^-24 in (0, 1] and
 // u2 = (w_b >> 8) 2^-24 in [0, 1) are exact in fp32. v_log_f32 is log2, so
-// -2 ln u1 = (-2 ln 2) log2 u1; v_sin_f32 / v_cos_f32 take revolutions, so
-// sin(2 pi u2) needs no multiply by 2 pi.
+// sqrt(-2 ln u1) = sqrt(2 ln 2) sqrt(-log2 u1); v_sin_f32 / v_cos_f32 take
+// revolutions, so sin(2 pi u2) needs no multiply by 2 pi.
+//
+// gauss4_unit returns z / sqrt(2 ln 2): the constant factor is left to the
+// caller, which folds it into the record's coefficient (one multiply per
+// record on the host instead of two per Gaussian pair on the device).
 struct Z4 {
     float z0, z1, z2, z3;
 };
 
-__device__ __forceinline__ void box_muller_pair(uint32_t wa, uint32_t wb, float& zc, float& zs)
+// sqrt(2 ln 2): z = kZScale * (the unit-scaled value below).
+constexpr float kZScale = 1.17741002251547469101f;
+
+__device__ __forceinline__ void box_muller_pair_unit(uint32_t wa, uint32_t wb, float& zc, float& zs)
 {
     constexpr float kTwoM24 = 0x1p-24f;
-    constexpr float kMinusTwoLn2 = -1.38629436111989061883f;
     // (t + 1) 2^-24 as one fma: t < 2^24, so the product, the sum and the
     // result are exact.
-    float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
-    float u2 = float(wb >> 8) * kTwoM24;
-    float r = __builtin_amdgcn_sqrtf(kMinusTwoLn2 * __builtin_amdgcn_logf(u1));
+    const float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
+    const float u2 = float(wb >> 8) * kTwoM24;
+    const float r = __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1));
     zc = r * __builtin_amdgcn_cosf(u2);
     zs = r * __builtin_amdgcn_sinf(u2);
 }
 
-__device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+__device__ __forceinline__ Z4 gauss4_unit(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
 {
     Z4 z;
-    box_muller_pair(w0, w1, z.z0, z.z1);
-    box_muller_pair(w2, w3, z.z2, z.z3);
+    box_muller_pair_unit(w0, w1, z.z0, z.z1);
+    box_muller_pair_unit(w2, w3, z.z2, z.z3);
+    return z;
+}
+
+// The four Gaussians themselves (inspection path).
+__device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+{
+    Z4 z = gauss4_unit(w0, w1, w2, w3);
+    z.z0 *= kZScale;
+    z.z1 *= kZScale;
+    z.z2 *= kZScale;
+    z.z3 *= kZScale;
     return z;
 }
 

@@ -130,7 +130,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
         for (int g = 0; g < kGroups; ++g) {
             uint32_t w0, w1, w2, w3;
             philox_words(u, pre[g], w0, w1, w2, w3);
-            const Z4 z = gauss4(w0, w1, w2, w3);
+            const Z4 z = gauss4_unit(w0, w1, w2, w3);
             acc[g][0] = __builtin_fmaf(c, z.z0, acc[g][0]);
             acc[g][1] = __builtin_fmaf(c, z.z1, acc[g][1]);
             acc[g][2] = __builtin_fmaf(c, z.z2, acc[g][2]);
@@ -210,7 +210,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
             for (int h = 0; h < 2; ++h) {
                 uint32_t w0, w1, w2, w3;
                 philox_words(u, pre[g][h], w0, w1, w2, w3);
-                const Z4 z = gauss4(w0, w1, w2, w3);
+                const Z4 z = gauss4_unit(w0, w1, w2, w3);
                 acc[g][4 * h + 0] = __builtin_fmaf(c, z.z0, acc[g][4 * h + 0]);
                 acc[g][4 * h + 1] = __builtin_fmaf(c, z.z1, acc[g][4 * h + 1]);
                 acc[g][4 * h + 2] = __builtin_fmaf(c, z.z2, acc[g][4 * h + 2]);

@@ -15,7 +15,8 @@ struct alignas(16) SeedRec {
     uint32_t step;    // counter word 3
     uint32_t mb_hi;   // high word of kMulB * sample (round 1, counter word 2)
     uint32_t mb_lo;   // low word  of kMulB * sample
-    float    coef;    // weight c of z in theta += c * z
+    float    coef;    // fl32(c * sqrt(2 ln 2)): the weight c of z in theta += c * z,
+                      // pre-multiplied by the constant the kernel leaves out of z
     uint32_t last;    // 1: round to storage after this record (end of a step)
     uint32_t sample;  // counter word 2 (inspection only)
 };
@@ -55,5 +56,9 @@ constexpr uint32_t kMulA = 0xD2511F53u;
 constexpr uint32_t kMulB = 0xCD9E8D57u;
 constexpr uint32_t kWeylA = 0x9E3779B9u;
 constexpr uint32_t kWeylB = 0xBB67AE85u;
+
+// sqrt(2 ln 2) in double: the engine kernels produce z / sqrt(2 ln 2) and the
+// host folds the factor into every record's coefficient.
+constexpr double kZScaleF64 = 1.17741002251547469101;
 
 }  // namespace mezo

@@ -218,14 +218,21 @@ def test_replay_matches_oracle_and_sequential_updates(mz, orc, dtype):
 
 def test_replay_long_log_staged(mz, orc):
     """More records than fit in the kernel arguments (staged buffer), reused
-    across calls on the same paramset."""
+    across six calls on the same paramset: bit-identical to the same steps
+    applied one update_multi call at a time (records in the kernel arguments),
+    each of which is checked against the oracle on its own input."""
     hosts = [synth.theta0_tensor((3001,), synth.BF16, 0, 4)]
     devs, ps = make_set(mz, hosts)
+    devs_seq, ps_seq = make_set(mz, hosts)
     for call in range(6):
         steps = [(synth.seeds(4, 4, step=100 * call + t), synth.grads_int8(16, seed=call * 10 + t),
                   5e-3) for t in range(5)]
-        step_and_check(devs, [0], lambda: ps.replay(steps),
-                       lambda th, tid: orc.replay(th, tid, steps), f"staged replay {call}")
+        ps.replay(steps)
+        for t, (s, q, lr) in enumerate(steps):
+            step_and_check(devs_seq, [0], lambda: ps_seq.update_multi(s, q, lr),
+                           lambda th, tid: orc.update(th, tid, s, q, lr), f"call {call} step {t}")
+    sync()
+    assert np.array_equal(to_host(devs[0]), to_host(devs_seq[0]))
 
 
 @pytest.mark.parametrize("case", ["lr0", "q0", "K0", "scale0"])
