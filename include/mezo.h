@@ -184,6 +184,24 @@ MEZO_API int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, con
 MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T,
                 const mezo_codec_t* codec, void* stream);
 
+/* Out of place (the weight restore of Algorithm 1 fused into the sweep; it
+ * also removes the perturb/restore drift Section 2 mentions): read every
+ * tensor of src, write the corresponding tensor of dst, in one pass.
+ *   mezo_perturb_from:      theta_dst = round(theta_src + scale * z(seed))
+ *   mezo_update_multi_from: theta_dst = round(theta_src + sum_k c_k z(seed_k))
+ * src is left unchanged. dst and src must describe the same tensors in the
+ * same order (per storage type: numel and tensor_id; else MEZO_EINVAL) and
+ * share no memory except where a tensor is its own source (MEZO_EOVERLAP);
+ * src == dst is the in-place call. Arguments are checked as for the in-place
+ * calls. Unlike those, zero weights still enqueue one pass: theta_dst =
+ * theta_src (a copy). src's device tables are created on first use, on the
+ * same device as dst's. */
+MEZO_API int mezo_perturb_from(mezo_paramset_t dst, mezo_paramset_t src, mezo_seed_t seed,
+                               float scale, void* stream);
+MEZO_API int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src,
+                                    const mezo_seed_t* seeds, const int8_t* q, uint32_t K,
+                                    const mezo_codec_t* codec, float lr, void* stream);
+
 /* ---- the one-byte gradient (host, pure) ------------------------------- */
 
 /* Projected gradient g = (l+ - l-) / (2 eps) -> q (Section 3). ±inf clip to

@@ -10,6 +10,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "../../include/mezo.h"
@@ -188,11 +189,22 @@ int ensure_device(mezo_paramset* ps)
     return MEZO_OK;
 }
 
-int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hipStream_t stream)
+// Enqueue the engine over every storage type of ps. With src (same layout),
+// read src and write ps; that launch is made even with no records (a copy).
+int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hipStream_t stream,
+                   mezo_paramset* src = nullptr)
 {
-    if (recs.empty()) return MEZO_OK;
+    if (recs.empty() && !src) return MEZO_OK;
     int rc = ensure_device(ps);
     if (rc) return rc;
+    if (src && src != ps) {
+        rc = ensure_device(src);
+        if (rc) return rc;
+        if (src->device != ps->device) {
+            t_last_error = "source and destination paramsets live on different devices";
+            return MEZO_EINVAL;
+        }
+    }
     mezo::EngineArgs args;
     std::memset(&args, 0, sizeof(args));
     args.n_rec = static_cast<uint32_t>(recs.size());
@@ -225,12 +237,41 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
         if (ps->table[dt].empty()) continue;
         args.tensors = ps->d_table[dt];
         args.tile_tensor = ps->d_tile_tensor[dt];
+        args.src_tensors = src ? src->d_table[dt] : nullptr;
         args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
         args.total_tiles = ps->total_tiles[dt];
         MEZO_HIP(mezo::launch_engine(args, dt, stream));
     }
     if (slot) MEZO_HIP(hipEventRecord(slot->done, stream));
     MEZO_HIP(hipEventRecord(ps->last, stream));
+    if (src && src != ps) MEZO_HIP(hipEventRecord(src->last, stream));
+    return MEZO_OK;
+}
+
+// dst and src describe the same tensors (count, ids, sizes, storage types, in
+// registration order per storage type) and share no memory except where a
+// tensor is its own source.
+int check_pair(const mezo_paramset* dst, const mezo_paramset* src)
+{
+    if (dst == src) return MEZO_OK;
+    std::vector<std::tuple<uint64_t, uint64_t>> spans;
+    for (int dt = 0; dt < 2; ++dt) {
+        const auto& a = dst->table[dt];
+        const auto& b = src->table[dt];
+        if (a.size() != b.size()) return MEZO_EINVAL;
+        const uint64_t esz = dt == 0 ? 4 : 2;
+        for (size_t i = 0; i < a.size(); ++i) {
+            if (a[i].numel != b[i].numel || a[i].tensor_id != b[i].tensor_id) return MEZO_EINVAL;
+            spans.emplace_back(a[i].data, a[i].data + a[i].numel * esz);
+            if (b[i].data != a[i].data) spans.emplace_back(b[i].data, b[i].data + b[i].numel * esz);
+        }
+    }
+    std::sort(spans.begin(), spans.end());
+    uint64_t reach = 0;
+    for (const auto& sp : spans) {
+        if (std::get<0>(sp) < reach) return MEZO_EOVERLAP;
+        reach = std::max(reach, std::get<1>(sp));
+    }
     return MEZO_OK;
 }
 
@@ -332,6 +373,41 @@ int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t
     if (rc) return rc;
     std::lock_guard<std::mutex> lock(ps->mu);
     return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+}
+
+int mezo_perturb_from(mezo_paramset_t dst, mezo_paramset_t src, mezo_seed_t seed, float scale,
+                      void* stream)
+{
+    if (!dst || !src) return MEZO_EINVAL;
+    if (!std::isfinite(scale)) return MEZO_ERANGE;
+    int rc = check_pair(dst, src);
+    if (rc) return rc;
+    std::vector<mezo::SeedRec> recs;
+    if (scale != 0.0f) recs.push_back(make_rec(seed, scale, true));
+    if (dst == src) {
+        std::lock_guard<std::mutex> lock(dst->mu);
+        return launch_records(dst, recs, static_cast<hipStream_t>(stream));
+    }
+    std::scoped_lock lock(dst->mu, src->mu);
+    return launch_records(dst, recs, static_cast<hipStream_t>(stream), src);
+}
+
+int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src, const mezo_seed_t* seeds,
+                           const int8_t* q, uint32_t K, const mezo_codec_t* codec, float lr, void* stream)
+{
+    if (!dst || !src) return MEZO_EINVAL;
+    std::vector<mezo::SeedRec> recs;
+    recs.reserve(K);
+    int rc = append_step(seeds, q, K, codec, lr, recs);
+    if (rc) return rc;
+    rc = check_pair(dst, src);
+    if (rc) return rc;
+    if (dst == src) {
+        std::lock_guard<std::mutex> lock(dst->mu);
+        return launch_records(dst, recs, static_cast<hipStream_t>(stream));
+    }
+    std::scoped_lock lock(dst->mu, src->mu);
+    return launch_records(dst, recs, static_cast<hipStream_t>(stream), src);
 }
 
 int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const mezo_codec_t* codec,

@@ -6,6 +6,9 @@
 // of records, each step's last flagged). Every element is read once and
 // written once; its noise is regenerated in registers for every record.
 //
+// In place, or out of place from a source set of the same layout (theta =
+// backup + sum c z: the restore of Algorithm 1 fused into the update).
+//
 // Launch shape: one launch per storage type, one workgroup per 2048-element
 // tile; the workgroup finds its tensor with two scalar loads (tile -> tensor
 // index -> descriptor). theta streams through with non-temporal 16-byte loads
@@ -76,7 +79,7 @@ __device__ __forceinline__ void store_stream(uint64_t addr, uint4 v)
 }
 
 template <uint32_t kDtype>
-__device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t tile,
+__device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t src, uint64_t tile,
                                           TileRaw<Layout<kDtype>::kGroups>& raw)
 {
     constexpr int kGroups = Layout<kDtype>::kGroups;
@@ -84,7 +87,7 @@ __device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t tile,
     for (int g = 0; g < kGroups; ++g) {
         const uint64_t grp = group_index<kGroups>(tile, g);
         if ((grp + 1) * Layout<kDtype>::kPerGroup <= d.numel)
-            raw.g[g] = load_stream(d.data + grp * 16);
+            raw.g[g] = load_stream(src + grp * 16);
         else
             raw.g[g] = make_uint4(0u, 0u, 0u, 0u);
     }
@@ -93,11 +96,12 @@ __device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t tile,
 // One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
 // (one Philox block each).
 template <bool kInline>
-__device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& d, uint64_t tile,
-                                         const TileRaw<kGroupsF32>& raw)
+__device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& d, uint64_t src,
+                                         uint64_t tile, const TileRaw<kGroupsF32>& raw)
 {
     constexpr int kGroups = kGroupsF32;
-    gfloat_t* __restrict__ base = reinterpret_cast<gfloat_t*>(d.data);
+    const gfloat_t* in = reinterpret_cast<const gfloat_t*>(src);
+    gfloat_t* out = reinterpret_cast<gfloat_t*>(d.data);
     const uint64_t numel = d.numel;
     float th[kGroups][4];
     float acc[kGroups][4];
@@ -115,7 +119,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
             th[g][3] = __uint_as_float(raw.g[g].w);
         } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) th[g][j] = (e0[g] + j < numel) ? base[e0[g] + j] : 0.0f;
+            for (int j = 0; j < 4; ++j) th[g][j] = (e0[g] + j < numel) ? in[e0[g] + j] : 0.0f;
         }
         pre[g] = block_pre(uint32_t(grp));
 #pragma unroll
@@ -155,7 +159,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
         } else {
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                if (e0[g] + j < numel) base[e0[g] + j] = th[g][j];
+                if (e0[g] + j < numel) out[e0[g] + j] = th[g][j];
         }
     }
 }
@@ -164,11 +168,12 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
 // Philox blocks each). theta is held as fp32 holding a bf16 value; a step ends
 // with one RNE rounding back to bf16.
 template <bool kInline>
-__device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t tile,
-                                          const TileRaw<kGroupsBF16>& raw)
+__device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t src,
+                                          uint64_t tile, const TileRaw<kGroupsBF16>& raw)
 {
     constexpr int kGroups = kGroupsBF16;
-    gu16_t* __restrict__ base = reinterpret_cast<gu16_t*>(d.data);
+    const gu16_t* in = reinterpret_cast<const gu16_t*>(src);
+    gu16_t* out = reinterpret_cast<gu16_t*>(d.data);
     const uint64_t numel = d.numel;
     float th[kGroups][8];
     float acc[kGroups][8];
@@ -192,7 +197,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                th[g][j] = (e0[g] + j < numel) ? __uint_as_float(uint32_t(base[e0[g] + j]) << 16) : 0.0f;
+                th[g][j] = (e0[g] + j < numel) ? __uint_as_float(uint32_t(in[e0[g] + j]) << 16) : 0.0f;
         }
         pre[g][0] = block_pre(uint32_t(2 * grp));
         pre[g][1] = block_pre(uint32_t(2 * grp + 1));
@@ -242,7 +247,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if (e0[g] + j < numel) base[e0[g] + j] = to_bf16(th[g][j]);
+                if (e0[g] + j < numel) out[e0[g] + j] = to_bf16(th[g][j]);
         }
     }
 }
@@ -251,13 +256,16 @@ template <bool kInline, uint32_t kDtype>
 __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
-    const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+    const uint32_t ti = a.tile_tensor[tile];
+    const TensorDesc d = a.tensors[ti];
+    // out of place: read tensor ti of the source set (same layout), write d
+    const uint64_t src = a.src_tensors ? a.src_tensors[ti].data : d.data;
     TileRaw<Layout<kDtype>::kGroups> raw;
-    load_tile<kDtype>(d, tile - d.tile_begin, raw);
+    load_tile<kDtype>(d, src, tile - d.tile_begin, raw);
     if constexpr (kDtype == kF32)
-        tile_f32<kInline>(a, d, tile - d.tile_begin, raw);
+        tile_f32<kInline>(a, d, src, tile - d.tile_begin, raw);
     else
-        tile_bf16<kInline>(a, d, tile - d.tile_begin, raw);
+        tile_bf16<kInline>(a, d, src, tile - d.tile_begin, raw);
 }
 
 // Inspection: RNG words and Gaussians of a range of elements, one Philox

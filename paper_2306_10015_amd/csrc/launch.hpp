@@ -15,6 +15,7 @@ namespace mezo {
 struct EngineArgs {
     const TensorDesc* tensors;     // device table of one storage type, tile_begin ascending
     const uint32_t* tile_tensor;   // device: index into tensors of every tile
+    const TensorDesc* src_tensors; // device table to read from (same layout), or null: in place
     uint64_t total_tiles;
     const SeedRec* ext;         // device records when n_rec > kInlineRecs
     uint32_t n_tensors;

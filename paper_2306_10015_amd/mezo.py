@@ -57,7 +57,8 @@ class Step(ctypes.Structure):
 
 #: Every symbol include/mezo.h declares.
 EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
-           "mezo_perturb", "mezo_update_multi", "mezo_replay", "quantize_projgrad",
+           "mezo_perturb", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
+           "mezo_update_multi_from", "quantize_projgrad",
            "mezo_dequantize", "mezo_debug_generate", "mezo_strerror", "mezo_last_error",
            "mezo_version")
 
@@ -85,6 +86,10 @@ def _load() -> ctypes.CDLL:
     L.mezo_update_multi.restype = i32
     L.mezo_replay.argtypes = [vp, ctypes.POINTER(Step), u32, ctypes.POINTER(Codec), vp]
     L.mezo_replay.restype = i32
+    L.mezo_perturb_from.argtypes = [vp, vp, Seed, f32, vp]
+    L.mezo_perturb_from.restype = i32
+    L.mezo_update_multi_from.argtypes = [vp, vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
+    L.mezo_update_multi_from.restype = i32
     L.quantize_projgrad.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
     L.quantize_projgrad.restype = i32
     L.mezo_dequantize.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
@@ -215,6 +220,23 @@ class ParamSet:
         _check(lib.mezo_update_multi(self._h, sa.ctypes.data, qa.ctypes.data, sa.size,
                                      ctypes.byref(codec_), float(lr), _stream_ptr(stream)),
                "mezo_update_multi")
+
+    def perturb_from(self, src: "ParamSet", seed, scale: float, stream=None) -> None:
+        """theta = theta_src + scale * z(seed), src unchanged (out of place)."""
+        _check(lib.mezo_perturb_from(self._h, src.handle, _seed(seed), float(scale),
+                                     _stream_ptr(stream)), "mezo_perturb_from")
+
+    def update_multi_from(self, src: "ParamSet", seeds, q, lr: float,
+                          codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
+        """theta = theta_src - lr * sum_k deq(q_k) z(seed_k): restore from the
+        backup and apply the iteration's gradients in one pass."""
+        sa = seeds_array(seeds)
+        qa = np.ascontiguousarray(q, dtype=np.int8)
+        if sa.size != qa.size:
+            raise ValueError("seeds and q differ in length")
+        _check(lib.mezo_update_multi_from(self._h, src.handle, sa.ctypes.data, qa.ctypes.data,
+                                          sa.size, ctypes.byref(codec_), float(lr),
+                                          _stream_ptr(stream)), "mezo_update_multi_from")
 
     def replay(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
         """Late-joiner catch-up: steps = [(seeds, q, lr), ...] in order."""

@@ -196,3 +196,35 @@ def test_one_hip_runtime_in_the_process():
             if "libamdhip64" in p:
                 paths.add(p)
     assert len(paths) == 1, paths
+
+
+def test_from_calls_check_layout_and_overlap():
+    lib = mezo.lib
+    c = mezo.codec()
+    s = seeds_of((0, 0, 0), (1, 0, 0))
+    q = np.array([3, 4], dtype=np.int8)
+    _, dst = create([(0x100000, 1024, 0, mezo.F32), (0x200000, 512, 1, mezo.BF16)])
+    _, ok_src = create([(0x300000, 1024, 0, mezo.F32), (0x400000, 512, 1, mezo.BF16)])
+    _, bad_n = create([(0x300000, 1000, 0, mezo.F32), (0x400000, 512, 1, mezo.BF16)])
+    _, bad_id = create([(0x300000, 1024, 5, mezo.F32), (0x400000, 512, 1, mezo.BF16)])
+    _, bad_cnt = create([(0x300000, 1024, 0, mezo.F32)])
+    _, overlap = create([(0x100800, 1024, 0, mezo.F32), (0x400000, 512, 1, mezo.BF16)])
+    _, twin = create([(0x100000, 1024, 0, mezo.F32), (0x400000, 512, 1, mezo.BF16)])
+    try:
+        for src, code in [(bad_n, mezo.EINVAL), (bad_id, mezo.EINVAL), (bad_cnt, mezo.EINVAL),
+                          (overlap, mezo.EOVERLAP)]:
+            assert lib.mezo_update_multi_from(dst, src, s.ctypes.data, q.ctypes.data, 2, c, 1e-3,
+                                              None) == code
+            assert lib.mezo_perturb_from(dst, src, mezo.Seed(0, 0, 0), 1e-3, None) == code
+        # argument checks come first, as for the in-place calls
+        assert lib.mezo_update_multi_from(dst, ok_src, s.ctypes.data, q.ctypes.data, 2, c,
+                                          float("nan"), None) == mezo.ERANGE
+        assert lib.mezo_perturb_from(dst, ok_src, mezo.Seed(0, 0, 0), float("inf"), None) == mezo.ERANGE
+        assert lib.mezo_perturb_from(None, ok_src, mezo.Seed(0, 0, 0), 1.0, None) == mezo.EINVAL
+        # a tensor that is its own source is allowed; valid calls get as far as
+        # the device (none here)
+        assert lib.mezo_perturb_from(dst, twin, mezo.Seed(0, 0, 0), 1.0, None) == mezo.EHIP
+        assert lib.mezo_perturb_from(dst, ok_src, mezo.Seed(0, 0, 0), 0.0, None) == mezo.EHIP
+    finally:
+        for h in (dst, ok_src, bad_n, bad_id, bad_cnt, overlap, twin):
+            lib.mezo_paramset_destroy(h)

@@ -300,3 +300,58 @@ def test_streams_are_respected(mz, orc):
     ref = orc.perturb(hosts[0].copy(), 0, (1, 1, 1), 1e-3)
     orc.update(ref, 0, synth.seeds(40, 1), synth.grads_int8(40, seed=6), 1e-4)
     assert_theta_close(to_host(devs[0]), ref, "side stream")
+
+
+# ---- out of place: the backup restore fused into the sweep ----------------
+
+def test_update_from_backup_matches_oracle_and_leaves_source(mz, orc):
+    hosts, ids = ragged_hosts()
+    backup_devs, backup = make_set(mz, hosts, ids)
+    zeros = [np.zeros_like(h) for h in hosts]
+    devs, ps = make_set(mz, zeros, ids)
+    seeds = synth.seeds(4, 2, step=3)
+    q = synth.grads_int8(8, seed=21)
+    ps.update_multi_from(backup, seeds, q, 2e-3)
+    sync()
+    for h, d, b, tid in zip(hosts, devs, backup_devs, ids):
+        ref = orc.update(h.copy(), tid, seeds, q, 2e-3)
+        assert_theta_close(to_host(d), ref, f"update_from n={h.size}", inp=h)
+        assert np.array_equal(to_host(b).view(np.uint8), h.view(np.uint8))
+
+
+def test_perturb_from_and_zero_weight_copy(mz, orc):
+    hosts, ids = ragged_hosts()
+    hosts[0][0] = -0.0
+    backup_devs, backup = make_set(mz, hosts, ids)
+    devs, ps = make_set(mz, [np.ones_like(h) for h in hosts], ids)
+    ps.perturb_from(backup, (7, 1, 2), 1e-3)
+    sync()
+    for h, d, tid in zip(hosts, devs, ids):
+        ref = orc.perturb(h.copy(), tid, (7, 1, 2), 1e-3)
+        assert_theta_close(to_host(d), ref, f"perturb_from n={h.size}", inp=h)
+    ps.update_multi_from(backup, synth.seeds(2, 1), np.zeros(2, dtype=np.int8), 1.0)
+    sync()
+    for h, d in zip(hosts, devs):
+        assert np.array_equal(to_host(d).view(np.uint8), h.view(np.uint8))
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_algorithm1_iteration_restore_fused(mz, orc, dtype):
+    """Backup, perturb triple in place (drifts), then the fused restore+update
+    gives exactly what copying the backup back and updating in place gives."""
+    import torch
+    hosts = [synth.theta0_tensor((n,), dtype, i, 8) for i, n in enumerate([70001, 4096, 33])]
+    devs, ps = make_set(mz, hosts)
+    backup_devs, backup = make_set(mz, hosts)
+    s, eps = (0, 5, 0), 1e-3
+    for c in (eps, -2 * eps, eps):
+        ps.perturb(s, c)
+    seeds = synth.seeds(8, 1, step=5)
+    q = synth.grads_int8(8, seed=31)
+    ps.update_multi_from(backup, seeds, q, 1e-3)
+    ref_devs, ref_ps = make_set(mz, hosts)
+    ref_ps.update_multi(seeds, q, 1e-3)
+    torch.cuda.synchronize()
+    for i, (d, r, h) in enumerate(zip(devs, ref_devs, hosts)):
+        assert np.array_equal(to_host(d).view(np.uint8), to_host(r).view(np.uint8))
+        assert_theta_close(to_host(d), orc.update(h.copy(), i, seeds, q, 1e-3), f"tensor {i}", inp=h)
