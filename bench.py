@@ -221,7 +221,8 @@ def main():
         bviews = [backup_flat[a:a + n] for a, n in offs]
         backup = mezo.ParamSet(bviews)
         q0 = mezo.quantize_projgrad(proj[0])
-        ps.update_multi_from(backup, seeds_t[0], q0, lr)
+        for _ in range(3):
+            ps.update_multi_from(backup, seeds_t[0], q0, lr)
         torch.cuda.synchronize()
         a_ev = torch.cuda.Event(enable_timing=True)
         b_ev = torch.cuda.Event(enable_timing=True)
@@ -234,6 +235,21 @@ def main():
         from_ms = a_ev.elapsed_time(b_ev) / reps
         backup.close()
         del backup_flat, bviews
+
+    # ChecksumMatch: the replica check after the apply loop (read-only stream),
+    # reported per op, not part of the step.
+    ck = torch.empty(1, dtype=torch.int64, device=dev)
+    for _ in range(3):
+        ps.checksum_into(ck)
+    torch.cuda.synchronize()
+    a_ev = torch.cuda.Event(enable_timing=True)
+    b_ev = torch.cuda.Event(enable_timing=True)
+    a_ev.record(stream)
+    for _ in range(args.steps):
+        ps.checksum_into(ck)
+    b_ev.record(stream)
+    torch.cuda.synchronize()
+    ck_ms = a_ev.elapsed_time(b_ev) / args.steps
 
     value = ps_per_step * args.steps / (ms_total / 1e3)
     bytes_per_launch = 2 * N * (4 if w.dtype == "f32" else 2)
@@ -256,6 +272,9 @@ def main():
                   "alg_GBps": bytes_per_launch / t_s / 1e9,
                   "hbm_frac": bytes_per_launch / t_s / 1e9 / HBM_PEAK_GBS,
                   "alu_frac": N * recs[c] * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S}
+    ck_bytes = bytes_per_launch / 2
+    ops["checksum"] = {"ms": round(ck_ms, 4), "alg_GBps": ck_bytes / (ck_ms / 1e3) / 1e9,
+                       "hbm_frac": ck_bytes / (ck_ms / 1e3) / 1e9 / HBM_PEAK_GBS}
     if from_ms is not None:
         t_s = from_ms / 1e3
         ops["update_from_backup"] = {

@@ -202,6 +202,21 @@ MEZO_API int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src,
                                     const mezo_seed_t* seeds, const int8_t* q, uint32_t K,
                                     const mezo_codec_t* codec, float lr, void* stream);
 
+/* ---- replica check ----------------------------------------------------- */
+
+/* ChecksumMatch (Algorithm 1): a 64-bit checksum of the bits of every tensor,
+ * for comparing replicas (and a late joiner after mezo_replay) with a peer.
+ * Each tensor's bytes are read as little-endian 8-byte chunks c_j (the last
+ * zero-padded) and
+ *   checksum = sum over tensors t, chunks j of
+ *              fmix64(c_j ^ j * 0x9E3779B97F4A7C15 ^ tensor_id_t * 0xD1B54A32D192ED03)
+ * mod 2^64, fmix64 being MurmurHash3's 64-bit finalizer. The sum does not
+ * depend on how tensors are grouped into paramsets or in which order they were
+ * registered (the checksum of a model split over several paramsets is the sum
+ * of theirs). Written asynchronously to out_dev, a device pointer to 8 bytes
+ * (8-byte aligned; MEZO_EINVAL otherwise), on stream. */
+MEZO_API int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream);
+
 /* ---- the one-byte gradient (host, pure) ------------------------------- */
 
 /* Projected gradient g = (l+ - l-) / (2 eps) -> q (Section 3). ±inf clip to

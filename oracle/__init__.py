@@ -94,6 +94,10 @@ def lib() -> ctypes.CDLL:
         L.orc_update.restype = i32
         L.orc_replay.argtypes = [vp, i32, u32, vp, u64, u64, vp, vp, vp, vp, u32, i32, f32, f32]
         L.orc_replay.restype = i32
+        L.orc_fmix64.argtypes = [u64]
+        L.orc_fmix64.restype = u64
+        L.orc_checksum.argtypes = [vp, u64, u32]
+        L.orc_checksum.restype = u64
         L.orc_set_threads.argtypes = [i32]
         L.orc_set_threads.restype = None
         L.orc_get_threads.argtypes = []
@@ -237,6 +241,22 @@ def update(theta: np.ndarray, tensor_id: int, seeds, q, lr: float, kind: int = L
     _check(lib().orc_update(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
                             _ptr(sa), _ptr(qa), sa.size, kind, scale, alpha, lr), "update")
     return theta
+
+
+def fmix64(x: int) -> int:
+    return int(lib().orc_fmix64(int(x) & 0xFFFFFFFFFFFFFFFF))
+
+
+def checksum_tensor(data: np.ndarray, tensor_id: int) -> int:
+    """Checksum of one tensor's bytes (fp32, or uint16 bf16 bits)."""
+    a = np.ascontiguousarray(data)
+    return int(lib().orc_checksum(_ptr(a), a.nbytes, int(tensor_id)))
+
+
+def checksum(tensors, tensor_ids=None) -> int:
+    """Checksum of a parameter set: the sum mod 2^64 of its tensors'."""
+    ids = range(len(tensors)) if tensor_ids is None else tensor_ids
+    return sum(checksum_tensor(t, i) for t, i in zip(tensors, ids)) & 0xFFFFFFFFFFFFFFFF
 
 
 def replay(theta: np.ndarray, tensor_id: int, steps, kind: int = LINEAR,

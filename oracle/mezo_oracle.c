@@ -336,6 +336,42 @@ int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
     return 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Checksum of theta (Algorithm 1, ChecksumMatch: a hash of the weights      */
+/* compared with a random peer). The paper fixes no hash; any function every */
+/* replica computes identically serves. A sum of per-chunk mixes is order-    */
+/* independent, so it is the same however the tensors are grouped.          */
+/* ------------------------------------------------------------------------ */
+
+uint64_t orc_fmix64(uint64_t x)
+{
+    /* MurmurHash3 (Appleby), 64-bit finalizer */
+    x ^= x >> 33;
+    x *= 0xFF51AFD7ED558CCDull;
+    x ^= x >> 33;
+    x *= 0xC4CEB9FE1A85EC53ull;
+    x ^= x >> 33;
+    return x;
+}
+
+uint64_t orc_checksum(const void* data, uint64_t nbytes, uint32_t tensor_id)
+{
+    const unsigned char* b = (const unsigned char*)data;
+    const uint64_t kPos = 0x9E3779B97F4A7C15ull;
+    const uint64_t kTensor = 0xD1B54A32D192ED03ull;
+    uint64_t n_chunks = (nbytes + 7) / 8;
+    uint64_t sum = 0;
+    for (uint64_t j = 0; j < n_chunks; ++j) {
+        uint64_t c = 0;
+        for (int k = 0; k < 8; ++k) {
+            uint64_t at = j * 8 + (uint64_t)k;
+            if (at < nbytes) c |= (uint64_t)b[at] << (8 * k); /* little-endian */
+        }
+        sum += orc_fmix64(c ^ (j * kPos) ^ ((uint64_t)tensor_id * kTensor));
+    }
+    return sum;
+}
+
 void orc_set_threads(int n)
 {
 #ifdef _OPENMP

@@ -112,6 +112,16 @@ int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
                const uint32_t* K_t, const float* lr_t, uint32_t T,
                int kind, float scale, float alpha);
 
+/* Checksum of a tensor's bits (ChecksumMatch, Algorithm 1: replicas compare a
+ * hash of theta). The tensor's nbytes bytes are read as little-endian 8-byte
+ * chunks c_j, the last one zero-padded; the result is
+ *     sum_j fmix64(c_j ^ (j * P1) ^ (tensor_id * P2))  mod 2^64
+ * with P1 = 0x9E3779B97F4A7C15, P2 = 0xD1B54A32D192ED03 and fmix64 the 64-bit
+ * finalizer of MurmurHash3. A parameter set's checksum is the sum over its
+ * tensors, so it does not depend on grouping or order. */
+uint64_t orc_fmix64(uint64_t x);
+uint64_t orc_checksum(const void* data, uint64_t nbytes, uint32_t tensor_id);
+
 /* Thread control for the OpenMP loops (1 when built without OpenMP). */
 void orc_set_threads(int n);
 int  orc_get_threads(void);

@@ -429,6 +429,31 @@ int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const 
     return launch_records(ps, recs, static_cast<hipStream_t>(stream));
 }
 
+int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
+{
+    if (!ps || !out_dev || (reinterpret_cast<uintptr_t>(out_dev) & 7u)) return MEZO_EINVAL;
+    std::lock_guard<std::mutex> lock(ps->mu);
+    int rc = ensure_device(ps);
+    if (rc) return rc;
+    mezo::ChecksumArgs tabs[2];
+    uint32_t dts[2];
+    int n = 0;
+    for (uint32_t dt = 0; dt < 2; ++dt) {
+        if (ps->table[dt].empty()) continue;
+        tabs[n].tensors = ps->d_table[dt];
+        tabs[n].tile_tensor = ps->d_tile_tensor[dt];
+        tabs[n].total_tiles = ps->total_tiles[dt];
+        tabs[n].out = reinterpret_cast<unsigned long long*>(out_dev);
+        dts[n] = dt;
+        ++n;
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
+                                   ps->device, st));
+    MEZO_HIP(hipEventRecord(ps->last, st));
+    return MEZO_OK;
+}
+
 int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t* codec)
 {
     if (!codec) return MEZO_EINVAL;

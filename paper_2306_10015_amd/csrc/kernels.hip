@@ -291,6 +291,83 @@ __global__ __launch_bounds__(kThreads) void generate_kernel(GenArgs a)
     }
 }
 
+// ---- checksum of theta (ChecksumMatch, Algorithm 1) ---------------------------
+// Read-only stream over the same tiles as the engine; every lane sums the
+// mixes of its 8-byte chunks, a workgroup reduces across lanes and waves and
+// adds its sum to the output with one 64-bit atomic. Sums mod 2^64 commute, so
+// the grid shape and the order of the atomics do not change the result.
+
+__device__ __forceinline__ uint64_t fmix64(uint64_t x)
+{
+    x ^= x >> 33;
+    x *= kFmixA;
+    x ^= x >> 33;
+    x *= kFmixB;
+    x ^= x >> 33;
+    return x;
+}
+
+template <uint32_t kDtype>
+__global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
+{
+    constexpr int kGroups = Layout<kDtype>::kGroups;
+    constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
+    constexpr uint64_t kEsz = 16 / kPer;
+    uint64_t sum = 0;
+    for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
+        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+        const uint64_t local = tile - d.tile_begin;
+        const uint64_t nbytes = d.numel * kEsz;
+        const uint64_t nchunks = (nbytes + 7) / 8;
+        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const uint64_t grp = group_index<kGroups>(local, g);
+            const uint64_t c0 = grp * 2;  // index of the group's first chunk
+            if (c0 >= nchunks) continue;
+            uint4 v;
+            if ((grp + 1) * kPer <= d.numel) {
+                v = load_stream(d.data + grp * 16);
+            } else {
+                // tail: read the elements that exist, zero the rest
+                uint32_t w[4] = {0u, 0u, 0u, 0u};
+                if constexpr (kDtype == kF32) {
+                    const MEZO_GLOBAL uint32_t* in = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.data);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (grp * 4 + j < d.numel) w[j] = in[grp * 4 + j];
+                } else {
+                    const gu16_t* in = reinterpret_cast<const gu16_t*>(d.data);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (grp * 8 + j < d.numel) w[j >> 1] |= uint32_t(in[grp * 8 + j]) << (16 * (j & 1));
+                }
+                v = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+            const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+            const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+            sum += fmix64(lo ^ (c0 * kChunkPos) ^ tmix);
+            if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((c0 + 1) * kChunkPos) ^ tmix);
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+    __shared__ uint64_t part[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t s = 0;
+#pragma unroll
+        for (int i = 0; i < kThreads / 64; ++i) s += part[i];
+        atomicAdd(a.out, static_cast<unsigned long long>(s));
+    }
+}
+
+__global__ void zero_u64_kernel(unsigned long long* out)
+{
+    if (threadIdx.x == 0 && blockIdx.x == 0) *out = 0ull;
+}
+
 // ---- host-side launchers ----------------------------------------------------
 
 hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream)
@@ -336,6 +413,39 @@ hipError_t launch_generate(const GenArgs& args, hipStream_t stream)
         left -= n;
         first += n;
         done += n;
+    }
+    return hipSuccess;
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+int g_cus[kMaxDevices] = {0};
+}  // namespace
+
+hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n_tables,
+                           unsigned long long* out, int device, hipStream_t stream)
+{
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidValue;
+    if (g_cus[device] == 0) {
+        hipError_t e = hipDeviceGetAttribute(&g_cus[device], hipDeviceAttributeMultiprocessorCount, device);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, stream, out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    for (int i = 0; i < n_tables; ++i) {
+        if (tables[i].total_tiles == 0) continue;
+        // as many workgroups as fill the device (8 per CU), each striding over tiles
+        const uint64_t cap = uint64_t(g_cus[device]) * 8;
+        const uint64_t grid = tables[i].total_tiles < cap ? tables[i].total_tiles : cap;
+        const dim3 g{uint32_t(grid)};
+        const dim3 b{uint32_t(kThreads)};
+        if (dtypes[i] == kF32)
+            hipLaunchKernelGGL(checksum_kernel<kF32>, g, b, 0, stream, tables[i]);
+        else
+            hipLaunchKernelGGL(checksum_kernel<kBF16>, g, b, 0, stream, tables[i]);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }

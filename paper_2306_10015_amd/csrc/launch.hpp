@@ -23,6 +23,13 @@ struct EngineArgs {
     SeedRec inl[kInlineRecs];
 };
 
+struct ChecksumArgs {
+    const TensorDesc* tensors;
+    const uint32_t* tile_tensor;
+    uint64_t total_tiles;
+    unsigned long long* out;  // device, accumulated with atomic adds
+};
+
 struct GenArgs {
     SeedRec rec;
     uint64_t first;
@@ -36,5 +43,9 @@ struct GenArgs {
 // workgroup per tile (at most 2^31 - 1 tiles).
 hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream);
 hipError_t launch_generate(const GenArgs& args, hipStream_t stream);
+
+// Zero *out, then add the checksum of every table given (one launch each).
+hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n_tables,
+                           unsigned long long* out, int device, hipStream_t stream);
 
 }  // namespace mezo

@@ -57,6 +57,16 @@ constexpr uint32_t kMulB = 0xCD9E8D57u;
 constexpr uint32_t kWeylA = 0x9E3779B9u;
 constexpr uint32_t kWeylB = 0xBB67AE85u;
 
+// ---- checksum -------------------------------------------------------------
+// A tensor's bytes as little-endian 8-byte chunks c_j (the last zero-padded);
+// checksum = sum over all chunks of all tensors of
+// fmix64(c_j ^ j * kChunkPos ^ tensor_id * kChunkTensor) mod 2^64, fmix64 being
+// MurmurHash3's 64-bit finalizer (multipliers kFmixA, kFmixB).
+constexpr uint64_t kChunkPos = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kChunkTensor = 0xD1B54A32D192ED03ull;
+constexpr uint64_t kFmixA = 0xFF51AFD7ED558CCDull;
+constexpr uint64_t kFmixB = 0xC4CEB9FE1A85EC53ull;
+
 // sqrt(2 ln 2) in double: the engine kernels produce z / sqrt(2 ln 2) and the
 // host folds the factor into every record's coefficient.
 constexpr double kZScaleF64 = 1.17741002251547469101;

@@ -58,7 +58,7 @@ class Step(ctypes.Structure):
 #: Every symbol include/mezo.h declares.
 EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
            "mezo_perturb", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
-           "mezo_update_multi_from", "quantize_projgrad",
+           "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
            "mezo_dequantize", "mezo_debug_generate", "mezo_strerror", "mezo_last_error",
            "mezo_version")
 
@@ -90,6 +90,8 @@ def _load() -> ctypes.CDLL:
     L.mezo_perturb_from.restype = i32
     L.mezo_update_multi_from.argtypes = [vp, vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
     L.mezo_update_multi_from.restype = i32
+    L.mezo_checksum.argtypes = [vp, vp, vp]
+    L.mezo_checksum.restype = i32
     L.quantize_projgrad.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
     L.quantize_projgrad.restype = i32
     L.mezo_dequantize.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
@@ -237,6 +239,20 @@ class ParamSet:
         _check(lib.mezo_update_multi_from(self._h, src.handle, sa.ctypes.data, qa.ctypes.data,
                                           sa.size, ctypes.byref(codec_), float(lr),
                                           _stream_ptr(stream)), "mezo_update_multi_from")
+
+    def checksum_into(self, out, stream=None) -> None:
+        """Enqueue the 64-bit checksum of every tensor's bits into `out`, a
+        device tensor of 8 bytes (ChecksumMatch, Algorithm 1)."""
+        if out.numel() * out.element_size() != 8 or not out.is_cuda:
+            raise ValueError("out must be an 8-byte device tensor")
+        _check(lib.mezo_checksum(self._h, out.data_ptr(), _stream_ptr(stream)), "mezo_checksum")
+
+    def checksum(self, stream=None) -> int:
+        """The checksum as a Python int (synchronises with the stream)."""
+        import torch
+        out = torch.empty(1, dtype=torch.int64, device=self.tensors[0].device)
+        self.checksum_into(out, stream)
+        return int(out.item()) & 0xFFFFFFFFFFFFFFFF
 
     def replay(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
         """Late-joiner catch-up: steps = [(seeds, q, lr), ...] in order."""

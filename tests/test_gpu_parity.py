@@ -355,3 +355,45 @@ def test_algorithm1_iteration_restore_fused(mz, orc, dtype):
     for i, (d, r, h) in enumerate(zip(devs, ref_devs, hosts)):
         assert np.array_equal(to_host(d).view(np.uint8), to_host(r).view(np.uint8))
         assert_theta_close(to_host(d), orc.update(h.copy(), i, seeds, q, 1e-3), f"tensor {i}", inp=h)
+
+
+# ---- checksum (ChecksumMatch, Algorithm 1) ---------------------------------
+
+def test_checksum_matches_oracle_and_is_additive(mz, orc):
+    hosts, ids = ragged_hosts()
+    devs, ps = make_set(mz, hosts, ids)
+    want = orc.checksum(hosts, ids)
+    assert ps.checksum() == want
+    half = len(hosts) // 2
+    _, a = make_set(mz, hosts[:half], ids[:half])
+    _, b = make_set(mz, hosts[half:], ids[half:])
+    assert (a.checksum() + b.checksum()) & 0xFFFFFFFFFFFFFFFF == want
+    # after GPU work the checksum is that of the bits the GPU holds
+    ps.update_multi(synth.seeds(3, 1), synth.grads_int8(3, seed=5), 1e-2)
+    sync()
+    assert ps.checksum() == orc.checksum([to_host(d) for d in devs], ids)
+
+
+def test_checksum_detects_one_flipped_bit(mz):
+    import torch
+    hosts = tiny_hosts(synth.BF16)
+    devs, ps = make_set(mz, hosts)
+    base = ps.checksum()
+    raw = devs[2].view(torch.int16)
+    raw[123457] ^= 1
+    assert ps.checksum() != base
+    raw[123457] ^= 1
+    assert ps.checksum() == base
+
+
+def test_checksum_full_125m_set(mz, orc):
+    import torch
+    from gpu_util import theta_on_device
+    w = synth.WORKLOADS["opt125m"]
+    tensors = theta_on_device(w, seed=3, device_rng=True)
+    ps = mz.ParamSet(tensors)
+    got = ps.checksum()
+    assert got == orc.checksum([to_host(t) for t in tensors])
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
