@@ -94,6 +94,18 @@ def lib() -> ctypes.CDLL:
         L.orc_update.restype = i32
         L.orc_replay.argtypes = [vp, i32, u32, vp, u64, u64, vp, vp, vp, vp, u32, i32, f32, f32]
         L.orc_replay.restype = i32
+        L.orc_box_muller_portable.argtypes = [vp, vp]
+        L.orc_box_muller_portable.restype = None
+        L.orc_z_portable.argtypes = [Seed, u32, u64]
+        L.orc_z_portable.restype = f32
+        L.orc_generate_portable.argtypes = [Seed, u32, u64, u64, vp]
+        L.orc_generate_portable.restype = i32
+        L.orc_perturb_portable.argtypes = [vp, i32, u32, vp, u64, u64, Seed, f32]
+        L.orc_perturb_portable.restype = i32
+        L.orc_update_portable.argtypes = [vp, i32, u32, vp, u64, u64, vp, vp, u32, i32, f32, f32, f32]
+        L.orc_update_portable.restype = i32
+        L.orc_replay_portable.argtypes = [vp, i32, u32, vp, u64, u64, vp, vp, vp, vp, u32, i32, f32, f32]
+        L.orc_replay_portable.restype = i32
         L.orc_fmix64.argtypes = [u64]
         L.orc_fmix64.restype = u64
         L.orc_checksum.argtypes = [vp, u64, u32]
@@ -164,13 +176,25 @@ def box_muller(words) -> np.ndarray:
     return z
 
 
-def generate(seed, tensor_id: int, first: int, count: int, words=True, z=True):
-    """RNG word and fp32 Gaussian of elements ``first .. first+count-1``."""
+def generate(seed, tensor_id: int, first: int, count: int, words=True, z=True,
+             portable: bool = False):
+    """RNG word and fp32 Gaussian of elements ``first .. first+count-1``
+    (portable: the binary32-only Gaussian)."""
     w = np.zeros(count, dtype=np.uint32) if words else None
     g = np.zeros(count, dtype=np.float32) if z else None
-    _check(lib().orc_generate(_seed(seed), tensor_id, first, count, _ptr(w), _ptr(g)),
-           "generate")
+    _check(lib().orc_generate(_seed(seed), tensor_id, first, count, _ptr(w),
+                              None if portable else _ptr(g)), "generate")
+    if portable and z:
+        _check(lib().orc_generate_portable(_seed(seed), tensor_id, first, count, _ptr(g)),
+               "generate_portable")
     return w, g
+
+
+def box_muller_portable(words) -> np.ndarray:
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    z = np.zeros(4, dtype=np.float32)
+    lib().orc_box_muller_portable(_ptr(w), _ptr(z))
+    return z
 
 
 def round_f32(x: float) -> float:
@@ -220,17 +244,20 @@ def _idx(idx):
     return None if idx is None else np.ascontiguousarray(idx, dtype=np.uint64)
 
 
-def perturb(theta: np.ndarray, tensor_id: int, seed, scale: float, idx=None, first: int = 0):
+def perturb(theta: np.ndarray, tensor_id: int, seed, scale: float, idx=None, first: int = 0,
+            portable: bool = False):
     """In place: theta <- round(theta + scale * z(seed)) (PerturbParameters)."""
     dt = _theta_args(theta)
     ix = _idx(idx)
-    _check(lib().orc_perturb(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
-                             _seed(seed), scale), "perturb")
+    fn = lib().orc_perturb_portable if portable else lib().orc_perturb
+    _check(fn(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size, _seed(seed), scale),
+           "perturb")
     return theta
 
 
 def update(theta: np.ndarray, tensor_id: int, seeds, q, lr: float, kind: int = LINEAR,
-           scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA, idx=None, first: int = 0):
+           scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA, idx=None, first: int = 0,
+           portable: bool = False):
     """In place: theta <- round(theta + sum_k c_k z_k), c_k = fl32(-lr * deq(q_k))."""
     dt = _theta_args(theta)
     ix = _idx(idx)
@@ -238,8 +265,9 @@ def update(theta: np.ndarray, tensor_id: int, seeds, q, lr: float, kind: int = L
     qa = np.ascontiguousarray(q, dtype=np.int8)
     if sa.size != qa.size:
         raise ValueError("seeds and q differ in length")
-    _check(lib().orc_update(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
-                            _ptr(sa), _ptr(qa), sa.size, kind, scale, alpha, lr), "update")
+    fn = lib().orc_update_portable if portable else lib().orc_update
+    _check(fn(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
+              _ptr(sa), _ptr(qa), sa.size, kind, scale, alpha, lr), "update")
     return theta
 
 
@@ -260,7 +288,8 @@ def checksum(tensors, tensor_ids=None) -> int:
 
 
 def replay(theta: np.ndarray, tensor_id: int, steps, kind: int = LINEAR,
-           scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA, idx=None, first: int = 0):
+           scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA, idx=None, first: int = 0,
+           portable: bool = False):
     """In place: apply ``steps`` = [(seeds, q, lr), ...] one after another."""
     dt = _theta_args(theta)
     ix = _idx(idx)
@@ -270,7 +299,8 @@ def replay(theta: np.ndarray, tensor_id: int, steps, kind: int = LINEAR,
         np.zeros(0, dtype=np.int8)
     kt = np.array([len(q) for _, q, _ in steps], dtype=np.uint32)
     lrt = np.array([lr for _, _, lr in steps], dtype=np.float32)
-    _check(lib().orc_replay(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
-                            _ptr(seeds), _ptr(qs), _ptr(kt), _ptr(lrt), len(steps),
-                            kind, scale, alpha), "replay")
+    fn = lib().orc_replay_portable if portable else lib().orc_replay
+    _check(fn(_ptr(theta), dt, tensor_id, _ptr(ix), first, theta.size,
+              _ptr(seeds), _ptr(qs), _ptr(kt), _ptr(lrt), len(steps),
+              kind, scale, alpha), "replay")
     return theta

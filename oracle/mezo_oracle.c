@@ -337,6 +337,155 @@ int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Portable mode: z from binary32 operations only (Appendix B asks for noise */
+/* that every device reproduces; hardware transcendentals differ between    */
+/* devices, IEEE +, *, fma, / and sqrt do not). The header gives the steps.  */
+/* ------------------------------------------------------------------------ */
+
+static void box_muller_pair_portable(uint32_t wa, uint32_t wb, float* zc, float* zs)
+{
+    /* -2 ln u1 with u1 = n1 2^-24: reduce n1 to m in [sqrt(1/2), sqrt(2)) times
+     * a power of two, then ln m = 2 atanh(s), s = (m - 1)/(m + 1). */
+    uint32_t n1 = (wa >> 8) + 1u;
+    int e = 0;
+    while ((n1 >> (e + 1)) != 0u) ++e;                 /* floor(log2 n1) */
+    float m = ldexpf((float)n1, -e);                    /* exact, [1, 2) */
+    if (m >= 0x1.6a09e6p+0f) {                          /* fl32(sqrt 2) */
+        m = m * 0.5f;
+        e = e + 1;
+    }
+    float f = m - 1.0f;                                 /* exact */
+    float s = f / (f + 2.0f);
+    float s2 = s * s;
+    float p = fmaf(s2, 0x1.c71c72p-4f, 0x1.24924ap-3f); /* 1/9, 1/7 */
+    p = fmaf(s2, p, 0x1.99999ap-3f);                    /* 1/5 */
+    p = fmaf(s2, p, 0x1.555556p-2f);                    /* 1/3 */
+    p = fmaf(s2, p, 1.0f);
+    float ln_m = (s + s) * p;
+    float ln_u1 = fmaf((float)(e - 24), 0x1.62e430p-1f, ln_m); /* + (e-24) ln 2 */
+    float r = sqrtf(-2.0f * ln_u1);
+
+    /* (cos, sin)(2 pi u2), u2 = t 2^-24: octant q of v = 8 u2, angle within it */
+    uint32_t t = wb >> 8;
+    float v = ldexpf((float)t, -21);                    /* exact, [0, 8) */
+    int q = (int)v;                                     /* floor, v >= 0 */
+    float x = v - (float)q;                             /* exact, [0, 1) */
+    float y = (q & 1) ? 1.0f - x : x;                   /* exact, [0, 1] */
+    float a = y * 0x1.921fb6p-1f;                       /* fl32(pi/4) */
+    float a2 = a * a;
+    float sn = fmaf(a2, 0x1.71de3ap-19f, -0x1.a01a02p-13f); /* 1/9!, -1/7! */
+    sn = fmaf(a2, sn, 0x1.111112p-7f);                  /* 1/5! */
+    sn = fmaf(a2, sn, -0x1.555556p-3f);                 /* -1/3! */
+    sn = fmaf(a2, sn, 1.0f);
+    sn = a * sn;
+    float cs = fmaf(a2, -0x1.27e4fcp-22f, 0x1.a01a02p-16f); /* -1/10!, 1/8! */
+    cs = fmaf(a2, cs, -0x1.6c16c2p-10f);                /* -1/6! */
+    cs = fmaf(a2, cs, 0x1.555556p-5f);                  /* 1/4! */
+    cs = fmaf(a2, cs, -0.5f);                           /* -1/2! */
+    cs = fmaf(a2, cs, 1.0f);
+    /* the angle is q pi/4 + a (q even) or (q+1) pi/4 - a (q odd) */
+    int swap = ((q + 1) >> 1) & 1;                      /* octants 1, 2, 5, 6 */
+    int neg_cos = ((q + 2) >> 2) & 1;                   /* octants 2..5 */
+    int neg_sin = q >> 2;                               /* octants 4..7 */
+    float c0 = swap ? sn : cs;
+    float s0 = swap ? cs : sn;
+    if (neg_cos) c0 = -c0;
+    if (neg_sin) s0 = -s0;
+    *zc = r * c0;
+    *zs = r * s0;
+}
+
+void orc_box_muller_portable(const uint32_t w[4], float z[4])
+{
+    box_muller_pair_portable(w[0], w[1], &z[0], &z[1]);
+    box_muller_pair_portable(w[2], w[3], &z[2], &z[3]);
+}
+
+float orc_z_portable(orc_seed_t s, uint32_t tensor_id, uint64_t e)
+{
+    uint32_t w[4];
+    float z[4];
+    orc_block_words(s, tensor_id, e, w);
+    orc_box_muller_portable(w, z);
+    return z[e & 3u];
+}
+
+int orc_generate_portable(orc_seed_t s, uint32_t tensor_id, uint64_t first, uint64_t count,
+                          float* z)
+{
+    if (count > 0 && (first + count - 1) >> 34) return -1;
+    long long n = (long long)count;
+#pragma omp parallel for schedule(static)
+    for (long long i = 0; i < n; ++i) z[i] = orc_z_portable(s, tensor_id, first + (uint64_t)i);
+    return 0;
+}
+
+static float load_theta_f32(const void* theta, int dtype, uint64_t i)
+{
+    return (float)load_theta(theta, dtype, i); /* exact for both storage types */
+}
+
+int orc_perturb_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                         uint64_t first, uint64_t n, orc_seed_t s, float scale)
+{
+    if (!elems_ok(dtype, idx, first, n)) return -1;
+    if (!isfinite(scale)) return -2;
+    if (scale == 0.0f) return 0;
+    long long nn = (long long)n;
+#pragma omp parallel for schedule(static)
+    for (long long i = 0; i < nn; ++i) {
+        uint64_t e = idx ? idx[i] : first + (uint64_t)i;
+        float acc = fmaf(scale, orc_z_portable(s, tensor_id, e), 0.0f);
+        float v = load_theta_f32(theta, dtype, (uint64_t)i) + acc;
+        store_theta(theta, dtype, (uint64_t)i, (double)v);
+    }
+    return 0;
+}
+
+int orc_update_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                        uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+                        uint32_t K, int kind, float scale, float alpha, float lr)
+{
+    if (!elems_ok(dtype, idx, first, n)) return -1;
+    if (K > 0 && (!seeds || !q)) return -1;
+    float c[4096];
+    if (K > 4096) return -1;
+    int rc = orc_coefficients(q, K, kind, scale, alpha, lr, c);
+    if (rc) return rc;
+    uint32_t live = 0;
+    for (uint32_t k = 0; k < K; ++k) live += (c[k] != 0.0f);
+    if (live == 0) return 0;
+    long long nn = (long long)n;
+#pragma omp parallel for schedule(static)
+    for (long long i = 0; i < nn; ++i) {
+        uint64_t e = idx ? idx[i] : first + (uint64_t)i;
+        float acc = 0.0f;
+        for (uint32_t k = 0; k < K; ++k) {
+            if (c[k] == 0.0f) continue;
+            acc = fmaf(c[k], orc_z_portable(seeds[k], tensor_id, e), acc);
+        }
+        float v = load_theta_f32(theta, dtype, (uint64_t)i) + acc;
+        store_theta(theta, dtype, (uint64_t)i, (double)v);
+    }
+    return 0;
+}
+
+int orc_replay_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                        uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+                        const uint32_t* K_t, const float* lr_t, uint32_t T,
+                        int kind, float scale, float alpha)
+{
+    uint64_t off = 0;
+    for (uint32_t t = 0; t < T; ++t) {
+        int rc = orc_update_portable(theta, dtype, tensor_id, idx, first, n, seeds + off, q + off,
+                                     K_t[t], kind, scale, alpha, lr_t[t]);
+        if (rc) return rc;
+        off += K_t[t];
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Checksum of theta (Algorithm 1, ChecksumMatch: a hash of the weights      */
 /* compared with a random peer). The paper fixes no hash; any function every */
 /* replica computes identically serves. A sum of per-chunk mixes is order-    */

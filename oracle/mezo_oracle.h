@@ -112,6 +112,41 @@ int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
                const uint32_t* K_t, const float* lr_t, uint32_t T,
                int kind, float scale, float alpha);
 
+/*
+ * Portable mode (Appendix B: the noise must be reproducible on any device).
+ * z is defined by a fixed sequence of IEEE binary32 operations (+, -, *, fma,
+ * correctly rounded / and sqrt, exact scalings; round-to-nearest-even), so
+ * every IEEE machine computes it bit for bit:
+ *   n1 = (w_a >> 8) + 1, e = floor(log2 n1), m = n1 * 2^-e in [1, 2);
+ *   if m >= fl32(sqrt 2): m = m/2, e = e+1;
+ *   f = m - 1; s = f / (f + 2); s2 = s*s;
+ *   p = fma(s2, fma(s2, fma(s2, fma(s2, 1/9, 1/7), 1/5), 1/3), 1);
+ *   ln_u1 = fma(e - 24, fl32(ln 2), (s + s) * p);     [ln m = 2 atanh s]
+ *   r = sqrt(-2 * ln_u1);
+ *   v = (w_b >> 8) * 2^-21 (= 8 u2); q = floor v; x = v - q;
+ *   y = q odd ? 1 - x : x; a = y * fl32(pi/4); a2 = a*a;
+ *   sin a = a * (1 + a2(-1/3! + a2(1/5! + a2(-1/7! + a2/9!))))   (Horner, fma),
+ *   cos a = 1 + a2(-1/2! + a2(1/4! + a2(-1/6! + a2(1/8! - a2/10!))));
+ *   octant q maps (cos a, sin a) to (cos 2 pi u2, sin 2 pi u2) by swaps
+ *   and sign flips; z = (r cos, r sin).
+ * (all coefficients rounded to binary32). The update then accumulates in
+ * binary32 as acc = fma(c_k, z_k, acc) for k ascending (zero c_k skipped) and
+ * theta' = round_st(theta + acc) with the sum in binary32.
+ */
+void  orc_box_muller_portable(const uint32_t w[4], float z[4]);
+float orc_z_portable(orc_seed_t s, uint32_t tensor_id, uint64_t e);
+int   orc_generate_portable(orc_seed_t s, uint32_t tensor_id, uint64_t first, uint64_t count,
+                            float* z);
+int   orc_perturb_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                           uint64_t first, uint64_t n, orc_seed_t s, float scale);
+int   orc_update_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                          uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+                          uint32_t K, int kind, float scale, float alpha, float lr);
+int   orc_replay_portable(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
+                          uint64_t first, uint64_t n, const orc_seed_t* seeds, const int8_t* q,
+                          const uint32_t* K_t, const float* lr_t, uint32_t T,
+                          int kind, float scale, float alpha);
+
 /* Checksum of a tensor's bits (ChecksumMatch, Algorithm 1: replicas compare a
  * hash of theta). The tensor's nbytes bytes are read as little-endian 8-byte
  * chunks c_j, the last one zero-padded; the result is
