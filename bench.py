@@ -77,6 +77,11 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="opt125m")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-ops", action="store_true",
+                   help="skip the per-operation measurements after the timed region (profiling runs)")
+    p.add_argument("--gaussian", choices=["fast", "portable"], default="fast",
+                   help="how z is computed (portable: binary32 operations only, bit-identical "
+                        "on any IEEE device)")
     p.add_argument("--probe", choices=["copy"], default=None,
                    help="copy: time a plain device copy of the parameter buffer instead")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -140,7 +145,8 @@ def main():
     if args.probe == "copy":
         copy_probe(torch, flat, args)
         return
-    ps = mezo.ParamSet(views)
+    gauss = mezo.GAUSS_PORTABLE if args.gaussian == "portable" else mezo.GAUSS_FAST
+    ps = mezo.ParamSet(views, gaussian=gauss)
     eps, lr = w.eps, w.lr
 
     total_steps = args.warmup + args.steps
@@ -157,31 +163,15 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def step(t, ev=None):
+    def step(t):
         s = (0, t, 0)
-        marks = []
-
-        def mark():
-            if ev is not None:
-                e = torch.cuda.Event(enable_timing=True)
-                e.record(stream)
-                marks.append(e)
-
-        mark()
         if w.T == 0:
             ps.perturb(s, eps)
-            mark()
             ps.perturb(s, -2 * eps)
-            mark()
             ps.perturb(s, eps)
-            mark()
             q = mezo.quantize_projgrad(proj[t])
             ps.update_multi(seeds_t[t], q, lr)
-            mark()
         ps.replay(log)
-        mark()
-        if ev is not None:
-            ev.append(marks)
 
     for t in range(args.warmup):
         step(t)
@@ -201,87 +191,21 @@ def main():
     ms_total = start.elapsed_time(end)
     ms_per_step = ms_total / args.steps
 
-    # ---- per-launch durations (same stream, event pairs around each call) ----
-    marks_all = []
-    torch.cuda.synchronize()
-    for t in range(args.warmup, total_steps):
-        step(t, marks_all)
-    torch.cuda.synchronize()
-    per_call = {c: [] for c in calls}
-    for marks in marks_all:
-        for c, a, b in zip(calls, marks[:-1], marks[1:]):
-            per_call[c].append(a.elapsed_time(b))
-    launch_ms = {c: float(np.mean(v)) for c, v in per_call.items()}
-
-    # Fused restore + update (Algorithm 1: theta = backup, then the apply loop)
-    # against a backup copy of the set: reported per op, not part of the step.
-    from_ms = None
-    if w.T == 0:
-        backup_flat = flat.clone()
-        bviews = [backup_flat[a:a + n] for a, n in offs]
-        backup = mezo.ParamSet(bviews)
-        q0 = mezo.quantize_projgrad(proj[0])
-        for _ in range(3):
-            ps.update_multi_from(backup, seeds_t[0], q0, lr)
-        torch.cuda.synchronize()
-        a_ev = torch.cuda.Event(enable_timing=True)
-        b_ev = torch.cuda.Event(enable_timing=True)
-        reps = max(3, args.steps // 2)
-        a_ev.record(stream)
-        for _ in range(reps):
-            ps.update_multi_from(backup, seeds_t[0], q0, lr)
-        b_ev.record(stream)
-        torch.cuda.synchronize()
-        from_ms = a_ev.elapsed_time(b_ev) / reps
-        backup.close()
-        del backup_flat, bviews
-
-    # ChecksumMatch: the replica check after the apply loop (read-only stream),
-    # reported per op, not part of the step.
-    ck = torch.empty(1, dtype=torch.int64, device=dev)
-    for _ in range(3):
-        ps.checksum_into(ck)
-    torch.cuda.synchronize()
-    a_ev = torch.cuda.Event(enable_timing=True)
-    b_ev = torch.cuda.Event(enable_timing=True)
-    a_ev.record(stream)
-    for _ in range(args.steps):
-        ps.checksum_into(ck)
-    b_ev.record(stream)
-    torch.cuda.synchronize()
-    ck_ms = a_ev.elapsed_time(b_ev) / args.steps
-
     value = ps_per_step * args.steps / (ms_total / 1e3)
     bytes_per_launch = 2 * N * (4 if w.dtype == "f32" else 2)
 
     # Engine kernel: every call of the step is one launch of it (per storage
-    # type; this set is all fp32). Achieved ALU work = param-seeds x minimal
-    # lane-instructions per param-seed over the launch time.
+    # type; the sets here have one). Its average launch duration is the timed
+    # region's GPU time over its launches (the step enqueues nothing else on
+    # the stream); achieved ALU work = param-seeds x minimal lane-instructions
+    # per param-seed over that time.
     n_launch = len(calls)
-    kernel_ms = sum(launch_ms[c] for c in calls)
+    avg_launch_s = ms_per_step / n_launch / 1e3
     ps_per_launch = ps_per_step / n_launch
-    avg_launch_s = kernel_ms / n_launch / 1e3
     achieved = ps_per_launch * INSTR_PER_PARAM_SEED / avg_launch_s / 1e12
     peak = VALU_LANE_INSTR_PER_S / 1e12
-    costs = issue_costs()
-    ops = {}
-    for c in launch_ms:
-        t_s = launch_ms[c] / 1e3
-        ops[c] = {"records": recs[c], "ms": round(launch_ms[c], 4),
-                  "param_seeds_per_s": N * recs[c] / t_s,
-                  "alg_GBps": bytes_per_launch / t_s / 1e9,
-                  "hbm_frac": bytes_per_launch / t_s / 1e9 / HBM_PEAK_GBS,
-                  "alu_frac": N * recs[c] * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S}
-    ck_bytes = bytes_per_launch / 2
-    ops["checksum"] = {"ms": round(ck_ms, 4), "alg_GBps": ck_bytes / (ck_ms / 1e3) / 1e9,
-                       "hbm_frac": ck_bytes / (ck_ms / 1e3) / 1e9 / HBM_PEAK_GBS}
-    if from_ms is not None:
-        t_s = from_ms / 1e3
-        ops["update_from_backup"] = {
-            "records": K, "ms": round(from_ms, 4), "param_seeds_per_s": N * K / t_s,
-            "alg_GBps": bytes_per_launch / t_s / 1e9,
-            "hbm_frac": bytes_per_launch / t_s / 1e9 / HBM_PEAK_GBS,
-            "alu_frac": N * K * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S}
+    ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args,
+                                               recs, proj, seeds_t, log, bytes_per_launch, gauss)
 
     out = {
         "metric": "param-seed updates/sec (params x K per s)",
@@ -301,20 +225,22 @@ def main():
                                   f"step = perturb +eps,-2eps,+eps; quantize {K} grads; "
                                   f"update_multi K={K}; replay T={t_log}xK={K}"),
                    "params": N, "tensors": w.n_tensors, "K": K, "replay_T": t_log,
+                   "gaussian": args.gaussian,
                    "eps": eps, "lr": lr, "param_seeds_per_step": ps_per_step},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak,
                      "unit": "Tinstr/s", "frac": achieved / peak,
-                     "traffic": measured_traffic(w.name),
+                     "traffic": measured_traffic(w.name, args.gaussian),
                      "alg_bytes_per_launch": bytes_per_launch,
                      "kernel": f"engine_kernel<{'inline' if max(recs[c] for c in calls) <= 32 else 'staged'}"
                                f" records, {w.dtype}>",
                      "instr_per_param_seed": INSTR_PER_PARAM_SEED,
                      "param_seeds_per_launch": ps_per_launch,
-                     "avg_launch_ms": kernel_ms / n_launch,
-                     "issue_cycles_isolated": {k: round(v, 3) for k, v in costs.items()}},
+                     "avg_launch_ms": avg_launch_s * 1e3},
         "wall_s_timed": wall,
-        "ops": ops,
     }
+    if ops is not None:
+        out["ops"] = ops
+        out["issue_cycles_isolated"] = {k: round(v, 3) for k, v in issue_costs().items()}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, recs, calls, log, args.cpu_seconds)
     print(json.dumps(out))
@@ -350,10 +276,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, gaussian: str = "fast"):
     """HBM bytes per engine launch from the committed counter profile of this
     workload, or None when there is none or the kernel sources changed since
     it was taken."""
+    if gaussian != "fast":
+        return None
     try:
         with open(TRAFFIC_PROFILE.format(workload=workload)) as f:
             prof = json.load(f)
@@ -362,6 +290,53 @@ def measured_traffic(workload: str):
     if prof.get("kernel_source_sha256") != kernel_source_hash():
         return None
     return prof["hbm_bytes_per_dispatch"]
+
+
+def measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args, recs, proj, seeds_t, log,
+                bytes_per_launch, gauss):
+    """Each operation alone, repeated back to back between two events on the
+    kernels' stream (after the timed region, not part of the step)."""
+    N, K, lr = w.numel, w.K, w.lr
+    reps = max(3, min(args.steps, 10))
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    def entry(records, ms, nbytes=bytes_per_launch):
+        t_s = ms / 1e3
+        e = {"ms": round(ms, 4), "alg_GBps": nbytes / t_s / 1e9,
+             "hbm_frac": nbytes / t_s / 1e9 / HBM_PEAK_GBS}
+        if records:
+            e.update({"records": records, "param_seeds_per_s": N * records / t_s,
+                      "alu_frac": N * records * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S})
+        return e
+
+    q0 = mezo.quantize_projgrad(proj[0])
+    ops = {}
+    if w.T == 0:
+        ops["perturb"] = entry(1, timed(lambda: ps.perturb((0, 0, 0), w.eps)))
+        ops["update"] = entry(K, timed(lambda: ps.update_multi(seeds_t[0], q0, lr)))
+    ops["replay"] = entry(recs["replay"], timed(lambda: ps.replay(log)))
+    ck = torch.empty(1, dtype=torch.int64, device=flat.device)
+    ops["checksum"] = entry(0, timed(lambda: ps.checksum_into(ck)), bytes_per_launch / 2)
+    if w.T == 0:
+        # Algorithm 1's restore of the backup fused into the apply loop
+        backup_flat = flat.clone()
+        backup = mezo.ParamSet([backup_flat[a:a + n] for a, n in offs], gaussian=gauss)
+        ops["update_from_backup"] = entry(K, timed(lambda: ps.update_multi_from(backup, seeds_t[0], q0, lr)))
+        backup.close()
+        del backup_flat
+    return ops
 
 
 def copy_probe(torch, flat, args):

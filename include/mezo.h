@@ -95,6 +95,18 @@ extern "C" {
                                      code 127 would decode past fp32 (alpha <
                                      ~1.4314) is MEZO_ERANGE.                 */
 
+/* How z is computed (a property of a training run: every machine must use
+ * the same one).
+ *  FAST:     hardware transcendentals (v_log, v_sqrt, v_sin, v_cos); z within
+ *            1e-6 * max|z| of the exact Box-Muller value; the default.
+ *  PORTABLE: z and the update from IEEE binary32 +, -, *, fma, correctly
+ *            rounded / and sqrt only (Appendix B: noise every device
+ *            reproduces), so any IEEE machine computes bit-identical z and
+ *            weights; about 2.5x the arithmetic of FAST. The steps are listed
+ *            in the design notes and mirrored by the CPU reference. */
+#define MEZO_GAUSS_FAST     0u
+#define MEZO_GAUSS_PORTABLE 1u
+
 /* Largest number of elements of one tensor (the counter holds e >> 2 in 32
  * bits). */
 #define MEZO_MAX_NUMEL (1ull << 34)
@@ -156,6 +168,13 @@ MEZO_API void mezo_paramset_destroy(mezo_paramset_t ps);
 
 /* Total number of elements of a paramset (0 for NULL). */
 MEZO_API uint64_t mezo_paramset_numel(mezo_paramset_t ps);
+
+/* Select how z is computed for every later call on ps (MEZO_GAUSS_FAST, the
+ * default, or MEZO_GAUSS_PORTABLE; MEZO_EINVAL otherwise). For the *_from
+ * calls the destination's setting applies. In portable mode the update is
+ *   acc = fma(c_k, z_k, acc) (k ascending, binary32), theta' = round(theta + acc)
+ * with the binary32 sum theta + acc rounded to the storage type. */
+MEZO_API int mezo_paramset_set_gaussian(mezo_paramset_t ps, uint32_t gaussian);
 
 /* ---- the engine ------------------------------------------------------- */
 
@@ -229,11 +248,13 @@ MEZO_API int mezo_dequantize(const int8_t* q, float* g, uint32_t n, const mezo_c
 /* ---- inspection -------------------------------------------------------- */
 
 /* Write the RNG word (words_dev[i] = word e & 3 of the block of element e)
- * and/or the Gaussian z_dev[i] of elements e = first_elem + i, i < count, of
- * tensor tensor_id under seed. Either device pointer may be NULL;
- * first_elem + count <= MEZO_MAX_NUMEL (MEZO_EINVAL). */
+ * and/or the Gaussian z_dev[i] (computed as `gaussian` says) of elements
+ * e = first_elem + i, i < count, of tensor tensor_id under seed. Either device
+ * pointer may be NULL; first_elem + count <= MEZO_MAX_NUMEL and a known
+ * `gaussian` (MEZO_EINVAL). */
 MEZO_API int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t first_elem,
-                        uint64_t count, uint32_t* words_dev, float* z_dev, void* stream);
+                                 uint64_t count, uint32_t gaussian, uint32_t* words_dev,
+                                 float* z_dev, void* stream);
 
 MEZO_API const char* mezo_strerror(int code);
 

@@ -3,7 +3,8 @@
     python -m paper_2306_10015_amd.build
 
 Flags that fix the arithmetic: -ffp-contract=off (only the fma the source
-writes is fused), no fast-math, and packed fp32 instructions disabled.
+writes is fused), no fast-math, correctly rounded fp32 / and sqrt (the
+portable Gaussian relies on them), and packed fp32 instructions disabled.
 """
 from __future__ import annotations
 
@@ -26,6 +27,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall", "-Wextra
 # Code object v5: loadable by the HIP runtime that ships with PyTorch as well
 # as by the system one.
 DEVICE = ["--offload-arch=" + ARCH, "-mcode-object-version=5",
+          "-fhip-fp32-correctly-rounded-divide-sqrt",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 

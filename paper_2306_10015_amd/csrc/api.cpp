@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -76,7 +77,9 @@ bool seed_less(const mezo_seed_t& a, const mezo_seed_t& b)
     return a.sample < b.sample;
 }
 
-mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last)
+// fold: multiply the coefficient by the sqrt(2 ln 2) the fast kernels leave
+// out of z (not for the portable Gaussian, whose kernels produce z itself).
+mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last, bool fold)
 {
     mezo::SeedRec r;
     r.key0 = static_cast<uint32_t>(s.machine);
@@ -85,7 +88,7 @@ mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last)
     const uint64_t p = uint64_t(mezo::kMulB) * uint64_t(s.sample);
     r.mb_hi = static_cast<uint32_t>(p >> 32);
     r.mb_lo = static_cast<uint32_t>(p);
-    r.coef = static_cast<float>(double(coef) * mezo::kZScaleF64);
+    r.coef = fold ? static_cast<float>(double(coef) * mezo::kZScaleF64) : coef;
     r.last = last ? 1u : 0u;
     r.sample = s.sample;
     return r;
@@ -94,7 +97,7 @@ mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last)
 // Checks one step of the apply loop and appends its records (zero weights
 // dropped; the step's last kept record is flagged to round to storage).
 int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t* codec,
-                float lr, std::vector<mezo::SeedRec>& out)
+                float lr, bool fold, std::vector<mezo::SeedRec>& out)
 {
     if (!codec) return MEZO_EINVAL;
     if (!codec_valid(codec) || !std::isfinite(lr)) return MEZO_ERANGE;
@@ -108,7 +111,7 @@ int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mez
     for (uint32_t k = 0; k < K; ++k) {
         // weight of perturbation k in the apply loop: -grad * lr (Algorithm 1)
         const float c = static_cast<float>(-double(lr) * double(decode(q[k], *codec)));
-        if (c != 0.0f) out.push_back(make_rec(seeds[k], c, false));
+        if (c != 0.0f) out.push_back(make_rec(seeds[k], c, false, fold));
     }
     if (out.size() > first) out.back().last = 1u;
     return MEZO_OK;
@@ -126,6 +129,7 @@ struct mezo_paramset {
     uint64_t total_tiles[2] = {0, 0};
     uint64_t numel = 0;
     int device = -1;
+    std::atomic<uint32_t> gaussian{MEZO_GAUSS_FAST};
     mezo::TensorDesc* d_table[2] = {nullptr, nullptr};
     uint32_t* d_tile_tensor[2] = {nullptr, nullptr};  // tensor index of every tile
     hipEvent_t last = nullptr;  // after the latest launch that reads a table
@@ -144,6 +148,8 @@ struct mezo_paramset {
 };
 
 namespace {
+
+bool fold_of(const mezo_paramset* ps) { return ps->gaussian.load() == MEZO_GAUSS_FAST; }
 
 // Device resources are made on first use, on the device current then.
 int ensure_device(mezo_paramset* ps)
@@ -240,7 +246,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
         args.src_tensors = src ? src->d_table[dt] : nullptr;
         args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
         args.total_tiles = ps->total_tiles[dt];
-        MEZO_HIP(mezo::launch_engine(args, dt, stream));
+        MEZO_HIP(mezo::launch_engine(args, dt, ps->gaussian.load() == MEZO_GAUSS_PORTABLE, stream));
     }
     if (slot) MEZO_HIP(hipEventRecord(slot->done, stream));
     MEZO_HIP(hipEventRecord(ps->last, stream));
@@ -353,12 +359,20 @@ void mezo_paramset_destroy(mezo_paramset_t ps)
 
 uint64_t mezo_paramset_numel(mezo_paramset_t ps) { return ps ? ps->numel : 0; }
 
+int mezo_paramset_set_gaussian(mezo_paramset_t ps, uint32_t gaussian)
+{
+    if (!ps || (gaussian != MEZO_GAUSS_FAST && gaussian != MEZO_GAUSS_PORTABLE)) return MEZO_EINVAL;
+    std::lock_guard<std::mutex> lock(ps->mu);
+    ps->gaussian.store(gaussian);
+    return MEZO_OK;
+}
+
 int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream)
 {
     if (!ps) return MEZO_EINVAL;
     if (!std::isfinite(scale)) return MEZO_ERANGE;
     if (scale == 0.0f) return MEZO_OK;
-    std::vector<mezo::SeedRec> recs(1, make_rec(seed, scale, true));
+    std::vector<mezo::SeedRec> recs(1, make_rec(seed, scale, true, fold_of(ps)));
     std::lock_guard<std::mutex> lock(ps->mu);
     return launch_records(ps, recs, static_cast<hipStream_t>(stream));
 }
@@ -369,7 +383,7 @@ int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t
     if (!ps) return MEZO_EINVAL;
     std::vector<mezo::SeedRec> recs;
     recs.reserve(K);
-    int rc = append_step(seeds, q, K, codec, lr, recs);
+    int rc = append_step(seeds, q, K, codec, lr, fold_of(ps), recs);
     if (rc) return rc;
     std::lock_guard<std::mutex> lock(ps->mu);
     return launch_records(ps, recs, static_cast<hipStream_t>(stream));
@@ -383,7 +397,7 @@ int mezo_perturb_from(mezo_paramset_t dst, mezo_paramset_t src, mezo_seed_t seed
     int rc = check_pair(dst, src);
     if (rc) return rc;
     std::vector<mezo::SeedRec> recs;
-    if (scale != 0.0f) recs.push_back(make_rec(seed, scale, true));
+    if (scale != 0.0f) recs.push_back(make_rec(seed, scale, true, fold_of(dst)));
     if (dst == src) {
         std::lock_guard<std::mutex> lock(dst->mu);
         return launch_records(dst, recs, static_cast<hipStream_t>(stream));
@@ -398,7 +412,7 @@ int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src, const mezo_
     if (!dst || !src) return MEZO_EINVAL;
     std::vector<mezo::SeedRec> recs;
     recs.reserve(K);
-    int rc = append_step(seeds, q, K, codec, lr, recs);
+    int rc = append_step(seeds, q, K, codec, lr, fold_of(dst), recs);
     if (rc) return rc;
     rc = check_pair(dst, src);
     if (rc) return rc;
@@ -422,7 +436,7 @@ int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const 
     for (uint32_t t = 0; t < T; ++t) total += steps[t].K;
     recs.reserve(total);
     for (uint32_t t = 0; t < T; ++t) {
-        int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, recs);
+        int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, fold_of(ps), recs);
         if (rc) return rc;
     }
     std::lock_guard<std::mutex> lock(ps->mu);
@@ -479,13 +493,15 @@ int mezo_dequantize(const int8_t* q, float* g, uint32_t n, const mezo_codec_t* c
 }
 
 int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t first_elem, uint64_t count,
-                        uint32_t* words_dev, float* z_dev, void* stream)
+                        uint32_t gaussian, uint32_t* words_dev, float* z_dev, void* stream)
 {
     if (first_elem > MEZO_MAX_NUMEL || count > MEZO_MAX_NUMEL - first_elem) return MEZO_EINVAL;
+    if (gaussian != MEZO_GAUSS_FAST && gaussian != MEZO_GAUSS_PORTABLE) return MEZO_EINVAL;
     if (count == 0 || (!words_dev && !z_dev)) return MEZO_OK;
     mezo::GenArgs a;
     std::memset(&a, 0, sizeof(a));
-    a.rec = make_rec(seed, 0.0f, false);
+    a.rec = make_rec(seed, 0.0f, false, false);
+    a.portable = gaussian == MEZO_GAUSS_PORTABLE ? 1u : 0u;
     a.tensor_id = tensor_id;
     a.first = first_elem;
     a.count = count;

@@ -150,6 +150,83 @@ __device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint
     return z;
 }
 
+// ---- portable Box-Muller ----------------------------------------------------
+// The same Gaussian from binary32 +, -, *, fma, correctly rounded / and sqrt
+// and exact scalings only, so that any IEEE device (a CPU included) computes
+// it bit for bit (Appendix B: identical noise on every machine). -ln u1 comes
+// from 2 atanh((m-1)/(m+1)) after an exact reduction of u1 to m 2^e with m in
+// [sqrt(1/2), sqrt(2)); sin and cos of 2 pi u2 from the eighth of a turn that
+// u2 falls in and Taylor polynomials on [0, pi/4] (coefficients 1/k! rounded
+// to binary32). Division and sqrt here are the compiler's correctly rounded
+// sequences (-fhip-fp32-correctly-rounded-divide-sqrt), not v_rcp / v_sqrt.
+__device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t wb, float& zc, float& zs)
+{
+    const uint32_t n1 = (wa >> 8) + 1u;                     // u1 = n1 2^-24, n1 >= 1
+    int e = 31 - __builtin_clz(n1);                         // floor(log2 n1)
+    float m = __builtin_ldexpf(float(n1), -e);              // exact, [1, 2)
+    if (m >= 0x1.6a09e6p+0f) {                              // fl32(sqrt 2)
+        m = m * 0.5f;
+        e = e + 1;
+    }
+    const float f = m - 1.0f;                               // exact
+    const float s = f / (f + 2.0f);
+    const float s2 = s * s;
+    float p = __builtin_fmaf(s2, 0x1.c71c72p-4f, 0x1.24924ap-3f);  // 1/9, 1/7
+    p = __builtin_fmaf(s2, p, 0x1.99999ap-3f);              // 1/5
+    p = __builtin_fmaf(s2, p, 0x1.555556p-2f);              // 1/3
+    p = __builtin_fmaf(s2, p, 1.0f);
+    const float ln_m = (s + s) * p;
+    const float ln_u1 = __builtin_fmaf(float(e - 24), 0x1.62e430p-1f, ln_m);  // + (e-24) ln 2
+    const float r = sqrtf(-2.0f * ln_u1);
+
+    const uint32_t t = wb >> 8;                             // u2 = t 2^-24
+    const float v = __builtin_ldexpf(float(t), -21);        // 8 u2, exact, [0, 8)
+    const int q = int(v);                                   // octant
+    const float x = v - float(q);                           // exact, [0, 1)
+    const float y = (q & 1) ? 1.0f - x : x;                 // exact, [0, 1]
+    const float a = y * 0x1.921fb6p-1f;                     // fl32(pi/4)
+    const float a2 = a * a;
+    float sn = __builtin_fmaf(a2, 0x1.71de3ap-19f, -0x1.a01a02p-13f);  // 1/9!, -1/7!
+    sn = __builtin_fmaf(a2, sn, 0x1.111112p-7f);            // 1/5!
+    sn = __builtin_fmaf(a2, sn, -0x1.555556p-3f);           // -1/3!
+    sn = __builtin_fmaf(a2, sn, 1.0f);
+    sn = a * sn;
+    float cs = __builtin_fmaf(a2, -0x1.27e4fcp-22f, 0x1.a01a02p-16f);  // -1/10!, 1/8!
+    cs = __builtin_fmaf(a2, cs, -0x1.6c16c2p-10f);          // -1/6!
+    cs = __builtin_fmaf(a2, cs, 0x1.555556p-5f);            // 1/4!
+    cs = __builtin_fmaf(a2, cs, -0.5f);                     // -1/2!
+    cs = __builtin_fmaf(a2, cs, 1.0f);
+    // angle = q pi/4 + a for even q, (q + 1) pi/4 - a for odd q
+    const bool swap = ((q + 1) >> 1) & 1;                   // octants 1, 2, 5, 6
+    const bool neg_cos = ((q + 2) >> 2) & 1;                // octants 2..5
+    const bool neg_sin = (q >> 2) & 1;                      // octants 4..7
+    float c0 = swap ? sn : cs;
+    float s0 = swap ? cs : sn;
+    if (neg_cos) c0 = -c0;
+    if (neg_sin) s0 = -s0;
+    zc = r * c0;
+    zs = r * s0;
+}
+
+__device__ __forceinline__ Z4 gauss4_portable(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+{
+    Z4 z;
+    box_muller_pair_portable(w0, w1, z.z0, z.z1);
+    box_muller_pair_portable(w2, w3, z.z2, z.z3);
+    return z;
+}
+
+// The Gaussians a kernel accumulates: portable ones are z itself; the fast
+// ones are z / sqrt(2 ln 2) (the factor is folded into the coefficient).
+template <bool kPortable>
+__device__ __forceinline__ Z4 gauss4_for_update(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+{
+    if constexpr (kPortable)
+        return gauss4_portable(w0, w1, w2, w3);
+    else
+        return gauss4_unit(w0, w1, w2, w3);
+}
+
 // ---- storage conversions ---------------------------------------------------
 
 __device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }

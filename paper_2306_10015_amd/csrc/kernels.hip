@@ -17,6 +17,8 @@
 // owned block is computed once and reused by every record; seed words, tensor
 // id and coefficient are wave-uniform and live in SGPRs (scalar loads from the
 // kernel arguments or from the staged record buffer).
+#include <atomic>
+
 #include "engine.hpp"
 #include "launch.hpp"
 
@@ -95,7 +97,7 @@ __device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t src, uin
 
 // One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
 // (one Philox block each).
-template <bool kInline>
+template <bool kInline, bool kPortable>
 __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& d, uint64_t src,
                                          uint64_t tile, const TileRaw<kGroupsF32>& raw)
 {
@@ -134,7 +136,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
         for (int g = 0; g < kGroups; ++g) {
             uint32_t w0, w1, w2, w3;
             philox_words(u, pre[g], w0, w1, w2, w3);
-            const Z4 z = gauss4_unit(w0, w1, w2, w3);
+            const Z4 z = gauss4_for_update<kPortable>(w0, w1, w2, w3);
             acc[g][0] = __builtin_fmaf(c, z.z0, acc[g][0]);
             acc[g][1] = __builtin_fmaf(c, z.z1, acc[g][1]);
             acc[g][2] = __builtin_fmaf(c, z.z2, acc[g][2]);
@@ -167,7 +169,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
 // One tile of a bf16 tensor: each lane owns kGroups groups of 8 elements (two
 // Philox blocks each). theta is held as fp32 holding a bf16 value; a step ends
 // with one RNE rounding back to bf16.
-template <bool kInline>
+template <bool kInline, bool kPortable>
 __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t src,
                                           uint64_t tile, const TileRaw<kGroupsBF16>& raw)
 {
@@ -215,7 +217,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
             for (int h = 0; h < 2; ++h) {
                 uint32_t w0, w1, w2, w3;
                 philox_words(u, pre[g][h], w0, w1, w2, w3);
-                const Z4 z = gauss4_unit(w0, w1, w2, w3);
+                const Z4 z = gauss4_for_update<kPortable>(w0, w1, w2, w3);
                 acc[g][4 * h + 0] = __builtin_fmaf(c, z.z0, acc[g][4 * h + 0]);
                 acc[g][4 * h + 1] = __builtin_fmaf(c, z.z1, acc[g][4 * h + 1]);
                 acc[g][4 * h + 2] = __builtin_fmaf(c, z.z2, acc[g][4 * h + 2]);
@@ -252,7 +254,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
     }
 }
 
-template <bool kInline, uint32_t kDtype>
+template <bool kInline, uint32_t kDtype, bool kPortable>
 __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
@@ -263,9 +265,9 @@ __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
     TileRaw<Layout<kDtype>::kGroups> raw;
     load_tile<kDtype>(d, src, tile - d.tile_begin, raw);
     if constexpr (kDtype == kF32)
-        tile_f32<kInline>(a, d, src, tile - d.tile_begin, raw);
+        tile_f32<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
     else
-        tile_bf16<kInline>(a, d, src, tile - d.tile_begin, raw);
+        tile_bf16<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
 }
 
 // Inspection: RNG words and Gaussians of a range of elements, one Philox
@@ -279,7 +281,7 @@ __global__ __launch_bounds__(kThreads) void generate_kernel(GenArgs a)
     const SeedUniform u = seed_uniform(a.rec, a.tensor_id);
     uint32_t w[4];
     philox_words(u, block_pre(uint32_t(blk)), w[0], w[1], w[2], w[3]);
-    const Z4 z4 = gauss4(w[0], w[1], w[2], w[3]);
+    const Z4 z4 = a.portable ? gauss4_portable(w[0], w[1], w[2], w[3]) : gauss4(w[0], w[1], w[2], w[3]);
     const float z[4] = {z4.z0, z4.z1, z4.z2, z4.z3};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -370,7 +372,24 @@ __global__ void zero_u64_kernel(unsigned long long* out)
 
 // ---- host-side launchers ----------------------------------------------------
 
-hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream)
+namespace {
+template <bool kInline, uint32_t kDtype, bool kPortable>
+void launch_one(const EngineArgs& args, dim3 g, dim3 b, hipStream_t stream)
+{
+    hipLaunchKernelGGL((engine_kernel<kInline, kDtype, kPortable>), g, b, 0, stream, args);
+}
+
+template <bool kInline, bool kPortable>
+void launch_dtype(const EngineArgs& args, uint32_t dtype, dim3 g, dim3 b, hipStream_t stream)
+{
+    if (dtype == kF32)
+        launch_one<kInline, kF32, kPortable>(args, g, b, stream);
+    else
+        launch_one<kInline, kBF16, kPortable>(args, g, b, stream);
+}
+}  // namespace
+
+hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, bool portable, hipStream_t stream)
 {
     if (args.total_tiles == 0) return hipSuccess;
     if (args.total_tiles > uint64_t(0x7FFFFFFF) || dtype > kBF16) return hipErrorInvalidValue;
@@ -378,15 +397,15 @@ hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t str
     const dim3 g{uint32_t(args.total_tiles)};
     const dim3 b{uint32_t(kThreads)};
     if (inl) {
-        if (dtype == kF32)
-            hipLaunchKernelGGL((engine_kernel<true, kF32>), g, b, 0, stream, args);
+        if (portable)
+            launch_dtype<true, true>(args, dtype, g, b, stream);
         else
-            hipLaunchKernelGGL((engine_kernel<true, kBF16>), g, b, 0, stream, args);
+            launch_dtype<true, false>(args, dtype, g, b, stream);
     } else {
-        if (dtype == kF32)
-            hipLaunchKernelGGL((engine_kernel<false, kF32>), g, b, 0, stream, args);
+        if (portable)
+            launch_dtype<false, true>(args, dtype, g, b, stream);
         else
-            hipLaunchKernelGGL((engine_kernel<false, kBF16>), g, b, 0, stream, args);
+            launch_dtype<false, false>(args, dtype, g, b, stream);
     }
     return hipGetLastError();
 }
@@ -419,16 +438,18 @@ hipError_t launch_generate(const GenArgs& args, hipStream_t stream)
 
 namespace {
 constexpr int kMaxDevices = 64;
-int g_cus[kMaxDevices] = {0};
+std::atomic<int> g_cus[kMaxDevices];  // compute units per device, 0 = not yet asked
 }  // namespace
 
 hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n_tables,
                            unsigned long long* out, int device, hipStream_t stream)
 {
     if (device < 0 || device >= kMaxDevices) return hipErrorInvalidValue;
-    if (g_cus[device] == 0) {
-        hipError_t e = hipDeviceGetAttribute(&g_cus[device], hipDeviceAttributeMultiprocessorCount, device);
+    int cus = g_cus[device].load(std::memory_order_relaxed);
+    if (cus == 0) {
+        hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
         if (e != hipSuccess) return e;
+        g_cus[device].store(cus, std::memory_order_relaxed);
     }
     hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, stream, out);
     hipError_t e = hipGetLastError();
@@ -436,7 +457,7 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
     for (int i = 0; i < n_tables; ++i) {
         if (tables[i].total_tiles == 0) continue;
         // as many workgroups as fill the device (8 per CU), each striding over tiles
-        const uint64_t cap = uint64_t(g_cus[device]) * 8;
+        const uint64_t cap = uint64_t(cus) * 8;
         const uint64_t grid = tables[i].total_tiles < cap ? tables[i].total_tiles : cap;
         const dim3 g{uint32_t(grid)};
         const dim3 b{uint32_t(kThreads)};

@@ -37,11 +37,13 @@ struct GenArgs {
     uint32_t* words;
     float* z;
     uint32_t tensor_id;
+    uint32_t portable;  // 1: the portable Gaussian
 };
 
 // Launch the engine over the tensors of one storage type (dtype): one
-// workgroup per tile (at most 2^31 - 1 tiles).
-hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, hipStream_t stream);
+// workgroup per tile (at most 2^31 - 1 tiles); portable selects the Gaussian
+// made of binary32 operations only.
+hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, bool portable, hipStream_t stream);
 hipError_t launch_generate(const GenArgs& args, hipStream_t stream);
 
 // Zero *out, then add the checksum of every table given (one launch each).

@@ -27,6 +27,7 @@ LIB_PATH = Path(__file__).resolve().parent / "libmezo.so"
 
 OK, EINVAL, EDTYPE, EOVERLAP, EORDER, ERANGE, EHIP = 0, -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
+GAUSS_FAST, GAUSS_PORTABLE = 0, 1
 LINEAR, SIGNED_LOG = 0, 1
 #: Signed-log slope of a base-2 log: code 127 decodes just inside fp32.
 LOG2_ALPHA = 1.0 / math.log(2.0)
@@ -57,6 +58,7 @@ class Step(ctypes.Structure):
 
 #: Every symbol include/mezo.h declares.
 EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
+           "mezo_paramset_set_gaussian",
            "mezo_perturb", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
            "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
            "mezo_dequantize", "mezo_debug_generate", "mezo_strerror", "mezo_last_error",
@@ -80,6 +82,8 @@ def _load() -> ctypes.CDLL:
     L.mezo_paramset_destroy.restype = None
     L.mezo_paramset_numel.argtypes = [vp]
     L.mezo_paramset_numel.restype = u64
+    L.mezo_paramset_set_gaussian.argtypes = [vp, u32]
+    L.mezo_paramset_set_gaussian.restype = i32
     L.mezo_perturb.argtypes = [vp, Seed, f32, vp]
     L.mezo_perturb.restype = i32
     L.mezo_update_multi.argtypes = [vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
@@ -96,7 +100,7 @@ def _load() -> ctypes.CDLL:
     L.quantize_projgrad.restype = i32
     L.mezo_dequantize.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
     L.mezo_dequantize.restype = i32
-    L.mezo_debug_generate.argtypes = [Seed, u32, u64, u64, vp, vp, vp]
+    L.mezo_debug_generate.argtypes = [Seed, u32, u64, u64, u32, vp, vp, vp]
     L.mezo_debug_generate.restype = i32
     L.mezo_strerror.argtypes = [i32]
     L.mezo_strerror.restype = ctypes.c_char_p
@@ -173,7 +177,8 @@ class ParamSet:
     tensor's noise stream and must be the same on every machine.
     """
 
-    def __init__(self, tensors: Sequence, tensor_ids: Iterable[int] | None = None):
+    def __init__(self, tensors: Sequence, tensor_ids: Iterable[int] | None = None,
+                 gaussian: int = GAUSS_FAST):
         self.tensors = list(tensors)
         ids = list(range(len(self.tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
         if len(ids) != len(self.tensors):
@@ -188,6 +193,13 @@ class ParamSet:
                "mezo_paramset_create")
         self._h = h
         self.tensor_ids = ids
+        if gaussian != GAUSS_FAST:
+            self.set_gaussian(gaussian)
+
+    def set_gaussian(self, gaussian: int) -> None:
+        """GAUSS_FAST (hardware transcendentals) or GAUSS_PORTABLE (binary32
+        operations only: bit-identical on any IEEE device)."""
+        _check(lib.mezo_paramset_set_gaussian(self._h, int(gaussian)), "mezo_paramset_set_gaussian")
 
     @property
     def handle(self) -> ctypes.c_void_p:
@@ -286,14 +298,14 @@ def dequantize(q, codec_: Codec = DEFAULT_CODEC) -> np.ndarray:
 
 
 def debug_generate(seed, tensor_id: int, first: int, count: int, words=True, z=True,
-                   stream=None):
+                   stream=None, gaussian: int = GAUSS_FAST):
     """Device tensors (words uint32 as int32 bits, z float32) of elements
     first .. first+count-1 of tensor tensor_id under seed."""
     import torch
     w = torch.empty(count, dtype=torch.int32, device="cuda") if words else None
     zz = torch.empty(count, dtype=torch.float32, device="cuda") if z else None
     _check(lib.mezo_debug_generate(_seed(seed), int(tensor_id), int(first), int(count),
-                                   None if w is None else w.data_ptr(),
+                                   int(gaussian), None if w is None else w.data_ptr(),
                                    None if zz is None else zz.data_ptr(), _stream_ptr(stream)),
            "mezo_debug_generate")
     return w, zz

@@ -174,9 +174,20 @@ def test_perturb_and_replay_argument_checks(fake_ps):
 
 def test_debug_generate_range_check():
     lib = mezo.lib
-    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, (1 << 34) - 4, 8, 0x1000, None, None) == mezo.EINVAL
-    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 0, 0x1000, None, None) == mezo.OK
-    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 16, None, None, None) == mezo.OK
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, (1 << 34) - 4, 8, 0, 0x1000, None, None) == mezo.EINVAL
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 16, 7, 0x1000, None, None) == mezo.EINVAL
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 0, 0, 0x1000, None, None) == mezo.OK
+    assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, 0, 16, 1, None, None, None) == mezo.OK
+
+
+def test_gaussian_mode_setter():
+    rc, h = create([(0x1000, 16, 0, mezo.F32)])
+    assert rc == mezo.OK
+    assert mezo.lib.mezo_paramset_set_gaussian(h, mezo.GAUSS_PORTABLE) == mezo.OK
+    assert mezo.lib.mezo_paramset_set_gaussian(h, mezo.GAUSS_FAST) == mezo.OK
+    assert mezo.lib.mezo_paramset_set_gaussian(h, 2) == mezo.EINVAL
+    assert mezo.lib.mezo_paramset_set_gaussian(None, 0) == mezo.EINVAL
+    mezo.lib.mezo_paramset_destroy(h)
 
 
 def test_strerror_covers_every_code():
