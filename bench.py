@@ -26,6 +26,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -43,6 +44,10 @@ sys.path.insert(0, ROOT)
 CLOCK_GHZ = 2.4
 VALU_LANE_INSTR_PER_S = 256 * 4 * 16 * CLOCK_GHZ * 1e9
 HBM_PEAK_GBS = 8000.0
+# each call timed alone: repeated for about this long (at least 3, at most
+# OPS_MAX_REPS launches)
+OPS_LOOP_MS = 30.0
+OPS_MAX_REPS = 400
 
 #: VALU instructions per Philox block (4 Gaussians) per seed in the engine's
 #: inner loop, the method's minimal sequence on gfx950: round 1 and the
@@ -50,14 +55,15 @@ HBM_PEAK_GBS = 8000.0
 #: 2..10 cost 17 wide multiplies (v_mad_u64_u32), 16 three-way xors
 #: (v_bitop3_b32) and 3 xors; Box-Muller per pair of Gaussians (radius factor
 #: sqrt(2 ln 2) folded into the coefficient): 2 shifts, 2 int->float
-#: conversions, one fma forming u1, 3 muls, log2, sqrt, sin, cos; and one fma
-#: per Gaussian accumulating c_k * z.
+#: conversions, one fma forming u1, 2 muls (u2's scale, c_k times the radius),
+#: log2, sqrt, sin, cos; and one fma per Gaussian accumulating into theta's
+#: increment.
 INNER_LOOP_MIX = {
     "v_mad_u64_u32": 17, "v_bitop3_b32": 16, "v_xor_b32": 3, "v_lshrrev_b32": 4,
-    "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 6, "v_log_f32": 2, "v_sqrt_f32": 2,
+    "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 4, "v_log_f32": 2, "v_sqrt_f32": 2,
     "v_sin_f32": 2, "v_cos_f32": 2, "v_fmac_f32": 4,
 }
-#: lane-instructions per param-seed (= 64 / 4)
+#: lane-instructions per param-seed (= 62 / 4)
 INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
 
 #: counter profile of the engine kernel on this workload (FETCH_SIZE /
@@ -297,12 +303,8 @@ def measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args, recs, proj,
     """Each operation alone, repeated back to back between two events on the
     kernels' stream (after the timed region, not part of the step)."""
     N, K, lr = w.numel, w.K, w.lr
-    reps = max(3, min(args.steps, 10))
 
-    def timed(fn):
-        for _ in range(2):
-            fn()
-        torch.cuda.synchronize()
+    def loop(fn, reps):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record(stream)
@@ -311,6 +313,15 @@ def measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args, recs, proj,
         b.record(stream)
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
+
+    def timed(fn):
+        # warm up, then repeat for about OPS_LOOP_MS so that short calls are
+        # timed over many launches at the clock a long run settles at
+        fn()
+        torch.cuda.synchronize()
+        once = loop(fn, 1)
+        reps = max(3, min(OPS_MAX_REPS, math.ceil(OPS_LOOP_MS / max(once, 1e-3))))
+        return loop(fn, reps)
 
     def entry(records, ms, nbytes=bytes_per_launch):
         t_s = ms / 1e3

@@ -32,9 +32,11 @@
  * the GPU's transcendental instructions (absolute error below 1e-6 * max|z|).
  *
  * Arithmetic. theta is loaded into fp32 (bf16 exactly), the perturbations are
- * accumulated in fp32 for k ascending as acc = fma(c'_k, y_k, acc), where
- * y_k = z_k / sqrt(2 ln 2) (the constant factor of Box-Muller's radius is
- * taken out of the per-element work) and c'_k = fl32(c_k * sqrt(2 ln 2));
+ * accumulated in fp32 for k ascending, per Box-Muller pair as
+ *     cr = c'_k * rho,  acc_c = fma(cr, cos 2 pi u2, acc_c),
+ *                       acc_s = fma(cr, sin 2 pi u2, acc_s),
+ * where rho = sqrt(-log2 u1) = z's radius / sqrt(2 ln 2) (the constant factor
+ * is taken out of the per-element work) and c'_k = fl32(c_k * sqrt(2 ln 2));
  * then theta' = round(theta + acc) to the storage type, round-to-nearest-even;
  * subnormals are kept.
  *

@@ -131,6 +131,19 @@ __device__ __forceinline__ void box_muller_pair_unit(uint32_t wa, uint32_t wb, f
     zs = r * __builtin_amdgcn_sinf(u2);
 }
 
+// acc_c += c z_c and acc_s += c z_s for one pair, with c the record's
+// coefficient (which carries sqrt(2 ln 2)): c r is formed once and scales
+// cos and sin inside the two fmas, so the pair costs one multiply.
+__device__ __forceinline__ void box_muller_pair_acc(uint32_t wa, uint32_t wb, float c, float& acc_c, float& acc_s)
+{
+    constexpr float kTwoM24 = 0x1p-24f;
+    const float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
+    const float u2 = float(wb >> 8) * kTwoM24;
+    const float cr = c * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1));
+    acc_c = __builtin_fmaf(cr, __builtin_amdgcn_cosf(u2), acc_c);
+    acc_s = __builtin_fmaf(cr, __builtin_amdgcn_sinf(u2), acc_s);
+}
+
 __device__ __forceinline__ Z4 gauss4_unit(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
 {
     Z4 z;
@@ -216,15 +229,23 @@ __device__ __forceinline__ Z4 gauss4_portable(uint32_t w0, uint32_t w1, uint32_t
     return z;
 }
 
-// The Gaussians a kernel accumulates: portable ones are z itself; the fast
-// ones are z / sqrt(2 ln 2) (the factor is folded into the coefficient).
+// acc_j += c z_j for the four Gaussians of one Philox block. Portable mode:
+// the portable z, then fma(c, z, acc) as its definition states. Fast mode: c
+// carries sqrt(2 ln 2), and each pair forms c r once (box_muller_pair_acc).
 template <bool kPortable>
-__device__ __forceinline__ Z4 gauss4_for_update(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3)
+__device__ __forceinline__ void accumulate4(float c, uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                            float& a0, float& a1, float& a2, float& a3)
 {
-    if constexpr (kPortable)
-        return gauss4_portable(w0, w1, w2, w3);
-    else
-        return gauss4_unit(w0, w1, w2, w3);
+    if constexpr (kPortable) {
+        const Z4 z = gauss4_portable(w0, w1, w2, w3);
+        a0 = __builtin_fmaf(c, z.z0, a0);
+        a1 = __builtin_fmaf(c, z.z1, a1);
+        a2 = __builtin_fmaf(c, z.z2, a2);
+        a3 = __builtin_fmaf(c, z.z3, a3);
+    } else {
+        box_muller_pair_acc(w0, w1, c, a0, a1);
+        box_muller_pair_acc(w2, w3, c, a2, a3);
+    }
 }
 
 // ---- storage conversions ---------------------------------------------------

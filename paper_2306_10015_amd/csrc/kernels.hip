@@ -136,11 +136,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
         for (int g = 0; g < kGroups; ++g) {
             uint32_t w0, w1, w2, w3;
             philox_words(u, pre[g], w0, w1, w2, w3);
-            const Z4 z = gauss4_for_update<kPortable>(w0, w1, w2, w3);
-            acc[g][0] = __builtin_fmaf(c, z.z0, acc[g][0]);
-            acc[g][1] = __builtin_fmaf(c, z.z1, acc[g][1]);
-            acc[g][2] = __builtin_fmaf(c, z.z2, acc[g][2]);
-            acc[g][3] = __builtin_fmaf(c, z.z3, acc[g][3]);
+            accumulate4<kPortable>(c, w0, w1, w2, w3, acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
         }
         if (rec.last) {
 #pragma unroll
@@ -166,47 +162,25 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
     }
 }
 
-// One tile of a bf16 tensor: each lane owns kGroups groups of 8 elements (two
-// Philox blocks each). theta is held as fp32 holding a bf16 value; a step ends
-// with one RNE rounding back to bf16.
+// A lane's bf16 groups of 8 elements (two Philox blocks each) through all
+// records. theta stays packed: after every step it is a bf16 value again, so
+// the packed pairs lose nothing; a step ends with one RNE rounding of
+// theta + acc.
 template <bool kInline, bool kPortable>
-__device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t src,
-                                          uint64_t tile, const TileRaw<kGroupsBF16>& raw)
+__device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t tile,
+                                            uint32_t (&th)[kGroupsBF16][4])
 {
     constexpr int kGroups = kGroupsBF16;
-    const gu16_t* in = reinterpret_cast<const gu16_t*>(src);
-    gu16_t* out = reinterpret_cast<gu16_t*>(d.data);
-    const uint64_t numel = d.numel;
-    float th[kGroups][8];
     float acc[kGroups][8];
     BlockPre pre[kGroups][2];
-    uint64_t e0[kGroups];
-
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         const uint64_t grp = group_index<kGroups>(tile, g);
-        e0[g] = grp * 8;
-        if (e0[g] + 8 <= numel) {
-            const uint4 v = raw.g[g];
-            th[g][0] = bf16_lo(v.x);
-            th[g][1] = bf16_hi(v.x);
-            th[g][2] = bf16_lo(v.y);
-            th[g][3] = bf16_hi(v.y);
-            th[g][4] = bf16_lo(v.z);
-            th[g][5] = bf16_hi(v.z);
-            th[g][6] = bf16_lo(v.w);
-            th[g][7] = bf16_hi(v.w);
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j)
-                th[g][j] = (e0[g] + j < numel) ? __uint_as_float(uint32_t(in[e0[g] + j]) << 16) : 0.0f;
-        }
         pre[g][0] = block_pre(uint32_t(2 * grp));
         pre[g][1] = block_pre(uint32_t(2 * grp + 1));
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[g][j] = 0.0f;
     }
-
     for (uint32_t r = 0; r < a.n_rec; ++r) {
         const SeedRec& rec = rec_at<kInline>(a, r);
         const SeedUniform u = seed_uniform(rec, d.tensor_id);
@@ -217,39 +191,59 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
             for (int h = 0; h < 2; ++h) {
                 uint32_t w0, w1, w2, w3;
                 philox_words(u, pre[g][h], w0, w1, w2, w3);
-                const Z4 z = gauss4_for_update<kPortable>(w0, w1, w2, w3);
-                acc[g][4 * h + 0] = __builtin_fmaf(c, z.z0, acc[g][4 * h + 0]);
-                acc[g][4 * h + 1] = __builtin_fmaf(c, z.z1, acc[g][4 * h + 1]);
-                acc[g][4 * h + 2] = __builtin_fmaf(c, z.z2, acc[g][4 * h + 2]);
-                acc[g][4 * h + 3] = __builtin_fmaf(c, z.z3, acc[g][4 * h + 3]);
+                accumulate4<kPortable>(c, w0, w1, w2, w3, acc[g][4 * h + 0], acc[g][4 * h + 1],
+                                       acc[g][4 * h + 2], acc[g][4 * h + 3]);
             }
         if (rec.last) {
 #pragma unroll
             for (int g = 0; g < kGroups; ++g)
 #pragma unroll
-                for (int j = 0; j < 8; j += 2) {
-                    const uint32_t p = pack_bf16(th[g][j] + acc[g][j], th[g][j + 1] + acc[g][j + 1]);
-                    th[g][j] = bf16_lo(p);
-                    th[g][j + 1] = bf16_hi(p);
-                    acc[g][j] = 0.0f;
-                    acc[g][j + 1] = 0.0f;
+                for (int j = 0; j < 4; ++j) {
+                    th[g][j] = pack_bf16(bf16_lo(th[g][j]) + acc[g][2 * j], bf16_hi(th[g][j]) + acc[g][2 * j + 1]);
+                    acc[g][2 * j] = 0.0f;
+                    acc[g][2 * j + 1] = 0.0f;
                 }
         }
     }
+}
 
+// One tile of a bf16 tensor: each lane owns kGroupsBF16 groups of 8 elements.
+template <bool kInline, bool kPortable>
+__device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t src,
+                                          uint64_t tile, const TileRaw<kGroupsBF16>& raw)
+{
+    constexpr int kGroups = kGroupsBF16;
+    const gu16_t* in = reinterpret_cast<const gu16_t*>(src);
+    gu16_t* out = reinterpret_cast<gu16_t*>(d.data);
+    const uint64_t numel = d.numel;
+    uint32_t th[kGroups][4];
+    uint64_t e0[kGroups];
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        e0[g] = group_index<kGroups>(tile, g) * 8;
+        if (e0[g] + 8 <= numel) {
+            th[g][0] = raw.g[g].x;
+            th[g][1] = raw.g[g].y;
+            th[g][2] = raw.g[g].z;
+            th[g][3] = raw.g[g].w;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t lo = (e0[g] + 2 * j < numel) ? uint32_t(in[e0[g] + 2 * j]) : 0u;
+                const uint32_t hi = (e0[g] + 2 * j + 1 < numel) ? uint32_t(in[e0[g] + 2 * j + 1]) : 0u;
+                th[g][j] = lo | (hi << 16);
+            }
+        }
+    }
+    groups_bf16<kInline, kPortable>(a, d, tile, th);
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         if (e0[g] + 8 <= numel) {
-            uint4 v;
-            v.x = pack_bf16(th[g][0], th[g][1]);
-            v.y = pack_bf16(th[g][2], th[g][3]);
-            v.z = pack_bf16(th[g][4], th[g][5]);
-            v.w = pack_bf16(th[g][6], th[g][7]);
-            store_stream(d.data + e0[g] * 2, v);
+            store_stream(d.data + e0[g] * 2, make_uint4(th[g][0], th[g][1], th[g][2], th[g][3]));
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if (e0[g] + j < numel) out[e0[g] + j] = to_bf16(th[g][j]);
+                if (e0[g] + j < numel) out[e0[g] + j] = uint16_t(th[g][j >> 1] >> (16 * (j & 1)));
         }
     }
 }

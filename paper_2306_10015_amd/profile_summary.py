@@ -72,7 +72,7 @@ def main():
     ap.add_argument("--elements", type=int, required=True)
     ap.add_argument("--elem-bytes", type=int, required=True)
     ap.add_argument("--records", default="", help="records per dispatch, cycling (e.g. 1,1,1,8,32)")
-    ap.add_argument("--instr-per-param-seed", type=float, default=16.0)
+    ap.add_argument("--instr-per-param-seed", type=float, default=15.5)
     ap.add_argument("--commands", help="text file with the commands that made the inputs")
     ap.add_argument("--outdir", default=os.path.join(ROOT, "profiles"))
     a = ap.parse_args()
