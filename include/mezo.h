@@ -87,6 +87,13 @@ extern "C" {
 /* ---- storage types and codecs ---------------------------------------- */
 #define MEZO_F32  0u      /* IEEE binary32                                    */
 #define MEZO_BF16 1u      /* bfloat16: top 16 bits of a binary32              */
+#define MEZO_NF4  2u      /* 4-bit NormalFloat in blocks of 64 elements with an
+                             fp32 absmax per block (the 4-bit forward-only
+                             variant, Section 3, in QLoRA's format, which the
+                             paper cites there); see mezo_tensor_t          */
+
+/* NF4 blocks: elements per absmax value. */
+#define MEZO_NF4_BLOCK 64u
 
 #define MEZO_CODEC_LINEAR     0u  /* q = clamp(rne(g / scale), -127, 127);
                                      g~ = fl32(q * scale)                     */
@@ -125,12 +132,24 @@ typedef struct {
 /* One parameter tensor: `numel` contiguous elements at device address
  * `data` (16-byte aligned), storage `dtype`. `tensor_id` selects the tensor's
  * noise stream and must be unique within a paramset; keep it stable across
- * machines (e.g. the registration order of the model's parameters). */
+ * machines (e.g. the registration order of the model's parameters).
+ *
+ * MEZO_NF4: `data` holds ceil(numel / 2) bytes of 4-bit codes, element 2i in
+ * the low nibble of byte i (for odd numel the last high nibble is written as
+ * 0); `absmax` (16-byte aligned) holds ceil(numel / 64) fp32 values, one per
+ * block of 64 consecutive elements (the last block may be shorter). Element e
+ * is v[code_e] * absmax[e / 64], v the 16 NF4 values. Every call quantizes
+ * again at the end of each step it applies: with w' the block's fp32 values
+ * after the step, a' = max |w'|, r = fl32(1 / a') (0 when a' = 0),
+ * x = fl32(w' * r), and the new code is the number of NF4 midpoints
+ * fl32((v_i + v_{i+1}) / 2) strictly below x (the nearest value, ties to the
+ * lower code). For MEZO_F32 and MEZO_BF16 `absmax` must be NULL. */
 typedef struct {
     void*    data;
     uint64_t numel;
     uint32_t tensor_id;
     uint32_t dtype;
+    void*    absmax;
 } mezo_tensor_t;
 
 /* One-byte gradient code (Section 3). `scale` is used by LINEAR, `alpha` by
@@ -157,8 +176,10 @@ typedef struct mezo_paramset* mezo_paramset_t;
 
 /* Register n tensors (copied; the array may be reused). Checks: t and out
  * non-null, n >= 1, every data non-null and 16-byte aligned, 1 <= numel <=
- * MEZO_MAX_NUMEL (else MEZO_EINVAL), dtype known (MEZO_EDTYPE), tensor_ids
- * unique (MEZO_EINVAL), no two tensors overlapping in memory (MEZO_EOVERLAP).
+ * MEZO_MAX_NUMEL, absmax 16-byte aligned for MEZO_NF4 and NULL otherwise
+ * (else MEZO_EINVAL), dtype known (MEZO_EDTYPE), tensor_ids unique
+ * (MEZO_EINVAL), no two tensors (codes and absmax arrays included)
+ * overlapping in memory (MEZO_EOVERLAP).
  * Device resources are created on the current HIP device at the first launch;
  * every later call must be made with that same device current (MEZO_EINVAL
  * otherwise). */
@@ -234,9 +255,29 @@ MEZO_API int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src,
  * mod 2^64, fmix64 being MurmurHash3's 64-bit finalizer. The sum does not
  * depend on how tensors are grouped into paramsets or in which order they were
  * registered (the checksum of a model split over several paramsets is the sum
- * of theirs). Written asynchronously to out_dev, a device pointer to 8 bytes
+ * of theirs). An MEZO_NF4 tensor's bytes are its ceil(numel / 2) code bytes
+ * zero-padded to a multiple of 8, followed by its absmax values (chunk numbers
+ * continue). Written asynchronously to out_dev, a device pointer to 8 bytes
  * (8-byte aligned; MEZO_EINVAL otherwise), on stream. */
 MEZO_API int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream);
+
+/* ---- 4-bit storage (Section 3, the 4-bit forward-only variant) -------- */
+
+/* Quantize n values of storage src_dtype (MEZO_F32 or MEZO_BF16) at device
+ * address src into NF4: ceil(n / 2) code bytes at `codes` and ceil(n / 64)
+ * fp32 absmax values at `absmax`, by the rule under mezo_tensor_t. The caller
+ * owns all three buffers (device memory, 16-byte aligned, not overlapping;
+ * MEZO_EINVAL / MEZO_EDTYPE / MEZO_EOVERLAP otherwise; 1 <= n <=
+ * MEZO_MAX_NUMEL). Asynchronous on stream. */
+MEZO_API int mezo_nf4_quantize(const void* src, uint32_t src_dtype, uint64_t n, void* codes,
+                               float* absmax, void* stream);
+
+/* Dequantize n NF4 elements into dst of storage dst_dtype (MEZO_F32: the
+ * value fl32(v[code] * absmax); MEZO_BF16: that value rounded to bf16, to
+ * nearest even) — what a forward pass over the 4-bit weights reads. Same
+ * ownership, alignment and checks as mezo_nf4_quantize. */
+MEZO_API int mezo_nf4_dequantize(const void* codes, const float* absmax, uint64_t n, void* dst,
+                                 uint32_t dst_dtype, void* stream);
 
 /* ---- the one-byte gradient (host, pure) ------------------------------- */
 

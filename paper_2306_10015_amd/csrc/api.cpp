@@ -11,7 +11,6 @@
 #include <mutex>
 #include <new>
 #include <string>
-#include <tuple>
 #include <vector>
 
 #include "../../include/mezo.h"
@@ -122,16 +121,17 @@ int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mez
 // ---- paramset -----------------------------------------------------------------
 
 struct mezo_paramset {
+    static constexpr int kTypes = static_cast<int>(mezo::kStorageTypes);
     std::mutex mu;
     // One table per storage type (index = dtype), each in registration order
     // with tile_begin ascending; the engine runs one launch per non-empty table.
-    std::vector<mezo::TensorDesc> table[2];
-    uint64_t total_tiles[2] = {0, 0};
+    std::vector<mezo::TensorDesc> table[kTypes];
+    uint64_t total_tiles[kTypes] = {};
     uint64_t numel = 0;
     int device = -1;
     std::atomic<uint32_t> gaussian{MEZO_GAUSS_FAST};
-    mezo::TensorDesc* d_table[2] = {nullptr, nullptr};
-    uint32_t* d_tile_tensor[2] = {nullptr, nullptr};  // tensor index of every tile
+    mezo::TensorDesc* d_table[kTypes] = {};
+    uint32_t* d_tile_tensor[kTypes] = {};  // tensor index of every tile
     hipEvent_t last = nullptr;  // after the latest launch that reads a table
 
     // Staging of record lists too long for the kernel arguments: a ring of
@@ -164,7 +164,7 @@ int ensure_device(mezo_paramset* ps)
         return MEZO_OK;
     }
     hipError_t e = hipSuccess;
-    for (int dt = 0; dt < 2 && e == hipSuccess; ++dt) {
+    for (int dt = 0; dt < mezo_paramset::kTypes && e == hipSuccess; ++dt) {
         const std::vector<mezo::TensorDesc>& tab = ps->table[dt];
         if (tab.empty()) continue;
         const size_t bytes = tab.size() * sizeof(mezo::TensorDesc);
@@ -183,7 +183,7 @@ int ensure_device(mezo_paramset* ps)
     }
     if (e == hipSuccess) e = hipEventCreateWithFlags(&ps->last, hipEventDisableTiming);
     if (e != hipSuccess) {
-        for (int dt = 0; dt < 2; ++dt) {
+        for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
             if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
             ps->d_table[dt] = nullptr;
@@ -239,7 +239,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
                                 hipMemcpyHostToDevice, stream));
         args.ext = slot->dev;
     }
-    for (uint32_t dt = 0; dt < 2; ++dt) {
+    for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
         if (ps->table[dt].empty()) continue;
         args.tensors = ps->d_table[dt];
         args.tile_tensor = ps->d_tile_tensor[dt];
@@ -254,31 +254,57 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
     return MEZO_OK;
 }
 
+// Byte ranges [begin, end) of device memory a tensor occupies.
+using Span = std::pair<uint64_t, uint64_t>;
+
+uint64_t nf4_code_bytes(uint64_t n) { return (n + 1) / 2; }
+uint64_t nf4_absmax_bytes(uint64_t n) { return 4 * ((n + MEZO_NF4_BLOCK - 1) / MEZO_NF4_BLOCK); }
+
+void add_spans(uint64_t data, uint64_t aux, uint64_t numel, uint32_t dtype, std::vector<Span>& out)
+{
+    if (dtype == MEZO_NF4) {
+        out.emplace_back(data, data + nf4_code_bytes(numel));
+        out.emplace_back(aux, aux + nf4_absmax_bytes(numel));
+    } else {
+        out.emplace_back(data, data + numel * (dtype == MEZO_F32 ? 4 : 2));
+    }
+}
+
+bool disjoint(std::vector<Span>& spans)
+{
+    std::sort(spans.begin(), spans.end());
+    uint64_t reach = 0;
+    for (const auto& sp : spans) {
+        if (sp.first < reach) return false;
+        reach = std::max(reach, sp.second);
+    }
+    return true;
+}
+
+uint64_t tile_of(uint32_t dtype)
+{
+    return dtype == MEZO_F32 ? mezo::kTileF32 : (dtype == MEZO_BF16 ? mezo::kTileBF16 : mezo::kTileNF4);
+}
+
 // dst and src describe the same tensors (count, ids, sizes, storage types, in
 // registration order per storage type) and share no memory except where a
 // tensor is its own source.
 int check_pair(const mezo_paramset* dst, const mezo_paramset* src)
 {
     if (dst == src) return MEZO_OK;
-    std::vector<std::tuple<uint64_t, uint64_t>> spans;
-    for (int dt = 0; dt < 2; ++dt) {
+    std::vector<Span> spans;
+    for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
         const auto& a = dst->table[dt];
         const auto& b = src->table[dt];
         if (a.size() != b.size()) return MEZO_EINVAL;
-        const uint64_t esz = dt == 0 ? 4 : 2;
         for (size_t i = 0; i < a.size(); ++i) {
             if (a[i].numel != b[i].numel || a[i].tensor_id != b[i].tensor_id) return MEZO_EINVAL;
-            spans.emplace_back(a[i].data, a[i].data + a[i].numel * esz);
-            if (b[i].data != a[i].data) spans.emplace_back(b[i].data, b[i].data + b[i].numel * esz);
+            const bool same = b[i].data == a[i].data && b[i].aux == a[i].aux;
+            add_spans(a[i].data, a[i].aux, a[i].numel, a[i].dtype, spans);
+            if (!same) add_spans(b[i].data, b[i].aux, b[i].numel, b[i].dtype, spans);
         }
     }
-    std::sort(spans.begin(), spans.end());
-    uint64_t reach = 0;
-    for (const auto& sp : spans) {
-        if (std::get<0>(sp) < reach) return MEZO_EOVERLAP;
-        reach = std::max(reach, std::get<1>(sp));
-    }
-    return MEZO_OK;
+    return disjoint(spans) ? MEZO_OK : MEZO_EOVERLAP;
 }
 
 }  // namespace
@@ -288,24 +314,26 @@ extern "C" {
 int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* out)
 {
     if (!t || !out || n == 0) return MEZO_EINVAL;
-    std::vector<std::pair<uintptr_t, uintptr_t>> spans;
+    std::vector<Span> spans;
     std::vector<uint32_t> ids;
-    spans.reserve(n);
+    spans.reserve(2 * size_t(n));
     ids.reserve(n);
     for (uint32_t i = 0; i < n; ++i) {
-        if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16) return MEZO_EDTYPE;
+        if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16 && t[i].dtype != MEZO_NF4) return MEZO_EDTYPE;
         if (!t[i].data || (reinterpret_cast<uintptr_t>(t[i].data) & 15u)) return MEZO_EINVAL;
         if (t[i].numel == 0 || t[i].numel > MEZO_MAX_NUMEL) return MEZO_EINVAL;
-        const uintptr_t b = reinterpret_cast<uintptr_t>(t[i].data);
-        const uint64_t esz = t[i].dtype == MEZO_F32 ? 4 : 2;
-        spans.emplace_back(b, b + t[i].numel * esz);
+        if (t[i].dtype == MEZO_NF4) {
+            if (!t[i].absmax || (reinterpret_cast<uintptr_t>(t[i].absmax) & 15u)) return MEZO_EINVAL;
+        } else if (t[i].absmax) {
+            return MEZO_EINVAL;
+        }
+        add_spans(reinterpret_cast<uint64_t>(t[i].data), reinterpret_cast<uint64_t>(t[i].absmax), t[i].numel,
+                  t[i].dtype, spans);
         ids.push_back(t[i].tensor_id);
     }
     std::sort(ids.begin(), ids.end());
     if (std::adjacent_find(ids.begin(), ids.end()) != ids.end()) return MEZO_EINVAL;
-    std::sort(spans.begin(), spans.end());
-    for (size_t i = 1; i < spans.size(); ++i)
-        if (spans[i].first < spans[i - 1].second) return MEZO_EOVERLAP;
+    if (!disjoint(spans)) return MEZO_EOVERLAP;
 
     mezo_paramset* ps = new (std::nothrow) mezo_paramset;
     if (!ps) return MEZO_EINVAL;
@@ -314,19 +342,22 @@ int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* ou
         const uint32_t dt = t[i].dtype;
         mezo::TensorDesc d;
         d.data = reinterpret_cast<uint64_t>(t[i].data);
+        d.aux = reinterpret_cast<uint64_t>(t[i].absmax);
         d.numel = t[i].numel;
         d.tensor_id = t[i].tensor_id;
         d.dtype = dt;
         d.tile_begin = ps->total_tiles[dt];
-        const uint64_t per = dt == MEZO_F32 ? mezo::kTileF32 : mezo::kTileBF16;
+        const uint64_t per = tile_of(dt);
         ps->total_tiles[dt] += (t[i].numel + per - 1) / per;
         ps->table[dt].push_back(d);
         numel += t[i].numel;
     }
     ps->numel = numel;
-    if (ps->total_tiles[0] > 0x7FFFFFFFull || ps->total_tiles[1] > 0x7FFFFFFFull) {
-        delete ps;  // more tiles than one launch can address
-        return MEZO_EINVAL;
+    for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
+        if (ps->total_tiles[dt] > 0x7FFFFFFFull) {
+            delete ps;  // more tiles than one launch can address
+            return MEZO_EINVAL;
+        }
     }
     *out = ps;
     return MEZO_OK;
@@ -349,7 +380,7 @@ void mezo_paramset_destroy(mezo_paramset_t ps)
             if (s.host) (void)hipHostFree(s.host);
             if (s.dev) (void)hipFree(s.dev);
         }
-        for (int dt = 0; dt < 2; ++dt) {
+        for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
             if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
         }
@@ -449,10 +480,10 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
     std::lock_guard<std::mutex> lock(ps->mu);
     int rc = ensure_device(ps);
     if (rc) return rc;
-    mezo::ChecksumArgs tabs[2];
-    uint32_t dts[2];
+    mezo::ChecksumArgs tabs[mezo_paramset::kTypes];
+    uint32_t dts[mezo_paramset::kTypes];
     int n = 0;
-    for (uint32_t dt = 0; dt < 2; ++dt) {
+    for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
         if (ps->table[dt].empty()) continue;
         tabs[n].tensors = ps->d_table[dt];
         tabs[n].tile_tensor = ps->d_tile_tensor[dt];
@@ -466,6 +497,42 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
                                    ps->device, st));
     MEZO_HIP(hipEventRecord(ps->last, st));
     return MEZO_OK;
+}
+
+namespace {
+int nf4_convert(const void* values, uint32_t dtype, uint64_t n, const void* codes, const float* absmax,
+                bool quantize, void* stream)
+{
+    if (dtype != MEZO_F32 && dtype != MEZO_BF16) return MEZO_EDTYPE;
+    if (!values || !codes || !absmax || n == 0 || n > MEZO_MAX_NUMEL) return MEZO_EINVAL;
+    const uint64_t v = reinterpret_cast<uint64_t>(values);
+    const uint64_t c = reinterpret_cast<uint64_t>(codes);
+    const uint64_t a = reinterpret_cast<uint64_t>(absmax);
+    if ((v | c | a) & 15u) return MEZO_EINVAL;
+    std::vector<Span> spans;
+    add_spans(v, 0, n, dtype, spans);
+    add_spans(c, a, n, MEZO_NF4, spans);
+    if (!disjoint(spans)) return MEZO_EOVERLAP;
+    mezo::NF4ConvArgs args;
+    args.values = v;
+    args.codes = c;
+    args.absmax = a;
+    args.n = n;
+    args.dtype = dtype;
+    MEZO_HIP(mezo::launch_nf4(args, quantize, static_cast<hipStream_t>(stream)));
+    return MEZO_OK;
+}
+}  // namespace
+
+int mezo_nf4_quantize(const void* src, uint32_t src_dtype, uint64_t n, void* codes, float* absmax, void* stream)
+{
+    return nf4_convert(src, src_dtype, n, codes, absmax, true, stream);
+}
+
+int mezo_nf4_dequantize(const void* codes, const float* absmax, uint64_t n, void* dst, uint32_t dst_dtype,
+                        void* stream)
+{
+    return nf4_convert(dst, dst_dtype, n, codes, absmax, false, stream);
 }
 
 int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t* codec)

@@ -21,6 +21,7 @@
 
 #include "engine.hpp"
 #include "launch.hpp"
+#include "nf4.hpp"
 
 namespace mezo {
 
@@ -248,20 +249,246 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
     }
 }
 
+// ---- NF4 storage (the 4-bit forward-only variant) -----------------------------
+// A lane owns 8 consecutive elements (one dword of codes); the 8 lanes
+// tid & ~7 .. tid | 7 own one 64-element block and share its absmax. Codes
+// become values through a 16-entry table and values become codes through the
+// 128-bin table of nf4.hpp, both copied into LDS by every workgroup.
+
+struct NF4Lds {
+    NF4Bin bin[kNF4Bins];
+    float val[kNF4Codes];
+};
+
+__device__ __forceinline__ void nf4_lds_init(NF4Lds& s)
+{
+    if (threadIdx.x < kNF4Bins) s.bin[threadIdx.x] = kNF4Table.bin[threadIdx.x];
+    if (threadIdx.x < kNF4Codes) s.val[threadIdx.x] = kNF4Values[threadIdx.x];
+    __syncthreads();
+}
+
+// Which of a lane's 8 elements e0 .. e0 + 7 exist (bit j for element e0 + j).
+__device__ __forceinline__ uint32_t nf4_valid(uint64_t e0, uint64_t numel)
+{
+    if (e0 >= numel) return 0u;
+    if (e0 + 8 <= numel) return 0xFFu;
+    return (1u << uint32_t(numel - e0)) - 1u;
+}
+
+// A lane's code dword and its block's absmax (zeros past the end).
+__device__ __forceinline__ void nf4_load(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
+                                         uint32_t& packed, float& am)
+{
+    packed = 0u;
+    am = 0.0f;
+    if (e0 >= numel) return;
+    if (e0 + 8 <= numel) {
+        packed = __builtin_nontemporal_load(reinterpret_cast<const MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
+    } else {
+        const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k)
+            if (e0 + 2 * k < numel) packed |= uint32_t(b[k]) << (8 * k);
+    }
+    am = reinterpret_cast<const gfloat_t*>(absmax)[e0 / kNF4Block];
+}
+
+__device__ __forceinline__ void nf4_store(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
+                                          uint32_t packed, float am)
+{
+    if (e0 >= numel) return;
+    if (e0 + 8 <= numel) {
+        __builtin_nontemporal_store(packed, reinterpret_cast<MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
+    } else {
+        MEZO_GLOBAL uint8_t* b = reinterpret_cast<MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k)
+            if (e0 + 2 * k < numel) b[k] = uint8_t(packed >> (8 * k));
+    }
+    if ((threadIdx.x & 7u) == 0u) reinterpret_cast<gfloat_t*>(absmax)[e0 / kNF4Block] = am;
+}
+
+__device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, float am, uint32_t valid,
+                                            float (&w)[8])
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        w[j] = ((valid >> j) & 1u) ? s.val[(packed >> (4 * j)) & 15u] * am : 0.0f;
+}
+
+// Quantize a block held by 8 lanes (w = 0 for elements that do not exist):
+// a = max |w| over the block, r = 1 / a (correctly rounded; 0 for a = 0),
+// code = nearest NF4 value to fl32(w * r), ties to the lower code. Returns the
+// packed codes (0 for missing elements) and the new absmax, and replaces w by
+// the dequantized values fl32(v * a) the next step starts from. Every lane of
+// the wave must call it (the block maximum is exchanged across lanes).
+__device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, float (&w)[8], uint32_t& packed,
+                                            float& am)
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
+    m = fmaxf(m, __shfl_xor(m, 1));
+    m = fmaxf(m, __shfl_xor(m, 2));
+    m = fmaxf(m, __shfl_xor(m, 4));
+    const float r = m > 0.0f ? 1.0f / m : 0.0f;
+    uint32_t p = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float x = w[j] * r;
+        int b = static_cast<int>(__builtin_fmaf(x, 64.0f, 64.0f));
+        b = b < 0 ? 0 : (b > kNF4Bins - 1 ? kNF4Bins - 1 : b);
+        const NF4Bin e = s.bin[b];
+        const bool up = x > e.mid;
+        const bool ok = (valid >> j) & 1u;
+        w[j] = ok ? (up ? e.v_hi : e.v_lo) * m : 0.0f;
+        p |= (ok ? e.lo + (up ? 1u : 0u) : 0u) << (4 * j);
+    }
+    packed = p;
+    am = m;
+}
+
+template <bool kInline, bool kPortable>
+__device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& d, uint64_t e0, uint32_t packed,
+                                         float am, const NF4Lds& s)
+{
+    const uint32_t valid = nf4_valid(e0, d.numel);
+    float w[8];
+    nf4_dequant(s, packed, am, valid, w);
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+    const BlockPre pre0 = block_pre(uint32_t(e0 >> 2));
+    const BlockPre pre1 = block_pre(uint32_t((e0 >> 2) + 1));
+    for (uint32_t r = 0; r < a.n_rec; ++r) {
+        const SeedRec& rec = rec_at<kInline>(a, r);
+        const SeedUniform u = seed_uniform(rec, d.tensor_id);
+        const float c = rec.coef;
+        uint32_t w0, w1, w2, w3;
+        philox_words(u, pre0, w0, w1, w2, w3);
+        accumulate4<kPortable>(c, w0, w1, w2, w3, acc[0], acc[1], acc[2], acc[3]);
+        philox_words(u, pre1, w0, w1, w2, w3);
+        accumulate4<kPortable>(c, w0, w1, w2, w3, acc[4], acc[5], acc[6], acc[7]);
+        if (rec.last) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                w[j] = ((valid >> j) & 1u) ? w[j] + acc[j] : 0.0f;
+                acc[j] = 0.0f;
+            }
+            nf4_requant(s, valid, w, packed, am);
+        }
+    }
+    nf4_store(d.data, d.aux, e0, d.numel, packed, am);
+}
+
 template <bool kInline, uint32_t kDtype, bool kPortable>
 __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
     const uint32_t ti = a.tile_tensor[tile];
     const TensorDesc d = a.tensors[ti];
-    // out of place: read tensor ti of the source set (same layout), write d
-    const uint64_t src = a.src_tensors ? a.src_tensors[ti].data : d.data;
-    TileRaw<Layout<kDtype>::kGroups> raw;
-    load_tile<kDtype>(d, src, tile - d.tile_begin, raw);
-    if constexpr (kDtype == kF32)
-        tile_f32<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
-    else
-        tile_bf16<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
+    if constexpr (kDtype == kNF4) {
+        __shared__ NF4Lds lds;
+        // out of place: read tensor ti of the source set (same layout), write d
+        const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
+        const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
+        const uint64_t e0 = (tile - d.tile_begin) * kTileNF4 + threadIdx.x * 8u;
+        uint32_t packed;
+        float am;
+        nf4_load(codes, absmax, e0, d.numel, packed, am);
+        nf4_lds_init(lds);
+        tile_nf4<kInline, kPortable>(a, d, e0, packed, am, lds);
+    } else {
+        // out of place: read tensor ti of the source set (same layout), write d
+        const uint64_t src = a.src_tensors ? a.src_tensors[ti].data : d.data;
+        TileRaw<Layout<kDtype>::kGroups> raw;
+        load_tile<kDtype>(d, src, tile - d.tile_begin, raw);
+        if constexpr (kDtype == kF32)
+            tile_f32<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
+        else
+            tile_bf16<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
+    }
+}
+
+// Standalone NF4 conversions (one tile of 2048 elements per workgroup).
+__global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
+{
+    __shared__ NF4Lds lds;
+    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
+    const uint32_t valid = nf4_valid(e0, a.n);
+    float w[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = 0.0f;
+    if (a.dtype == kF32) {
+        const gfloat_t* in = reinterpret_cast<const gfloat_t*>(a.values);
+        if (valid == 0xFFu) {
+            const uint4 v0 = load_stream(a.values + e0 * 4);
+            const uint4 v1 = load_stream(a.values + e0 * 4 + 16);
+            const uint32_t u[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) w[j] = __uint_as_float(u[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if ((valid >> j) & 1u) w[j] = in[e0 + j];
+        }
+    } else {
+        const gu16_t* in = reinterpret_cast<const gu16_t*>(a.values);
+        if (valid == 0xFFu) {
+            const uint4 v = load_stream(a.values + e0 * 2);
+            const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                w[2 * j] = bf16_lo(u[j]);
+                w[2 * j + 1] = bf16_hi(u[j]);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if ((valid >> j) & 1u) w[j] = __uint_as_float(uint32_t(in[e0 + j]) << 16);
+        }
+    }
+    nf4_lds_init(lds);
+    uint32_t packed;
+    float am;
+    nf4_requant(lds, valid, w, packed, am);
+    nf4_store(a.codes, a.absmax, e0, a.n, packed, am);
+}
+
+__global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
+{
+    __shared__ NF4Lds lds;
+    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
+    const uint32_t valid = nf4_valid(e0, a.n);
+    uint32_t packed;
+    float am;
+    nf4_load(a.codes, a.absmax, e0, a.n, packed, am);
+    nf4_lds_init(lds);
+    float w[8];
+    nf4_dequant(lds, packed, am, valid, w);
+    if (a.dtype == kF32) {
+        gfloat_t* out = reinterpret_cast<gfloat_t*>(a.values);
+        if (valid == 0xFFu) {
+            store_stream(a.values + e0 * 4, make_uint4(__float_as_uint(w[0]), __float_as_uint(w[1]),
+                                                       __float_as_uint(w[2]), __float_as_uint(w[3])));
+            store_stream(a.values + e0 * 4 + 16, make_uint4(__float_as_uint(w[4]), __float_as_uint(w[5]),
+                                                            __float_as_uint(w[6]), __float_as_uint(w[7])));
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if ((valid >> j) & 1u) out[e0 + j] = w[j];
+        }
+    } else {
+        gu16_t* out = reinterpret_cast<gu16_t*>(a.values);
+        if (valid == 0xFFu) {
+            store_stream(a.values + e0 * 2, make_uint4(pack_bf16(w[0], w[1]), pack_bf16(w[2], w[3]),
+                                                       pack_bf16(w[4], w[5]), pack_bf16(w[6], w[7])));
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if ((valid >> j) & 1u) out[e0 + j] = to_bf16(w[j]);
+        }
+    }
 }
 
 // Inspection: RNG words and Gaussians of a range of elements, one Philox
@@ -301,6 +528,23 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t x)
     x *= kFmixB;
     x ^= x >> 33;
     return x;
+}
+
+// Reduce every lane's sum across the workgroup and add it to *out with one
+// 64-bit atomic (all lanes of the workgroup must call it).
+__device__ __forceinline__ void add_workgroup_sum(uint64_t sum, unsigned long long* out)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+    __shared__ uint64_t part[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t s = 0;
+#pragma unroll
+        for (int i = 0; i < kThreads / 64; ++i) s += part[i];
+        atomicAdd(out, static_cast<unsigned long long>(s));
+    }
 }
 
 template <uint32_t kDtype>
@@ -346,17 +590,48 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
             if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((c0 + 1) * kChunkPos) ^ tmix);
         }
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
-    __shared__ uint64_t part[kThreads / 64];
-    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint64_t s = 0;
-#pragma unroll
-        for (int i = 0; i < kThreads / 64; ++i) s += part[i];
-        atomicAdd(a.out, static_cast<unsigned long long>(s));
+    add_workgroup_sum(sum, a.out);
+}
+
+// NF4 tensors: the code bytes zero-padded to whole chunks, then the absmax
+// values, chunk numbers continuing. Per tile of 2048 elements, lanes 0..127
+// take its 128 code chunks and lanes 128..143 its 16 absmax chunks.
+__global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
+{
+    uint64_t sum = 0;
+    for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
+        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+        const uint64_t local = tile - d.tile_begin;
+        const uint64_t cbytes = (d.numel + 1) / 2;
+        const uint64_t cchunks = (cbytes + 7) / 8;
+        const uint64_t abytes = 4 * ((d.numel + kNF4Block - 1) / kNF4Block);
+        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+        const uint32_t lane = threadIdx.x;
+        if (lane < kTileNF4 / 16) {
+            const uint64_t j = local * (kTileNF4 / 16) + lane;  // bytes [8j, 8j + 8) of the codes
+            if (j < cchunks) {
+                uint64_t v = 0;
+                if (8 * j + 8 <= cbytes) {
+                    v = *reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.data + 8 * j);
+                } else {
+                    const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(d.data);
+                    for (uint64_t k = 8 * j; k < cbytes; ++k) v |= uint64_t(b[k]) << (8 * (k - 8 * j));
+                }
+                sum += fmix64(v ^ (j * kChunkPos) ^ tmix);
+            }
+        } else if (lane < kTileNF4 / 16 + kTileNF4 / kNF4Block / 2) {
+            const uint64_t k = local * (kTileNF4 / kNF4Block / 2) + (lane - kTileNF4 / 16);  // absmax chunk
+            if (8 * k < abytes) {
+                uint64_t v;
+                if (8 * k + 8 <= abytes)
+                    v = *reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.aux + 8 * k);
+                else
+                    v = *reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.aux + 8 * k);
+                sum += fmix64(v ^ ((cchunks + k) * kChunkPos) ^ tmix);
+            }
+        }
     }
+    add_workgroup_sum(sum, a.out);
 }
 
 __global__ void zero_u64_kernel(unsigned long long* out)
@@ -378,15 +653,17 @@ void launch_dtype(const EngineArgs& args, uint32_t dtype, dim3 g, dim3 b, hipStr
 {
     if (dtype == kF32)
         launch_one<kInline, kF32, kPortable>(args, g, b, stream);
-    else
+    else if (dtype == kBF16)
         launch_one<kInline, kBF16, kPortable>(args, g, b, stream);
+    else
+        launch_one<kInline, kNF4, kPortable>(args, g, b, stream);
 }
 }  // namespace
 
 hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, bool portable, hipStream_t stream)
 {
     if (args.total_tiles == 0) return hipSuccess;
-    if (args.total_tiles > uint64_t(0x7FFFFFFF) || dtype > kBF16) return hipErrorInvalidValue;
+    if (args.total_tiles > uint64_t(0x7FFFFFFF) || dtype >= kStorageTypes) return hipErrorInvalidValue;
     const bool inl = args.n_rec <= kInlineRecs;
     const dim3 g{uint32_t(args.total_tiles)};
     const dim3 b{uint32_t(kThreads)};
@@ -457,12 +734,28 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
         const dim3 b{uint32_t(kThreads)};
         if (dtypes[i] == kF32)
             hipLaunchKernelGGL(checksum_kernel<kF32>, g, b, 0, stream, tables[i]);
-        else
+        else if (dtypes[i] == kBF16)
             hipLaunchKernelGGL(checksum_kernel<kBF16>, g, b, 0, stream, tables[i]);
+        else
+            hipLaunchKernelGGL(checksum_nf4_kernel, g, b, 0, stream, tables[i]);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_nf4(const NF4ConvArgs& args, bool quantize, hipStream_t stream)
+{
+    const uint64_t tiles = (args.n + kTileNF4 - 1) / kTileNF4;
+    if (tiles == 0) return hipSuccess;
+    if (tiles > uint64_t(0x7FFFFFFF)) return hipErrorInvalidValue;
+    const dim3 g{uint32_t(tiles)};
+    const dim3 b{uint32_t(kThreads)};
+    if (quantize)
+        hipLaunchKernelGGL(nf4_quantize_kernel, g, b, 0, stream, args);
+    else
+        hipLaunchKernelGGL(nf4_dequantize_kernel, g, b, 0, stream, args);
+    return hipGetLastError();
 }
 
 }  // namespace mezo

@@ -40,11 +40,24 @@ struct GenArgs {
     uint32_t portable;  // 1: the portable Gaussian
 };
 
+// Standalone NF4 conversion of n elements between a fp32/bf16 array and NF4
+// codes + absmax (device addresses).
+struct NF4ConvArgs {
+    uint64_t values;  // fp32 or bf16 elements
+    uint64_t codes;
+    uint64_t absmax;
+    uint64_t n;
+    uint32_t dtype;   // kF32 or kBF16 (of values)
+};
+
 // Launch the engine over the tensors of one storage type (dtype): one
 // workgroup per tile (at most 2^31 - 1 tiles); portable selects the Gaussian
 // made of binary32 operations only.
 hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, bool portable, hipStream_t stream);
 hipError_t launch_generate(const GenArgs& args, hipStream_t stream);
+
+// values -> NF4 (quantize) or NF4 -> values.
+hipError_t launch_nf4(const NF4ConvArgs& args, bool quantize, hipStream_t stream);
 
 // Zero *out, then add the checksum of every table given (one launch each).
 hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n_tables,

@@ -23,15 +23,18 @@ struct alignas(16) SeedRec {
 
 // One registered tensor as the kernels see it.
 struct alignas(16) TensorDesc {
-    uint64_t data;        // device address, 16-byte aligned
+    uint64_t data;        // device address, 16-byte aligned (NF4: the codes)
     uint64_t numel;
     uint64_t tile_begin;  // first global tile of this tensor
     uint32_t tensor_id;
-    uint32_t dtype;       // 0 = fp32, 1 = bf16
+    uint32_t dtype;       // 0 = fp32, 1 = bf16, 2 = NF4
+    uint64_t aux;         // NF4: device address of the per-block absmax values
 };
 
 constexpr uint32_t kF32 = 0u;
 constexpr uint32_t kBF16 = 1u;
+constexpr uint32_t kNF4 = 2u;
+constexpr uint32_t kStorageTypes = 3u;
 
 // Work decomposition: a workgroup of kThreads lanes handles one tile per
 // iteration; each lane owns a few 16-byte groups of the tile, strided by
@@ -44,6 +47,9 @@ constexpr int kGroupsF32 = 2;
 constexpr int kGroupsBF16 = 1;
 constexpr uint64_t kTileF32 = uint64_t(kThreads) * kGroupsF32 * 4;
 constexpr uint64_t kTileBF16 = uint64_t(kThreads) * kGroupsBF16 * 8;
+// NF4: each lane owns 8 consecutive elements (4 code bytes, two Philox
+// blocks); 8 lanes make one 64-element block.
+constexpr uint64_t kTileNF4 = uint64_t(kThreads) * 8;
 
 // Records that travel inside the kernel arguments (above this they are staged
 // in device memory).

@@ -26,7 +26,9 @@ import numpy as np
 LIB_PATH = Path(__file__).resolve().parent / "libmezo.so"
 
 OK, EINVAL, EDTYPE, EOVERLAP, EORDER, ERANGE, EHIP = 0, -1, -2, -3, -4, -5, -6
-F32, BF16 = 0, 1
+F32, BF16, NF4 = 0, 1, 2
+#: NF4 elements per absmax value.
+NF4_BLOCK = 64
 GAUSS_FAST, GAUSS_PORTABLE = 0, 1
 LINEAR, SIGNED_LOG = 0, 1
 #: Signed-log slope of a base-2 log: code 127 decodes just inside fp32.
@@ -44,7 +46,8 @@ class Seed(ctypes.Structure):
 
 class Tensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("numel", ctypes.c_uint64),
-                ("tensor_id", ctypes.c_uint32), ("dtype", ctypes.c_uint32)]
+                ("tensor_id", ctypes.c_uint32), ("dtype", ctypes.c_uint32),
+                ("absmax", ctypes.c_void_p)]
 
 
 class Codec(ctypes.Structure):
@@ -61,8 +64,8 @@ EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel
            "mezo_paramset_set_gaussian",
            "mezo_perturb", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
            "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
-           "mezo_dequantize", "mezo_debug_generate", "mezo_strerror", "mezo_last_error",
-           "mezo_version")
+           "mezo_dequantize", "mezo_nf4_quantize", "mezo_nf4_dequantize", "mezo_debug_generate",
+           "mezo_strerror", "mezo_last_error", "mezo_version")
 
 
 def _load() -> ctypes.CDLL:
@@ -100,6 +103,10 @@ def _load() -> ctypes.CDLL:
     L.quantize_projgrad.restype = i32
     L.mezo_dequantize.argtypes = [vp, vp, u32, ctypes.POINTER(Codec)]
     L.mezo_dequantize.restype = i32
+    L.mezo_nf4_quantize.argtypes = [vp, u32, u64, vp, vp, vp]
+    L.mezo_nf4_quantize.restype = i32
+    L.mezo_nf4_dequantize.argtypes = [vp, vp, u64, vp, u32, vp]
+    L.mezo_nf4_dequantize.restype = i32
     L.mezo_debug_generate.argtypes = [Seed, u32, u64, u64, u32, vp, vp, vp]
     L.mezo_debug_generate.restype = i32
     L.mezo_strerror.argtypes = [i32]
@@ -170,8 +177,75 @@ def _dtype_code(t) -> int:
     raise TypeError(f"unsupported parameter dtype {t.dtype}")
 
 
+class NF4Tensor:
+    """A tensor of ``numel`` elements in 4-bit NormalFloat storage (the 4-bit
+    forward-only variant): ``codes`` (uint8, ceil(numel / 2) bytes, element
+    2i in the low nibble of byte i) and ``absmax`` (float32, one per block of
+    64 elements), both contiguous device tensors owned by torch."""
+
+    def __init__(self, codes, absmax, numel: int):
+        import torch
+        if codes.dtype != torch.uint8 or absmax.dtype != torch.float32:
+            raise TypeError("codes must be uint8 and absmax float32")
+        if not (codes.is_cuda and absmax.is_cuda and codes.is_contiguous() and absmax.is_contiguous()):
+            raise ValueError("codes and absmax must be contiguous CUDA tensors")
+        if codes.numel() < (numel + 1) // 2 or absmax.numel() < (numel + NF4_BLOCK - 1) // NF4_BLOCK:
+            raise ValueError("codes / absmax too small for numel")
+        self.codes, self.absmax, self._numel = codes, absmax, int(numel)
+
+    @classmethod
+    def empty(cls, numel: int, device="cuda") -> "NF4Tensor":
+        import torch
+        return cls(torch.empty((numel + 1) // 2, dtype=torch.uint8, device=device),
+                   torch.empty((numel + NF4_BLOCK - 1) // NF4_BLOCK, dtype=torch.float32, device=device),
+                   numel)
+
+    def numel(self) -> int:
+        return self._numel
+
+    @property
+    def device(self):
+        return self.codes.device
+
+    @property
+    def is_cuda(self) -> bool:
+        return True
+
+
+def nf4_quantize(values, out: NF4Tensor | None = None, stream=None) -> NF4Tensor:
+    """values (contiguous fp32/bf16 device tensor) -> NF4 storage."""
+    n = values.numel()
+    out = NF4Tensor.empty(n, values.device) if out is None else out
+    if out.numel() != n or not values.is_contiguous():
+        raise ValueError("size mismatch or non-contiguous values")
+    _check(lib.mezo_nf4_quantize(values.data_ptr(), _dtype_code(values), n, out.codes.data_ptr(),
+                                 out.absmax.data_ptr(), _stream_ptr(stream)), "mezo_nf4_quantize")
+    return out
+
+
+def nf4_dequantize(t: NF4Tensor, dtype=None, out=None, stream=None):
+    """NF4 storage -> a fp32 (default) or bf16 device tensor of numel elements."""
+    import torch
+    if out is None:
+        out = torch.empty(t.numel(), dtype=dtype or torch.float32, device=t.device)
+    if out.numel() != t.numel() or not out.is_contiguous():
+        raise ValueError("size mismatch or non-contiguous out")
+    _check(lib.mezo_nf4_dequantize(t.codes.data_ptr(), t.absmax.data_ptr(), t.numel(), out.data_ptr(),
+                                   _dtype_code(out), _stream_ptr(stream)), "mezo_nf4_dequantize")
+    return out
+
+
+def _tensor_struct(t, tid: int) -> Tensor:
+    if isinstance(t, NF4Tensor):
+        return Tensor(t.codes.data_ptr(), t.numel(), tid, NF4, t.absmax.data_ptr())
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("parameters must be contiguous CUDA tensors")
+    return Tensor(t.data_ptr(), t.numel(), tid, _dtype_code(t), None)
+
+
 class ParamSet:
-    """A registered set of parameter tensors (device memory owned by torch).
+    """A registered set of parameter tensors (device memory owned by torch):
+    fp32 / bf16 torch tensors or NF4Tensor objects.
 
     ``tensor_ids`` default to the position in ``tensors``; they select each
     tensor's noise stream and must be the same on every machine.
@@ -185,9 +259,7 @@ class ParamSet:
             raise ValueError("one tensor_id per tensor")
         arr = (Tensor * max(1, len(self.tensors)))()
         for i, (t, tid) in enumerate(zip(self.tensors, ids)):
-            if not t.is_cuda or not t.is_contiguous():
-                raise ValueError("parameters must be contiguous CUDA tensors")
-            arr[i] = Tensor(t.data_ptr(), t.numel(), tid, _dtype_code(t))
+            arr[i] = _tensor_struct(t, tid)
         h = ctypes.c_void_p()
         _check(lib.mezo_paramset_create(arr, len(self.tensors), ctypes.byref(h)),
                "mezo_paramset_create")

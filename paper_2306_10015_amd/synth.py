@@ -18,7 +18,8 @@ import numpy as np
 #: Memory layout of one seed (machine u64, step u32, sample u32), 16 bytes.
 SEED_DTYPE = np.dtype([("machine", "<u8"), ("step", "<u4"), ("sample", "<u4")])
 
-F32, BF16 = "f32", "bf16"
+F32, BF16, NF4 = "f32", "bf16", "nf4"
+NF4_BLOCK = 64
 
 
 def _opt_shapes(d: int, ffn: int, layers: int, vocab: int = 50272):
@@ -71,6 +72,11 @@ WORKLOADS = {
                         machines=64, samples_per_machine=1),
     "replay1.3b": Workload("replay1.3b", _opt_shapes(2048, 8192, 24), BF16, K=32,
                            machines=4, samples_per_machine=8, T=200),
+    # the 4-bit forward-only variant (Section 3) on the paper's model size
+    "opt6.7b-nf4": Workload("opt6.7b-nf4", _opt_shapes(4096, 16384, 32), NF4, K=64,
+                            machines=64, samples_per_machine=1),
+    "opt1.3b-nf4": Workload("opt1.3b-nf4", _opt_shapes(2048, 8192, 24), NF4, K=16,
+                            grad_kind="normal40", machines=4, samples_per_machine=4),
 }
 
 
@@ -126,6 +132,21 @@ def theta0_tensor(shape, dtype: str, tensor_id: int, seed: int = 0) -> np.ndarra
     rng = np.random.Generator(np.random.PCG64([seed, tensor_id]))
     x = rng.standard_normal(size=int(np.prod(shape)), dtype=np.float32) * np.float32(0.02)
     return x if dtype == F32 else fp32_to_bf16_bits(x)
+
+
+def nf4_theta0_tensor(numel: int, tensor_id: int, seed: int = 0):
+    """Starting 4-bit storage of one tensor: packed code bytes uniform over all
+    16 codes (NF4's values are quantiles of the normal law, so the codes of
+    normal weights are close to uniform) with the unused high nibble of an
+    odd-length tensor zero, and absmax = 0.02 * U(2, 3) per 64-element block
+    (where the largest |N(0, 0.02)| of 64 draws usually falls)."""
+    rng = np.random.Generator(np.random.PCG64([seed, tensor_id, 4]))
+    packed = rng.integers(0, 256, size=(numel + 1) // 2, dtype=np.int64).astype(np.uint8)
+    if numel % 2:
+        packed[-1] &= 0x0F
+    absmax = (np.float32(0.02) * rng.uniform(2.0, 3.0, size=(numel + NF4_BLOCK - 1) // NF4_BLOCK)
+              .astype(np.float32)).astype(np.float32)
+    return packed, absmax
 
 
 def theta0(w: Workload, seed: int = 0) -> list:

@@ -87,8 +87,9 @@ def test_codec_errors():
 
 def create(entries):
     arr = (mezo.Tensor * max(1, len(entries)))()
-    for i, (ptr, n, tid, dt) in enumerate(entries):
-        arr[i] = mezo.Tensor(ptr, n, tid, dt)
+    for i, e in enumerate(entries):
+        ptr, n, tid, dt = e[:4]
+        arr[i] = mezo.Tensor(ptr, n, tid, dt, e[4] if len(e) > 4 else None)
     h = ctypes.c_void_p()
     rc = mezo.lib.mezo_paramset_create(arr, len(entries), ctypes.byref(h))
     return rc, h
@@ -104,6 +105,12 @@ def create(entries):
     ([(0x1000, 16, 3, mezo.F32), (0x2000, 16, 3, mezo.F32)], mezo.EINVAL),   # duplicate id
     ([(0x1000, 16, 0, mezo.F32), (0x1030, 16, 1, mezo.F32)], mezo.EOVERLAP),
     ([(0x1000, 16, 0, mezo.BF16), (0x1010, 16, 1, mezo.F32)], mezo.EOVERLAP),
+    ([(0x1000, 16, 0, mezo.NF4)], mezo.EINVAL),                    # NF4 without absmax
+    ([(0x1000, 16, 0, mezo.NF4, 0x2008)], mezo.EINVAL),            # absmax not 16-byte aligned
+    ([(0x1000, 16, 0, mezo.F32, 0x2000)], mezo.EINVAL),            # absmax on a float tensor
+    ([(0x1000, 16, 0, mezo.NF4, 0x1000)], mezo.EOVERLAP),          # codes and absmax overlap
+    ([(0x1000, 260, 0, mezo.NF4, 0x2000), (0x2010, 4, 1, mezo.F32)], mezo.EOVERLAP),  # 5 absmax = 20 B
+    ([(0x1000, 33, 0, mezo.NF4, 0x2000), (0x1010, 4, 1, mezo.F32)], mezo.EOVERLAP),   # 17 code bytes
 ])
 def test_paramset_create_rejects(entries, code):
     rc, h = create(entries)
@@ -117,6 +124,34 @@ def test_paramset_create_accepts_adjacent_and_reports_numel():
     assert mezo.lib.mezo_paramset_numel(h) == 40
     mezo.lib.mezo_paramset_destroy(h)
     mezo.lib.mezo_paramset_destroy(None)
+
+
+def test_nf4_tensors_accepted_when_adjacent():
+    # 32 elements: 16 code bytes and one absmax; the next tensor may start right after
+    rc, h = create([(0x1000, 32, 0, mezo.NF4, 0x3000), (0x1010, 4, 1, mezo.F32), (0x3010, 8, 2, mezo.BF16)])
+    assert rc == mezo.OK
+    assert mezo.lib.mezo_paramset_numel(h) == 44
+    mezo.lib.mezo_paramset_destroy(h)
+
+
+def test_nf4_conversion_argument_checks():
+    lib = mezo.lib
+    q, d = lib.mezo_nf4_quantize, lib.mezo_nf4_dequantize
+    assert q(0x1000, 9, 64, 0x2000, 0x3000, None) == mezo.EDTYPE
+    assert q(None, mezo.F32, 64, 0x2000, 0x3000, None) == mezo.EINVAL
+    assert q(0x1000, mezo.F32, 0, 0x2000, 0x3000, None) == mezo.EINVAL
+    assert q(0x1000, mezo.F32, (1 << 34) + 1, 0x2000, 0x3000, None) == mezo.EINVAL
+    assert q(0x1008, mezo.F32, 64, 0x2000, 0x3000, None) == mezo.EINVAL
+    assert q(0x1000, mezo.F32, 64, 0x1080, 0x3000, None) == mezo.EOVERLAP    # 256 B of values
+    assert q(0x1000, mezo.BF16, 64, 0x1080, 0x1090, None) == mezo.EOVERLAP   # 32 code bytes
+    assert d(0x2000, 0x3000, 64, 0x1000, 9, None) == mezo.EDTYPE
+    assert d(0x2000, None, 64, 0x1000, mezo.F32, None) == mezo.EINVAL
+    assert d(0x2000, 0x2010, 64, 0x1000, mezo.F32, None) == mezo.EOVERLAP
+
+
+def test_tensor_struct_layout():
+    assert ctypes.sizeof(mezo.Tensor) == 32
+    assert mezo.Tensor.absmax.offset == 24
 
 
 @pytest.fixture

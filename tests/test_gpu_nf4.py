@@ -1,0 +1,313 @@
+"""GPU parity of the 4-bit (NF4) variant (Section 3: dequantize, add the
+noise, quantize again; QLoRA's NF4 format), through the C ABI, against the
+oracle (oracle/nf4.py).
+
+Bars. Conversions (quantize / dequantize kernels) are bit-exact: the same
+binary32 operations decide every code. The engine in portable mode is
+bit-exact too (its z and update are binary32 operations only). In fast mode
+the values entering the quantizer carry the fp32 update's tolerance, so: each
+block's absmax within 1e-6 * the tensor's largest absmax of the oracle's, and
+a code may differ from the oracle's only by one, where the oracle's x lies
+within 1e-5 of the midpoint between the two codes (at most 1 in 1000 codes).
+Every step is compared with the oracle applied to the GPU's own input state.
+"""
+import numpy as np
+import pytest
+
+from paper_2306_10015_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+SIZES = [1, 7, 64, 65, 2048, 4097, 70001]
+
+
+@pytest.fixture(scope="module")
+def mz():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    from paper_2306_10015_amd import mezo
+    return mezo
+
+
+@pytest.fixture(scope="module")
+def nf4(orc):
+    from oracle import nf4 as m
+    return m
+
+
+def upload(mz, packed, absmax, n):
+    import torch
+    return mz.NF4Tensor(torch.from_numpy(packed.copy()).cuda(), torch.from_numpy(absmax.copy()).cuda(), n)
+
+
+def download(t):
+    return t.codes.cpu().numpy().copy(), t.absmax.cpu().numpy().copy()
+
+
+def values_of(n, seed, zero_block=False):
+    w = synth.theta0_tensor((n,), synth.F32, seed)
+    if zero_block and n > 64:
+        w[64:128] = 0.0
+    return w
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_quantize_kernel_bit_exact(mz, nf4, n, dtype):
+    import torch
+    from gpu_util import to_device
+    w = values_of(n, n, zero_block=True)
+    if dtype == "bf16":
+        bits = synth.fp32_to_bf16_bits(w)
+        src = to_device(bits)
+        w = synth.bf16_bits_to_fp32(bits)
+    else:
+        src = to_device(w)
+    t = mz.nf4_quantize(src)
+    torch.cuda.synchronize()
+    packed, absmax = download(t)
+    c_ref, a_ref = nf4.quantize(w)
+    assert np.array_equal(absmax.view(np.uint32), a_ref.view(np.uint32))
+    assert np.array_equal(packed, nf4.pack(c_ref))      # incl. a zero pad nibble for odd n
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dequantize_kernel_bit_exact(mz, nf4, n, dtype):
+    import torch
+    from gpu_util import to_host
+    packed, absmax = synth.nf4_theta0_tensor(n, 3)
+    t = upload(mz, packed, absmax, n)
+    out = mz.nf4_dequantize(t, torch.float32 if dtype == "f32" else torch.bfloat16)
+    torch.cuda.synchronize()
+    ref = nf4.dequantize(nf4.unpack(packed, n), absmax)
+    got = to_host(out)
+    if dtype == "f32":
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+    else:
+        assert np.array_equal(got, synth.fp32_to_bf16_bits(ref))
+
+
+def test_code_values(mz, nf4):
+    import torch
+    from gpu_util import to_host
+    codes = np.tile(np.arange(16, dtype=np.uint8), 4)
+    t = upload(mz, nf4.pack(codes), np.ones(1, np.float32), 64)
+    got = to_host(mz.nf4_dequantize(t))
+    torch.cuda.synchronize()
+    assert np.array_equal(got[:16].view(np.uint32), nf4.table().view(np.uint32))
+
+
+# ---- the engine on NF4 storage -------------------------------------------------
+
+def nf4_set(mz, sizes, seed=0, ids=None):
+    ids = list(range(len(sizes))) if ids is None else ids
+    host = [synth.nf4_theta0_tensor(n, tid, seed) for n, tid in zip(sizes, ids)]
+    dev = [upload(mz, p, a, n) for (p, a), n in zip(host, sizes)]
+    return dev, ids
+
+
+def compare_step(nf4, got, start, n, tid, apply, exact, what, blocks=None):
+    """got/start: (packed, absmax) of the blocks checked (all blocks by
+    default); apply(w, idx) applies the step to fp32 values in place (an
+    oracle call)."""
+    b = np.arange((n + 63) // 64) if blocks is None else np.asarray(blocks)
+    lens = nf4.block_lengths(n, b)
+    c0 = start[0] if blocks is not None else nf4.unpack(start[0], n)
+    cg = got[0] if blocks is not None else nf4.unpack(got[0], n)
+    w = nf4.dequantize(c0, start[1], n, b)
+    apply(w, nf4.block_elements(n, b))
+    c_ref, a_ref = nf4.quantize(w, n, b)
+    if exact:
+        assert np.array_equal(got[1].view(np.uint32), a_ref.view(np.uint32)), f"{what}: absmax"
+        assert np.array_equal(cg, c_ref), f"{what}: codes"
+        if blocks is None:
+            assert np.array_equal(got[0], nf4.pack(c_ref)), f"{what}: packed bytes"
+        return {"exact": True}
+    scale = float(np.max(a_ref)) if a_ref.size else 0.0
+    aerr = float(np.max(np.abs(got[1].astype(np.float64) - a_ref))) if a_ref.size else 0.0
+    assert aerr <= 1e-6 * scale + 1e-30, f"{what}: absmax off by {aerr:.3e}"
+    mism = np.nonzero(cg != c_ref)[0]
+    if mism.size:
+        assert np.all(np.abs(cg[mism].astype(int) - c_ref[mism].astype(int)) == 1), f"{what}: code off by >1"
+        r = np.repeat(np.where(a_ref > 0, np.float32(1) / np.where(a_ref > 0, a_ref, 1), 0).astype(np.float32),
+                      lens)
+        x = (w * r)[mism].astype(np.float64)
+        mid = nf4.midpoints().astype(np.float64)[np.minimum(cg[mism], c_ref[mism]).astype(int)]
+        assert np.all(np.abs(x - mid) <= 1e-5), f"{what}: code differs away from a midpoint"
+        assert mism.size <= max(1, cg.size // 1000), f"{what}: {mism.size} codes differ"
+    return {"codes_differing": int(mism.size), "absmax_err": aerr}
+
+
+SET_SIZES = [1, 65, 4097, 70001, 64 * 300]
+
+
+@pytest.mark.parametrize("portable", [True, False])
+def test_perturb_triple_and_updates(mz, orc, nf4, portable):
+    import torch
+    dev, ids = nf4_set(mz, SET_SIZES, seed=1, ids=[5, 0, 17, 3, 1 << 20])
+    ps = mz.ParamSet(dev, ids, gaussian=mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST)
+    eps = 1e-3
+    s = (7, 2, 1)
+    steps = [("perturb +eps", lambda: ps.perturb(s, eps),
+              lambda tid: (lambda w, ix: orc.perturb(w, tid, s, eps, idx=ix, portable=portable))),
+             ("perturb -2eps", lambda: ps.perturb(s, -2 * eps),
+              lambda tid: (lambda w, ix: orc.perturb(w, tid, s, -2 * eps, idx=ix, portable=portable))),
+             ("perturb +eps", lambda: ps.perturb(s, eps),
+              lambda tid: (lambda w, ix: orc.perturb(w, tid, s, eps, idx=ix, portable=portable)))]
+    for K in (4, 40):
+        seeds = synth.seeds(K, 1, step=3)
+        q = synth.grads_int8(K, seed=K)
+        steps.append((f"update K={K}", lambda seeds=seeds, q=q: ps.update_multi(seeds, q, 2e-3),
+                      lambda tid, seeds=seeds, q=q: (lambda w, ix: orc.update(w, tid, seeds, q, 2e-3, idx=ix,
+                                                                               portable=portable))))
+    for what, gpu_op, oracle_op in steps:
+        before = [download(t) for t in dev]
+        gpu_op()
+        torch.cuda.synchronize()
+        for t, n, tid, b in zip(dev, SET_SIZES, ids, before):
+            compare_step(nf4, download(t), b, n, tid, oracle_op(tid), portable, f"{what} tensor {tid}")
+    ps.close()
+
+
+@pytest.mark.parametrize("portable", [True, False])
+def test_replay_requantizes_every_step(mz, orc, nf4, portable):
+    import torch
+    sizes = [4097, 64 * 100 + 3]
+    dev, ids = nf4_set(mz, sizes, seed=2)
+    ps = mz.ParamSet(dev, ids, gaussian=mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST)
+    log = [(synth.seeds(2, 2, step=t), synth.grads_int8(4, seed=80 + t), 3e-3) for t in range(3)]
+    before = [download(t) for t in dev]
+    ps.replay(log)
+    torch.cuda.synchronize()
+    for t, n, tid, (p0, a0) in zip(dev, sizes, ids, before):
+        c_ref, a_ref = nf4.replay(nf4.unpack(p0, n), a0, tid, log, portable=portable)
+        p, a = download(t)
+        if portable:
+            assert np.array_equal(p, nf4.pack(c_ref)) and np.array_equal(a.view(np.uint32), a_ref.view(np.uint32))
+        else:
+            c = nf4.unpack(p, n)
+            assert np.max(np.abs(a.astype(np.float64) - a_ref)) <= 1e-6 * np.max(a_ref)
+            assert np.mean(c == c_ref) > 0.999
+    ps.close()
+
+
+def test_mixed_storage_set(mz, orc, nf4):
+    """NF4, fp32 and bf16 tensors in one paramset: three launches, each
+    tensor against the oracle of its storage type."""
+    import torch
+    from gpu_util import assert_theta_close, to_device, to_host
+    p, a = synth.nf4_theta0_tensor(5000, 0)
+    t_nf4 = upload(mz, p, a, 5000)
+    f = synth.theta0_tensor((3001,), synth.F32, 1)
+    b = synth.theta0_tensor((2999,), synth.BF16, 2)
+    t_f, t_b = to_device(f), to_device(b)
+    ps = mz.ParamSet([t_nf4, t_f, t_b], [0, 1, 2])
+    seeds = synth.seeds(8, 1)
+    q = synth.grads_int8(8, seed=5)
+    ps.update_multi(seeds, q, 1e-3)
+    torch.cuda.synchronize()
+    compare_step(nf4, download(t_nf4), (p, a), 5000, 0,
+                 lambda w, ix: orc.update(w, 0, seeds, q, 1e-3, idx=ix), False, "mixed nf4")
+    assert_theta_close(to_host(t_f), orc.update(f.copy(), 1, seeds, q, 1e-3), "mixed f32")
+    assert_theta_close(to_host(t_b), orc.update(b.copy(), 2, seeds, q, 1e-3), "mixed bf16", inp=b)
+    ps.close()
+
+
+def test_update_from_nf4_backup(mz, orc, nf4):
+    """Algorithm 1's restore fused into the apply loop on 4-bit storage
+    (portable mode: bit-exact); the backup is left as it was; with nothing to
+    apply the call copies the backup."""
+    import torch
+    sizes = [70001, 65]
+    back, ids = nf4_set(mz, sizes, seed=4)
+    work = [mz.NF4Tensor.empty(n) for n in sizes]
+    bk = mz.ParamSet(back, ids, gaussian=mz.GAUSS_PORTABLE)
+    ps = mz.ParamSet(work, ids, gaussian=mz.GAUSS_PORTABLE)
+    host_back = [download(t) for t in back]
+    seeds = synth.seeds(4, 2)
+    q = synth.grads_int8(8, seed=6)
+    ps.update_multi_from(bk, seeds, q, 2e-3)
+    torch.cuda.synchronize()
+    for t, tb, n, tid, hb in zip(work, back, sizes, ids, host_back):
+        compare_step(nf4, download(t), hb, n, tid,
+                     lambda w, ix, tid=tid: orc.update(w, tid, seeds, q, 2e-3, idx=ix, portable=True),
+                     True, f"from backup tensor {tid}")
+        pb, ab = download(tb)
+        assert np.array_equal(pb, hb[0]) and np.array_equal(ab, hb[1])
+    ps.update_multi_from(bk, seeds, np.zeros(8, np.int8), 2e-3)
+    torch.cuda.synchronize()
+    for t, hb in zip(work, host_back):
+        p, a = download(t)
+        assert np.array_equal(p, hb[0]) and np.array_equal(a, hb[1])
+    ps.close()
+    bk.close()
+
+
+def test_checksum_of_nf4_tensors(mz, orc, nf4):
+    import torch
+    from gpu_util import to_device
+    sizes = [1, 75, 4097, 2048 * 3 + 64 * 5 + 1]
+    dev, ids = nf4_set(mz, sizes, seed=5, ids=[9, 2, 40, 7])
+    f = synth.theta0_tensor((1001,), synth.F32, 1)
+    ps = mz.ParamSet(dev + [to_device(f)], ids + [100])
+    got = ps.checksum()
+    want = sum(nf4.checksum_tensor(*download(t), tid) for t, tid in zip(dev, ids)) + orc.checksum_tensor(f, 100)
+    assert got == want & 0xFFFFFFFFFFFFFFFF
+    # one flipped absmax bit is seen
+    dev[2].absmax[3:4].view(torch.int32).bitwise_xor_(1)
+    assert ps.checksum() != got
+    ps.close()
+
+
+def test_full_size_nf4_6p7b(mz, orc, nf4):
+    """The 6.7B-shaped set in 4-bit storage (3.3 GB of codes), perturb and the
+    K = 64 update, on sampled blocks (first, last and 16 random blocks of every
+    tensor), fast mode."""
+    import torch
+    w = synth.WORKLOADS["opt6.7b-nf4"]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    dev = []
+    for _, shape in w.shapes:
+        n = int(np.prod(shape))
+        codes = torch.randint(0, 256, ((n + 1) // 2,), generator=g, device="cuda", dtype=torch.int32).to(torch.uint8)
+        absmax = torch.rand(((n + 63) // 64,), generator=g, device="cuda") * 0.02 + 0.04
+        dev.append(mz.NF4Tensor(codes, absmax, n))
+    ps = mz.ParamSet(dev)
+    rng = np.random.Generator(np.random.PCG64(11))
+    picks = []
+    for t in dev:
+        nb = (t.numel() + 63) // 64
+        picks.append(np.unique(np.concatenate([[0, nb - 1], rng.integers(0, nb, size=16)])))
+
+    def gather():
+        out = []
+        for t, b in zip(dev, picks):
+            bi = torch.from_numpy(b.astype(np.int64)).cuda()
+            byte_ix = (bi[:, None] * 32 + torch.arange(32, device="cuda")[None, :]).reshape(-1)
+            p = t.codes.index_select(0, byte_ix).cpu().numpy()
+            out.append((nf4.unpack(p, p.size * 2), t.absmax.index_select(0, bi).cpu().numpy()))
+        return out
+
+    s = (0, 0, 0)
+    seeds = synth.workload_seeds(w)
+    q = synth.grads_int8(w.K, w.grad_kind, seed=1)
+    for what, op, app in [
+        ("perturb", lambda: ps.perturb(s, w.eps),
+         lambda tid: (lambda v, ix: orc.perturb(v, tid, s, w.eps, idx=ix))),
+        (f"update K={w.K}", lambda: ps.update_multi(seeds, q, w.lr),
+         lambda tid: (lambda v, ix: orc.update(v, tid, seeds, q, w.lr, idx=ix))),
+    ]:
+        before = gather()
+        op()
+        torch.cuda.synchronize()
+        after = gather()
+        differing = 0
+        for tid, (t, b, st, got) in enumerate(zip(dev, picks, before, after)):
+            r = compare_step(nf4, got, st, t.numel(), tid, app(tid), False, f"{what} tensor {tid}", blocks=b)
+            differing += r["codes_differing"]
+        print(f"6.7B nf4 {what}: codes differing from the oracle near a midpoint: {differing}")
+    ps.close()
+    del dev
+    torch.cuda.empty_cache()
