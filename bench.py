@@ -111,6 +111,33 @@ def flat_views(torch, w, device):
     return flat, views, offs
 
 
+def nf4_buffers(torch, mezo, synth, w, device):
+    """4-bit storage of every tensor as views into one code buffer and one
+    absmax buffer (each view 256-byte aligned)."""
+    import math
+    offs, ctot, atot = [], 0, 0
+    for _, shape in w.shapes:
+        n = int(math.prod(shape))
+        cb, nb = (n + 1) // 2, (n + synth.NF4_BLOCK - 1) // synth.NF4_BLOCK
+        offs.append((ctot, atot, n))
+        ctot += (cb + 255) // 256 * 256
+        atot += (nb + 63) // 64 * 64
+    codes = torch.empty(ctot, dtype=torch.uint8, device=device)
+    absmax = torch.empty(atot, dtype=torch.float32, device=device)
+
+    def views_of(c, a):
+        return [mezo.NF4Tensor(c[co:co + (n + 1) // 2], a[ao:ao + (n + synth.NF4_BLOCK - 1) // synth.NF4_BLOCK], n)
+                for co, ao, n in offs]
+
+    return codes, absmax, views_of
+
+
+def storage_bytes(w) -> float:
+    """Bytes of one element in storage (NF4: half a code byte plus its share
+    of the block's 4-byte absmax)."""
+    return {"f32": 4.0, "bf16": 2.0, "nf4": 0.5 + 4.0 / 64}[w.dtype]
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -128,30 +155,55 @@ def main():
     w = synth.WORKLOADS[args.workload]
     K = w.K
     N = w.numel
+    gauss = mezo.GAUSS_PORTABLE if args.gaussian == "portable" else mezo.GAUSS_FAST
 
     # ---- inputs resident in HBM before timing -------------------------------
-    flat, views, offs = flat_views(torch, w, dev)
-    if N <= 200_000_000:
-        # numpy PCG64 per tensor (the same theta0 the tests and the oracle use)
-        for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
-            h = synth.theta0_tensor(shape, w.dtype, i, 0)
-            if w.dtype == "f32":
-                v.copy_(torch.from_numpy(h))
-            else:
-                v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+    if w.dtype == synth.NF4:
+        codes, absmax, views_of = nf4_buffers(torch, mezo, synth, w, dev)
+        views = views_of(codes, absmax)
+        if N <= 200_000_000:
+            # numpy PCG64 per tensor (the same storage the tests start from)
+            for i, v in enumerate(views):
+                p, a = synth.nf4_theta0_tensor(v.numel(), i, 0)
+                v.codes.copy_(torch.from_numpy(p))
+                v.absmax.copy_(torch.from_numpy(a))
+        else:
+            # the same distribution drawn in HBM by torch's seeded generator
+            g = torch.Generator(device=dev)
+            g.manual_seed(0)
+            codes.random_(0, 256, generator=g)
+            absmax.uniform_(0.04, 0.06, generator=g)
+        flat = codes
+
+        def make_backup():
+            c2, a2 = codes.clone(), absmax.clone()
+            return mezo.ParamSet(views_of(c2, a2), gaussian=gauss), (c2, a2)
     else:
-        # billions of elements: N(0, 0.02) drawn in HBM by torch's seeded generator
-        g = torch.Generator(device=dev)
-        g.manual_seed(0)
-        for v in views:
-            tmp = torch.empty(v.numel(), dtype=torch.float32, device=dev)
-            tmp.normal_(0.0, 0.02, generator=g)
-            v.copy_(tmp)
-            del tmp
+        flat, views, offs = flat_views(torch, w, dev)
+        if N <= 200_000_000:
+            # numpy PCG64 per tensor (the same theta0 the tests and the oracle use)
+            for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
+                h = synth.theta0_tensor(shape, w.dtype, i, 0)
+                if w.dtype == "f32":
+                    v.copy_(torch.from_numpy(h))
+                else:
+                    v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+        else:
+            # billions of elements: N(0, 0.02) drawn in HBM by torch's seeded generator
+            g = torch.Generator(device=dev)
+            g.manual_seed(0)
+            for v in views:
+                tmp = torch.empty(v.numel(), dtype=torch.float32, device=dev)
+                tmp.normal_(0.0, 0.02, generator=g)
+                v.copy_(tmp)
+                del tmp
+
+        def make_backup():
+            b = flat.clone()
+            return mezo.ParamSet([b[a:a + n] for a, n in offs], gaussian=gauss), b
     if args.probe == "copy":
         copy_probe(torch, flat, args)
         return
-    gauss = mezo.GAUSS_PORTABLE if args.gaussian == "portable" else mezo.GAUSS_FAST
     ps = mezo.ParamSet(views, gaussian=gauss)
     eps, lr = w.eps, w.lr
 
@@ -198,7 +250,7 @@ def main():
     ms_per_step = ms_total / args.steps
 
     value = ps_per_step * args.steps / (ms_total / 1e3)
-    bytes_per_launch = 2 * N * (4 if w.dtype == "f32" else 2)
+    bytes_per_launch = 2 * N * storage_bytes(w)
 
     # Engine kernel: every call of the step is one launch of it (per storage
     # type; the sets here have one). Its average launch duration is the timed
@@ -210,8 +262,8 @@ def main():
     ps_per_launch = ps_per_step / n_launch
     achieved = ps_per_launch * INSTR_PER_PARAM_SEED / avg_launch_s / 1e12
     peak = VALU_LANE_INSTR_PER_S / 1e12
-    ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args,
-                                               recs, proj, seeds_t, log, bytes_per_launch, gauss)
+    ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args,
+                                               recs, proj, seeds_t, log, bytes_per_launch)
 
     out = {
         "metric": "param-seed updates/sec (params x K per s)",
@@ -224,13 +276,14 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: {N} {w.dtype} params in {w.n_tensors} tensors, K={K}; "
                                + (f"step = replay T={t_log}xK={K}" if w.T > 0 else
                                   f"step = perturb +eps,-2eps,+eps; quantize {K} grads; "
                                   f"update_multi K={K}; replay T={t_log}xK={K}"),
                    "params": N, "tensors": w.n_tensors, "K": K, "replay_T": t_log,
+                   "storage": w.dtype,
                    "gaussian": args.gaussian,
                    "eps": eps, "lr": lr, "param_seeds_per_step": ps_per_step},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": peak,
@@ -298,8 +351,8 @@ def measured_traffic(workload: str, gaussian: str = "fast"):
     return prof["hbm_bytes_per_dispatch"]
 
 
-def measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args, recs, proj, seeds_t, log,
-                bytes_per_launch, gauss):
+def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj, seeds_t, log,
+                bytes_per_launch):
     """Each operation alone, repeated back to back between two events on the
     kernels' stream (after the timed region, not part of the step)."""
     N, K, lr = w.numel, w.K, w.lr
@@ -338,15 +391,14 @@ def measure_ops(torch, mezo, synth, w, ps, flat, offs, stream, args, recs, proj,
         ops["perturb"] = entry(1, timed(lambda: ps.perturb((0, 0, 0), w.eps)))
         ops["update"] = entry(K, timed(lambda: ps.update_multi(seeds_t[0], q0, lr)))
     ops["replay"] = entry(recs["replay"], timed(lambda: ps.replay(log)))
-    ck = torch.empty(1, dtype=torch.int64, device=flat.device)
+    ck = torch.empty(1, dtype=torch.int64, device="cuda")
     ops["checksum"] = entry(0, timed(lambda: ps.checksum_into(ck)), bytes_per_launch / 2)
     if w.T == 0:
         # Algorithm 1's restore of the backup fused into the apply loop
-        backup_flat = flat.clone()
-        backup = mezo.ParamSet([backup_flat[a:a + n] for a, n in offs], gaussian=gauss)
+        backup, keep = make_backup()
         ops["update_from_backup"] = entry(K, timed(lambda: ps.update_multi_from(backup, seeds_t[0], q0, lr)))
         backup.close()
-        del backup_flat
+        del keep
     return ops
 
 
@@ -385,6 +437,18 @@ def cpu_baseline(w, recs, calls, log, target_s):
     seeds_per_elem = sum(recs[c] for c in calls)
 
     def run(n):
+        if w.dtype == synth.NF4:
+            from oracle import nf4
+            p, a = synth.nf4_theta0_tensor(n, 0, 0)
+            c = nf4.unpack(p, n)
+            t0 = time.perf_counter()
+            if w.T == 0:
+                c, a = nf4.perturb(c, a, 0, (0, 0, 0), w.eps)
+                c, a = nf4.perturb(c, a, 0, (0, 0, 0), -2 * w.eps)
+                c, a = nf4.perturb(c, a, 0, (0, 0, 0), w.eps)
+                c, a = nf4.update(c, a, 0, seeds, q, w.lr)
+            nf4.replay(c, a, 0, log)
+            return time.perf_counter() - t0
         th = synth.theta0_tensor((n,), w.dtype, 0, 0)
         t0 = time.perf_counter()
         if w.T == 0:
