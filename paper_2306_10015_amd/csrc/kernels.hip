@@ -316,12 +316,20 @@ __device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, fl
         w[j] = ((valid >> j) & 1u) ? s.val[(packed >> (4 * j)) & 15u] * am : 0.0f;
 }
 
+// Nibbles of the packed codes that hold existing elements.
+__device__ __forceinline__ uint32_t nf4_nibble_mask(uint32_t valid)
+{
+    const uint32_t k = __builtin_popcount(valid);  // valid is a run of low bits
+    return k >= 8 ? 0xFFFFFFFFu : (1u << (4 * k)) - 1u;
+}
+
 // Quantize a block held by 8 lanes (w = 0 for elements that do not exist):
 // a = max |w| over the block, r = 1 / a (correctly rounded; 0 for a = 0),
 // code = nearest NF4 value to fl32(w * r), ties to the lower code. Returns the
 // packed codes (0 for missing elements) and the new absmax, and replaces w by
-// the dequantized values fl32(v * a) the next step starts from. Every lane of
-// the wave must call it (the block maximum is exchanged across lanes).
+// the dequantized values fl32(v * a) the next step starts from (0 stays 0:
+// x = 0 lies in a bin without a midpoint whose lower value is 0). Every lane
+// of the wave must call it (the block maximum is exchanged across lanes).
 __device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, float (&w)[8], uint32_t& packed,
                                             float& am)
 {
@@ -340,11 +348,10 @@ __device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, flo
         b = b < 0 ? 0 : (b > kNF4Bins - 1 ? kNF4Bins - 1 : b);
         const NF4Bin e = s.bin[b];
         const bool up = x > e.mid;
-        const bool ok = (valid >> j) & 1u;
-        w[j] = ok ? (up ? e.v_hi : e.v_lo) * m : 0.0f;
-        p |= (ok ? e.lo + (up ? 1u : 0u) : 0u) << (4 * j);
+        w[j] = (up ? e.v_hi : e.v_lo) * m;
+        p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
     }
-    packed = p;
+    packed = p & nf4_nibble_mask(valid);
     am = m;
 }
 
@@ -372,8 +379,13 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
         if (rec.last) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                w[j] = ((valid >> j) & 1u) ? w[j] + acc[j] : 0.0f;
+                w[j] = w[j] + acc[j];
                 acc[j] = 0.0f;
+            }
+            if (valid != 0xFFu) {  // a tensor's last lanes only
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (!((valid >> j) & 1u)) w[j] = 0.0f;
             }
             nf4_requant(s, valid, w, packed, am);
         }
@@ -594,41 +606,63 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
 }
 
 // NF4 tensors: the code bytes zero-padded to whole chunks, then the absmax
-// values, chunk numbers continuing. Per tile of 2048 elements, lanes 0..127
-// take its 128 code chunks and lanes 128..143 its 16 absmax chunks.
+// values, chunk numbers continuing. One wave per tile of 2048 elements: every
+// lane reads 16 code bytes (two chunks) and lanes 0..7 also 16 bytes of the
+// tile's 128 absmax bytes.
 __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
 {
+    constexpr uint32_t kWaves = kThreads / 64;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63u;
     uint64_t sum = 0;
-    for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
+    for (uint64_t tile = uint64_t(blockIdx.x) * kWaves + wave; tile < a.total_tiles;
+         tile += uint64_t(gridDim.x) * kWaves) {
         const TensorDesc d = a.tensors[a.tile_tensor[tile]];
         const uint64_t local = tile - d.tile_begin;
         const uint64_t cbytes = (d.numel + 1) / 2;
         const uint64_t cchunks = (cbytes + 7) / 8;
         const uint64_t abytes = 4 * ((d.numel + kNF4Block - 1) / kNF4Block);
         const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
-        const uint32_t lane = threadIdx.x;
-        if (lane < kTileNF4 / 16) {
-            const uint64_t j = local * (kTileNF4 / 16) + lane;  // bytes [8j, 8j + 8) of the codes
-            if (j < cchunks) {
-                uint64_t v = 0;
-                if (8 * j + 8 <= cbytes) {
-                    v = *reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.data + 8 * j);
-                } else {
-                    const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(d.data);
-                    for (uint64_t k = 8 * j; k < cbytes; ++k) v |= uint64_t(b[k]) << (8 * (k - 8 * j));
+        // codes: bytes [16u, 16u + 16) = chunks 2u, 2u + 1
+        const uint64_t u = local * 64 + lane;
+        if (16 * u < cbytes) {
+            uint64_t lo = 0, hi = 0;
+            if (16 * u + 16 <= cbytes) {
+                const uint4 v = load_stream(d.data + 16 * u);
+                lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+                hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+            } else {
+                const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(d.data);
+                for (uint64_t k = 16 * u; k < cbytes; ++k) {
+                    const uint64_t byte = uint64_t(b[k]);
+                    const uint64_t off = k - 16 * u;
+                    if (off < 8)
+                        lo |= byte << (8 * off);
+                    else
+                        hi |= byte << (8 * (off - 8));
                 }
-                sum += fmix64(v ^ (j * kChunkPos) ^ tmix);
             }
-        } else if (lane < kTileNF4 / 16 + kTileNF4 / kNF4Block / 2) {
-            const uint64_t k = local * (kTileNF4 / kNF4Block / 2) + (lane - kTileNF4 / 16);  // absmax chunk
-            if (8 * k < abytes) {
-                uint64_t v;
-                if (8 * k + 8 <= abytes)
-                    v = *reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.aux + 8 * k);
-                else
-                    v = *reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.aux + 8 * k);
-                sum += fmix64(v ^ ((cchunks + k) * kChunkPos) ^ tmix);
+            sum += fmix64(lo ^ (2 * u * kChunkPos) ^ tmix);
+            if (16 * u + 8 < cbytes) sum += fmix64(hi ^ ((2 * u + 1) * kChunkPos) ^ tmix);
+        }
+        // absmax: bytes [ab, ab + 16) = absmax chunks k0, k0 + 1
+        const uint64_t ab = local * (kTileNF4 / kNF4Block * 4) + 16 * uint64_t(lane);
+        if (lane < kTileNF4 / kNF4Block * 4 / 16 && ab < abytes) {
+            const uint64_t k0 = ab / 8;
+            uint32_t f[4] = {0u, 0u, 0u, 0u};
+            if (ab + 16 <= abytes) {
+                const uint4 v = load_stream(d.aux + ab);
+                f[0] = v.x;
+                f[1] = v.y;
+                f[2] = v.z;
+                f[3] = v.w;
+            } else {
+                const MEZO_GLOBAL uint32_t* am = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.aux);
+                for (uint64_t k = ab; k < abytes; k += 4) f[(k - ab) / 4] = am[k / 4];
             }
+            sum += fmix64((uint64_t(f[0]) | (uint64_t(f[1]) << 32)) ^ ((cchunks + k0) * kChunkPos) ^ tmix);
+            if (ab + 8 < abytes)
+                sum += fmix64((uint64_t(f[2]) | (uint64_t(f[3]) << 32)) ^ ((cchunks + k0 + 1) * kChunkPos) ^ tmix);
         }
     }
     add_workgroup_sum(sum, a.out);
@@ -727,9 +761,12 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
     if (e != hipSuccess) return e;
     for (int i = 0; i < n_tables; ++i) {
         if (tables[i].total_tiles == 0) continue;
-        // as many workgroups as fill the device (8 per CU), each striding over tiles
+        // as many workgroups as fill the device (8 per CU), each striding over
+        // tiles (NF4: four tiles at a time, one per wave)
+        const uint64_t per_wg = dtypes[i] == kNF4 ? kThreads / 64 : 1;
+        const uint64_t need = (tables[i].total_tiles + per_wg - 1) / per_wg;
         const uint64_t cap = uint64_t(cus) * 8;
-        const uint64_t grid = tables[i].total_tiles < cap ? tables[i].total_tiles : cap;
+        const uint64_t grid = need < cap ? need : cap;
         const dim3 g{uint32_t(grid)};
         const dim3 b{uint32_t(kThreads)};
         if (dtypes[i] == kF32)
