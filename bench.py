@@ -71,7 +71,8 @@ INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
 #: reported only while the kernel sources it was taken on are unchanged.
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_{workload}_traffic.json")
 KERNEL_SOURCES = ["paper_2306_10015_amd/csrc/kernels.hip", "paper_2306_10015_amd/csrc/engine.hpp",
-                  "paper_2306_10015_amd/csrc/records.hpp"]
+                  "paper_2306_10015_amd/csrc/records.hpp", "paper_2306_10015_amd/csrc/nf4.hpp",
+                  "paper_2306_10015_amd/csrc/launch.hpp"]
 
 T_REPLAY = 4
 

@@ -24,7 +24,8 @@ import os
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 KERNEL_SOURCES = ["paper_2306_10015_amd/csrc/kernels.hip", "paper_2306_10015_amd/csrc/engine.hpp",
-                  "paper_2306_10015_amd/csrc/records.hpp"]
+                  "paper_2306_10015_amd/csrc/records.hpp", "paper_2306_10015_amd/csrc/nf4.hpp",
+                  "paper_2306_10015_amd/csrc/launch.hpp"]
 CUS, XCDS = 256, 8
 
 
@@ -70,13 +71,16 @@ def main():
     ap.add_argument("--copy-write")
     ap.add_argument("--valu")
     ap.add_argument("--elements", type=int, required=True)
-    ap.add_argument("--elem-bytes", type=int, required=True)
+    ap.add_argument("--elem-bytes", type=float, required=True,
+                    help="storage bytes per element (NF4: 0.5625 = half a code byte + 4/64 of an absmax)")
+    ap.add_argument("--copy-bytes", type=float,
+                    help="bytes each way of the copy probe's dispatch (default: the engine's algorithmic read)")
     ap.add_argument("--records", default="", help="records per dispatch, cycling (e.g. 1,1,1,8,32)")
     ap.add_argument("--instr-per-param-seed", type=float, default=15.5)
     ap.add_argument("--commands", help="text file with the commands that made the inputs")
     ap.add_argument("--outdir", default=os.path.join(ROOT, "profiles"))
     a = ap.parse_args()
-    alg = 2 * a.elements * a.elem_bytes
+    alg = round(2 * a.elements * a.elem_bytes)
     lines = [f"# {a.name}", ""]
     summary = {"kernel_source_sha256": source_hash(), "alg_bytes_per_dispatch": alg}
     if a.commands:
@@ -87,7 +91,8 @@ def main():
         lines += ["## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
                   "| kernel | calls | average ns | min ns | max ns | % time |", "|---|---|---|---|---|---|"]
         for r in csv.DictReader(open(one(a.trace, "kernel_stats.csv"))):
-            lines.append(f"| `{r['Name']}` | {r['Calls']} | {float(r['AverageNs']):.0f} | "
+            name = r["Name"] if len(r["Name"]) <= 100 else r["Name"][:80] + " ..."
+            lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']):.0f} | "
                          f"{r['MinNs']} | {r['MaxNs']} | {float(r['Percentage']):.2f} |")
         lines.append("")
     if a.fetch and a.write and a.copy_fetch and a.copy_write:
@@ -99,7 +104,7 @@ def main():
         # the copy probe moves the parameter buffer: the largest dispatch is it
         cf_kib = biggest(cf, "FETCH_SIZE")
         cw_kib = biggest(cw, "WRITE_SIZE")
-        copy_bytes_each = alg / 2  # read this many, write this many
+        copy_bytes_each = a.copy_bytes or alg / 2  # read this many, write this many
         fscale = copy_bytes_each / (cf_kib * 1024)
         wscale = copy_bytes_each / (cw_kib * 1024)
         fk = [e["FETCH_SIZE"] for e in f.values()]
