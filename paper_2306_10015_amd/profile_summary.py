@@ -2,10 +2,13 @@
 under profiles/ (measurement tooling; not used by the engine).
 
     python -m paper_2306_10015_amd.profile_summary --name engine_kernel_opt125m \\
-        --trace gpurun_out/prof_trace --fetch gpurun_out/prof_fetch \\
-        --write gpurun_out/prof_write --copy-fetch gpurun_out/prof_copy_fetch \\
-        --copy-write gpurun_out/prof_copy_write --valu gpurun_out/prof_valu \\
+        --trace out/prof_trace --fetch out/prof_fetch \\
+        --write out/prof_write --copy-fetch out/prof_copy_fetch \\
+        --copy-write out/prof_copy_write --valu out/prof_valu \\
         --elements 123581952 --elem-bytes 4 --records 1,1,1,8,32 --commands cmds.txt
+
+(each directory being the -d output of one rocprofv3 run: see the commands
+listed at the top of every summary).
 
 FETCH_SIZE and WRITE_SIZE are scaled by what the same counters read for a
 plain device copy of known size (--copy-*), per dispatch. VALU busy follows
