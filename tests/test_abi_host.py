@@ -40,6 +40,31 @@ def test_no_cpu_fallback_in_the_binding():
     assert "import oracle" not in src
 
 
+def test_product_package_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2306_10015_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".hpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(import|from)\s+oracle\b", text, re.M), f
+                assert "mezo_oracle" not in text and "liboracle" not in text, f
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """A copy of the binding next to no libmezo.so refuses to import."""
+    import shutil
+    import subprocess
+    import sys
+    pkg = tmp_path / "pkg"
+    pkg.mkdir()
+    shutil.copy(mezo.__file__, pkg / "mezo.py")
+    (pkg / "__init__.py").write_text("")
+    r = subprocess.run([sys.executable, "-c", "import pkg.mezo"], cwd=tmp_path, capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "not built" in r.stderr
+
+
 # ---- codec parity with the oracle -----------------------------------------
 
 CODECS = [(mezo.LINEAR, 1 / 127, 1.0), (mezo.LINEAR, 0.25, 1.0), (mezo.LINEAR, 3e-4, 1.0),
