@@ -397,3 +397,77 @@ def test_checksum_full_125m_set(mz, orc):
     ps.close()
     del tensors
     torch.cuda.empty_cache()
+
+
+# ---- log edge cases and concurrent callers ---------------------------------
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_replay_with_empty_and_zero_steps(mz, orc, dtype):
+    """A log holding an all-zero step, an empty step, a zero-lr step and a step
+    with some zero codes: bit-identical to the same steps as update_multi
+    calls (dropped steps do nothing, not even a rounding) and, in fp32, to the
+    oracle's replay within the bar."""
+    hosts = [synth.theta0_tensor((n,), dtype, i, 8) for i, n in enumerate([4097, 70])]
+    s = [synth.seeds(3, 1, step=t) for t in range(6)]
+    steps = [(s[0], synth.grads_int8(3, seed=1), 1e-3),
+             (s[1], np.zeros(3, np.int8), 1e-3),
+             (s[2][:0], np.zeros(0, np.int8), 1e-3),
+             (s[3], synth.grads_int8(3, seed=4), 0.0),
+             (s[4], np.array([0, 9, 0], np.int8), 2e-3),
+             (s[5], synth.grads_int8(3, seed=6), 1e-3)]
+    devs, ps = make_set(mz, hosts)
+    ps.replay(steps)
+    devs2, ps2 = make_set(mz, hosts)
+    for seeds, q, lr in steps:
+        ps2.update_multi(seeds, q, lr)
+    sync()
+    for i, (h, a, b) in enumerate(zip(hosts, devs, devs2)):
+        ga = to_host(a)
+        assert np.array_equal(ga.view(np.uint8), to_host(b).view(np.uint8))
+        if dtype == synth.F32:
+            assert_theta_close(ga, orc.replay(h.copy(), i, steps), f"replay with empty steps, tensor {i}")
+
+
+def test_concurrent_callers_on_separate_paramsets(mz):
+    """Four host threads, each driving its own paramset on its own stream
+    (perturbs, inline and staged updates, replays, checksums), give the same
+    bits as the same work done by one thread."""
+    import threading
+    import torch
+
+    def work(ps, stream, k, out):
+        with torch.cuda.stream(stream):
+            for it in range(5):
+                ps.perturb((k, it, 0), 1e-3)
+                ps.update_multi(synth.seeds(40, 1, step=it), synth.grads_int8(40, seed=k * 10 + it), 1e-4)
+                ps.replay([(synth.seeds(8, 1, step=100 + it + j), synth.grads_int8(8, seed=j), 1e-4)
+                           for j in range(6)])
+                ps.perturb((k, it, 0), -1e-3)
+            out[k] = ps.checksum(stream)
+
+    def run(parallel):
+        sets, streams, out = [], [], {}
+        for k in range(4):
+            hosts = [synth.theta0_tensor((n,), dt, i, k) for i, (n, dt) in
+                     enumerate([(20000, synth.F32), (9001, synth.BF16)])]
+            sets.append(make_set(mz, hosts))
+            streams.append(torch.cuda.Stream())
+        torch.cuda.synchronize()
+        if parallel:
+            threads = [threading.Thread(target=work, args=(sets[k][1], streams[k], k, out)) for k in range(4)]
+            for t in threads:
+                t.start()
+            for t in threads:
+                t.join()
+        else:
+            for k in range(4):
+                work(sets[k][1], streams[k], k, out)
+        torch.cuda.synchronize()
+        return out, [[to_host(d) for d in devs] for devs, _ in sets]
+
+    seq_sums, seq_vals = run(False)
+    par_sums, par_vals = run(True)
+    assert seq_sums == par_sums
+    for a, b in zip(seq_vals, par_vals):
+        for x, y in zip(a, b):
+            assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
