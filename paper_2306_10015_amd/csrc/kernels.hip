@@ -312,8 +312,26 @@ __device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, fl
                                             float (&w)[8])
 {
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-        w[j] = ((valid >> j) & 1u) ? s.val[(packed >> (4 * j)) & 15u] * am : 0.0f;
+    for (int j = 0; j < 8; ++j) w[j] = s.val[(packed >> (4 * j)) & 15u] * am;
+    if (valid != 0xFFu) {  // a tensor's last lanes only
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
+}
+
+// max over the 8 lanes of a block (lanes 8i .. 8i + 7) of a value >= 0:
+// swap neighbours, then pairs within each quad, then the two quads of each
+// half-row (DPP quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror).
+// Non-negative floats order like their bit patterns, so the maximum is taken
+// on the integers.
+__device__ __forceinline__ float max8(float m)
+{
+    uint32_t u = __float_as_uint(m);
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0xB1, 0xF, 0xF, false)));
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0x4E, 0xF, 0xF, false)));
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0x141, 0xF, 0xF, false)));
+    return __uint_as_float(u);
 }
 
 // Nibbles of the packed codes that hold existing elements.
@@ -326,19 +344,19 @@ __device__ __forceinline__ uint32_t nf4_nibble_mask(uint32_t valid)
 // Quantize a block held by 8 lanes (w = 0 for elements that do not exist):
 // a = max |w| over the block, r = 1 / a (correctly rounded; 0 for a = 0),
 // code = nearest NF4 value to fl32(w * r), ties to the lower code. Returns the
-// packed codes (0 for missing elements) and the new absmax, and replaces w by
-// the dequantized values fl32(v * a) the next step starts from (0 stays 0:
-// x = 0 lies in a bin without a midpoint whose lower value is 0). Every lane
-// of the wave must call it (the block maximum is exchanged across lanes).
+// packed codes (0 for missing elements) and the new absmax; with kNext it also
+// replaces w by the dequantized values fl32(v * a) the next step starts from
+// (0 stays 0: x = 0 lies in a bin without a midpoint whose lower value is 0).
+// Every lane of the wave must call it (the block maximum is exchanged across
+// lanes).
+template <bool kNext>
 __device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, float (&w)[8], uint32_t& packed,
                                             float& am)
 {
     float m = 0.0f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
-    m = fmaxf(m, __shfl_xor(m, 1));
-    m = fmaxf(m, __shfl_xor(m, 2));
-    m = fmaxf(m, __shfl_xor(m, 4));
+    m = max8(m);
     const float r = m > 0.0f ? 1.0f / m : 0.0f;
     uint32_t p = 0u;
 #pragma unroll
@@ -348,7 +366,7 @@ __device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, flo
         b = b < 0 ? 0 : (b > kNF4Bins - 1 ? kNF4Bins - 1 : b);
         const NF4Bin e = s.bin[b];
         const bool up = x > e.mid;
-        w[j] = (up ? e.v_hi : e.v_lo) * m;
+        if constexpr (kNext) w[j] = (up ? e.v_hi : e.v_lo) * m;
         p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
     }
     packed = p & nf4_nibble_mask(valid);
@@ -367,7 +385,7 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
     for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
     const BlockPre pre0 = block_pre(uint32_t(e0 >> 2));
     const BlockPre pre1 = block_pre(uint32_t((e0 >> 2) + 1));
-    for (uint32_t r = 0; r < a.n_rec; ++r) {
+    const auto accumulate = [&](uint32_t r) {
         const SeedRec& rec = rec_at<kInline>(a, r);
         const SeedUniform u = seed_uniform(rec, d.tensor_id);
         const float c = rec.coef;
@@ -376,20 +394,35 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
         accumulate4<kPortable>(c, w0, w1, w2, w3, acc[0], acc[1], acc[2], acc[3]);
         philox_words(u, pre1, w0, w1, w2, w3);
         accumulate4<kPortable>(c, w0, w1, w2, w3, acc[4], acc[5], acc[6], acc[7]);
-        if (rec.last) {
+    };
+    const auto step_end = [&]() {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                w[j] = w[j] + acc[j];
-                acc[j] = 0.0f;
-            }
-            if (valid != 0xFFu) {  // a tensor's last lanes only
+        for (int j = 0; j < 8; ++j) {
+            w[j] = w[j] + acc[j];
+            acc[j] = 0.0f;
+        }
+        if (valid != 0xFFu) {  // a tensor's last lanes only
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (!((valid >> j) & 1u)) w[j] = 0.0f;
-            }
-            nf4_requant(s, valid, w, packed, am);
+            for (int j = 0; j < 8; ++j)
+                if (!((valid >> j) & 1u)) w[j] = 0.0f;
+        }
+    };
+    if (a.n_rec == 0) {  // out of place with nothing to apply: a copy
+        nf4_store(d.data, d.aux, e0, d.numel, packed, am);
+        return;
+    }
+    // every record list ends a step with its last record, which is peeled off
+    // the loop: its quantization needs no values for a next step
+    for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
+        accumulate(r);
+        if (rec_at<kInline>(a, r).last) {
+            step_end();
+            nf4_requant<true>(s, valid, w, packed, am);
         }
     }
+    accumulate(a.n_rec - 1);
+    step_end();
+    nf4_requant<false>(s, valid, w, packed, am);
     nf4_store(d.data, d.aux, e0, d.numel, packed, am);
 }
 
@@ -463,7 +496,7 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
     nf4_lds_init(lds);
     uint32_t packed;
     float am;
-    nf4_requant(lds, valid, w, packed, am);
+    nf4_requant<false>(lds, valid, w, packed, am);
     nf4_store(a.codes, a.absmax, e0, a.n, packed, am);
 }
 
