@@ -353,6 +353,16 @@ class ParamSet:
                                _stream_ptr(stream)), "mezo_replay")
 
 
+def step_lr(eta: float, n_grads: int, sqrt_scaling: bool = False) -> float:
+    """The per-gradient learning rate of one iteration's apply loop: each
+    projected gradient is weighted by eta / n_grads (Algorithm 1); with the
+    learning rate scaled by the square root of the number of perturbations
+    (Section 4) that is eta * sqrt(n) / n = eta / sqrt(n)."""
+    if n_grads <= 0:
+        raise ValueError("n_grads must be positive")
+    return eta / math.sqrt(n_grads) if sqrt_scaling else eta / n_grads
+
+
 def quantize_projgrad(g, codec_: Codec = DEFAULT_CODEC) -> np.ndarray:
     ga = np.ascontiguousarray(g, dtype=np.float32)
     q = np.zeros(ga.size, dtype=np.int8)

@@ -299,3 +299,11 @@ def test_from_calls_check_layout_and_overlap():
     finally:
         for h in (dst, ok_src, bad_n, bad_id, bad_cnt, overlap, twin):
             lib.mezo_paramset_destroy(h)
+
+
+def test_step_lr():
+    assert mezo.step_lr(0.1, 4) == pytest.approx(0.025)
+    assert mezo.step_lr(0.1, 4, sqrt_scaling=True) == pytest.approx(0.05)
+    assert mezo.step_lr(1e-6, 1) == 1e-6
+    with pytest.raises(ValueError):
+        mezo.step_lr(0.1, 0)
