@@ -594,6 +594,6 @@ const char* mezo_strerror(int code)
 
 const char* mezo_last_error(void) { return t_last_error.c_str(); }
 
-int mezo_version(void) { return 100; }
+int mezo_version(void) { return 200; }
 
 }  // extern "C"

@@ -110,3 +110,32 @@ def test_full_size_replay_1p3b(mz, orc):
     ps.close()
     del tensors
     torch.cuda.empty_cache()
+
+
+def test_late_joiner_matches_replica_checksum_1p3b(mz):
+    """Appendix B end to end at full size: a replica applies T = 200 logged
+    steps of K = 32 one iteration at a time (update_multi per step); a late
+    joiner starting from the same weights replays the whole log in one call.
+    ChecksumMatch (Algorithm 1) then finds them identical, and so does a
+    comparison of every byte."""
+    import torch
+    w = synth.WORKLOADS["replay1.3b"]
+    replica = theta_on_device(w, seed=5, device_rng=True)
+    joiner = [t.clone() for t in replica]
+    ps_r, ps_j = mz.ParamSet(replica), mz.ParamSet(joiner)
+    assert ps_r.checksum() == ps_j.checksum()
+    steps = [(synth.seeds(w.machines, w.samples_per_machine, step=t),
+              synth.grads_int8(w.K, "uniform", seed=900 + t), w.lr * (1 + t % 3)) for t in range(w.T)]
+    for seeds, q, lr in steps:
+        ps_r.update_multi(seeds, q, lr)
+    ps_j.replay(steps)
+    torch.cuda.synchronize()
+    c_r, c_j = ps_r.checksum(), ps_j.checksum()
+    print(f"late joiner after T={w.T}: checksum {c_j:#018x}, replica {c_r:#018x}")
+    assert c_r == c_j
+    for a, b in zip(replica, joiner):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    ps_r.close()
+    ps_j.close()
+    del replica, joiner
+    torch.cuda.empty_cache()
