@@ -307,3 +307,22 @@ def test_step_lr():
     assert mezo.step_lr(1e-6, 1) == 1e-6
     with pytest.raises(ValueError):
         mezo.step_lr(0.1, 0)
+
+
+@pytest.mark.parametrize("compiler,std", [("gcc", "-std=c99"), ("g++", "-std=c++17")])
+def test_header_is_plain_c_and_cpp(tmp_path, compiler, std):
+    """include/mezo.h needs no HIP or torch header and compiles as C99 and
+    C++ with warnings as errors."""
+    import shutil
+    import subprocess
+    if not shutil.which(compiler):
+        pytest.skip(f"{compiler} not available")
+    src = tmp_path / ("use.c" if compiler == "gcc" else "use.cpp")
+    src.write_text('#include "mezo.h"\n'
+                   'int use(mezo_paramset_t ps, void* s) {\n'
+                   '    mezo_seed_t seed = {1u, 2u, 3u};\n'
+                   '    return mezo_perturb(ps, seed, 1e-3f, s) + (int)sizeof(mezo_tensor_t);\n'
+                   '}\n')
+    r = subprocess.run([compiler, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
+                        "-I", os.path.join(ROOT, "include"), str(src)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
