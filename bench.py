@@ -390,6 +390,10 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
     ops = {}
     if w.T == 0:
         ops["perturb"] = entry(1, timed(lambda: ps.perturb((0, 0, 0), w.eps)))
+        # Algorithm 1 between two samples: restore sample j and perturb for
+        # sample j + 1 in one pass (two separate perturbs cost two)
+        ops["restore_and_next_perturb"] = entry(
+            2, timed(lambda: ps.perturb_multi([(0, 0, 0), (0, 0, 1)], [w.eps, w.eps])))
         ops["update"] = entry(K, timed(lambda: ps.update_multi(seeds_t[0], q0, lr)))
     ops["replay"] = entry(recs["replay"], timed(lambda: ps.replay(log)))
     ck = torch.empty(1, dtype=torch.int64, device="cuda")

@@ -207,6 +207,17 @@ MEZO_API int mezo_paramset_set_gaussian(mezo_paramset_t ps, uint32_t gaussian);
  * scale = 0 enqueues nothing. */
 MEZO_API int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream);
 
+/* Several PerturbParameters calls in one pass (Algorithm 1, the loop over
+ * samples): for i = 0 .. n-1 in order, theta <- round(theta + scales[i] *
+ * z(seeds[i])), rounding to storage after every term — bit-identical to n
+ * mezo_perturb calls, for the traffic of one. Between two samples, the restore
+ * of sample j (+eps, seed j) and the perturbation for sample j + 1 (+eps,
+ * seed j + 1) share one sweep, so a sample costs two sweeps instead of three.
+ * Every scale must be finite (MEZO_ERANGE); zero terms are dropped; n = 0 (or
+ * nothing left) enqueues nothing; seeds may repeat and need no order. */
+MEZO_API int mezo_perturb_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const float* scales, uint32_t n,
+                                void* stream);
+
 /* The apply loop of one iteration — Algorithm 1 and Section 2: in
  * machine/timestamp order, perturb by -grad_k * lr with seed_k. Fused: for
  * every element, acc = sum_k c_k z(seed_k) with c_k = fl32(-lr * g~_k)

@@ -408,6 +408,22 @@ int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream
     return launch_records(ps, recs, static_cast<hipStream_t>(stream));
 }
 
+int mezo_perturb_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const float* scales, uint32_t n,
+                       void* stream)
+{
+    if (!ps) return MEZO_EINVAL;
+    if (n == 0) return MEZO_OK;
+    if (!seeds || !scales) return MEZO_EINVAL;
+    for (uint32_t i = 0; i < n; ++i)
+        if (!std::isfinite(scales[i])) return MEZO_ERANGE;
+    std::vector<mezo::SeedRec> recs;
+    recs.reserve(n);
+    for (uint32_t i = 0; i < n; ++i)
+        if (scales[i] != 0.0f) recs.push_back(make_rec(seeds[i], scales[i], true, fold_of(ps)));
+    std::lock_guard<std::mutex> lock(ps->mu);
+    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+}
+
 int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t* q, uint32_t K,
                       const mezo_codec_t* codec, float lr, void* stream)
 {

@@ -62,7 +62,7 @@ class Step(ctypes.Structure):
 #: Every symbol include/mezo.h declares.
 EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
            "mezo_paramset_set_gaussian",
-           "mezo_perturb", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
+           "mezo_perturb", "mezo_perturb_multi", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
            "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
            "mezo_dequantize", "mezo_nf4_quantize", "mezo_nf4_dequantize", "mezo_debug_generate",
            "mezo_strerror", "mezo_last_error", "mezo_version")
@@ -89,6 +89,8 @@ def _load() -> ctypes.CDLL:
     L.mezo_paramset_set_gaussian.restype = i32
     L.mezo_perturb.argtypes = [vp, Seed, f32, vp]
     L.mezo_perturb.restype = i32
+    L.mezo_perturb_multi.argtypes = [vp, vp, vp, u32, vp]
+    L.mezo_perturb_multi.restype = i32
     L.mezo_update_multi.argtypes = [vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
     L.mezo_update_multi.restype = i32
     L.mezo_replay.argtypes = [vp, ctypes.POINTER(Step), u32, ctypes.POINTER(Codec), vp]
@@ -296,6 +298,16 @@ class ParamSet:
         """PerturbParameters: theta += scale * z(seed)."""
         _check(lib.mezo_perturb(self._h, _seed(seed), float(scale), _stream_ptr(stream)),
                "mezo_perturb")
+
+    def perturb_multi(self, seeds, scales, stream=None) -> None:
+        """Perturbs in sequence in one pass: theta += scales[i] * z(seeds[i]),
+        rounded after each (e.g. restore sample j and perturb for sample j+1)."""
+        sa = seeds_array(seeds)
+        sc = np.ascontiguousarray(scales, dtype=np.float32)
+        if sa.size != sc.size:
+            raise ValueError("seeds and scales differ in length")
+        _check(lib.mezo_perturb_multi(self._h, sa.ctypes.data, sc.ctypes.data, sa.size, _stream_ptr(stream)),
+               "mezo_perturb_multi")
 
     def update_multi(self, seeds, q, lr: float, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
         """Apply loop of one iteration: theta -= lr * sum_k deq(q_k) z(seed_k)."""

@@ -232,6 +232,22 @@ def test_perturb_and_replay_argument_checks(fake_ps):
     assert lib.mezo_replay(fake_ps, steps, 2, c, None) == mezo.ERANGE
 
 
+def test_perturb_multi_argument_checks(fake_ps):
+    lib = mezo.lib
+    s = seeds_of((0, 0, 0), (1, 0, 0))
+    sc = np.array([1e-3, float("nan")], dtype=np.float32)
+    assert lib.mezo_perturb_multi(fake_ps, s.ctypes.data, sc.ctypes.data, 2, None) == mezo.ERANGE
+    sc = np.array([1e-3, float("inf")], dtype=np.float32)
+    assert lib.mezo_perturb_multi(fake_ps, s.ctypes.data, sc.ctypes.data, 2, None) == mezo.ERANGE
+    assert lib.mezo_perturb_multi(None, s.ctypes.data, sc.ctypes.data, 2, None) == mezo.EINVAL
+    assert lib.mezo_perturb_multi(fake_ps, None, sc.ctypes.data, 2, None) == mezo.EINVAL
+    assert lib.mezo_perturb_multi(fake_ps, s.ctypes.data, None, 2, None) == mezo.EINVAL
+    # nothing to apply: OK without touching a device
+    assert lib.mezo_perturb_multi(fake_ps, None, None, 0, None) == mezo.OK
+    z = np.zeros(2, dtype=np.float32)
+    assert lib.mezo_perturb_multi(fake_ps, s.ctypes.data, z.ctypes.data, 2, None) == mezo.OK
+
+
 def test_debug_generate_range_check():
     lib = mezo.lib
     assert lib.mezo_debug_generate(mezo.Seed(0, 0, 0), 0, (1 << 34) - 4, 8, 0, 0x1000, None, None) == mezo.EINVAL

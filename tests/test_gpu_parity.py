@@ -471,3 +471,48 @@ def test_concurrent_callers_on_separate_paramsets(mz):
     for a, b in zip(seq_vals, par_vals):
         for x, y in zip(a, b):
             assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("n", [2, 37])
+def test_perturb_multi_is_sequential_perturbs(mz, orc, dtype, n):
+    """n perturbs in one pass (inline and staged records) are bit-identical
+    to n perturb calls, and match the oracle's sequential perturbs."""
+    hosts = [synth.theta0_tensor((m,), dtype, i, 9) for i, m in enumerate([5003, 2048, 17])]
+    rng = np.random.Generator(np.random.PCG64(n))
+    seeds = [(int(rng.integers(0, 4)), int(rng.integers(0, 100)), int(rng.integers(0, 16))) for _ in range(n)]
+    scales = (rng.choice([1e-3, -2e-3, 0.0, 5e-4], size=n)).astype(np.float32)
+    devs, ps = make_set(mz, hosts)
+    ps.perturb_multi(seeds, scales)
+    devs2, ps2 = make_set(mz, hosts)
+    for sd, sc in zip(seeds, scales):
+        ps2.perturb(sd, float(sc))
+    sync()
+    for i, (h, a, b) in enumerate(zip(hosts, devs, devs2)):
+        ga = to_host(a)
+        assert np.array_equal(ga.view(np.uint8), to_host(b).view(np.uint8))
+        if dtype == synth.F32:
+            ref = h.copy()
+            for sd, sc in zip(seeds, scales):
+                orc.perturb(ref, i, sd, float(sc))
+            assert_theta_close(ga, ref, f"perturb_multi tensor {i}")
+
+
+def test_perturb_multi_nf4_portable_bit_exact(mz, orc):
+    """Restore sample j and perturb for sample j + 1 in one pass on 4-bit
+    storage: bit-identical to the oracle's two perturbs (portable mode)."""
+    import torch
+    from oracle import nf4
+    n = 4097
+    p, a = synth.nf4_theta0_tensor(n, 0)
+    t = mz.NF4Tensor(torch.from_numpy(p.copy()).cuda(), torch.from_numpy(a.copy()).cuda(), n)
+    ps = mz.ParamSet([t], [4], gaussian=mz.GAUSS_PORTABLE)
+    seeds, scales = [(1, 5, 3), (1, 5, 4)], [1e-3, 1e-3]
+    ps.perturb_multi(seeds, scales)
+    sync()
+    c, am = nf4.unpack(p, n), a
+    for sd, sc in zip(seeds, scales):
+        c, am = nf4.perturb(c, am, 4, sd, sc, portable=True)
+    assert np.array_equal(t.codes.cpu().numpy(), nf4.pack(c))
+    assert np.array_equal(t.absmax.cpu().numpy().view(np.uint32), am.view(np.uint32))
+    ps.close()
