@@ -96,6 +96,10 @@ def lib() -> ctypes.CDLL:
         L.orc_replay.restype = i32
         L.orc_box_muller_portable.argtypes = [vp, vp]
         L.orc_box_muller_portable.restype = None
+        L.orc_box_muller_blocks.argtypes = [vp, u64, vp]
+        L.orc_box_muller_blocks.restype = None
+        L.orc_box_muller_portable_blocks.argtypes = [vp, u64, vp]
+        L.orc_box_muller_portable_blocks.restype = None
         L.orc_z_portable.argtypes = [Seed, u32, u64]
         L.orc_z_portable.restype = f32
         L.orc_generate_portable.argtypes = [Seed, u32, u64, u64, vp]
@@ -188,6 +192,18 @@ def generate(seed, tensor_id: int, first: int, count: int, words=True, z=True,
         _check(lib().orc_generate_portable(_seed(seed), tensor_id, first, count, _ptr(g)),
                "generate_portable")
     return w, g
+
+
+def box_muller_blocks(words, portable: bool = False) -> np.ndarray:
+    """z (fp32) of every block of 4 given words: the fp64 transform rounded
+    once, or the portable binary32 one."""
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    if w.size % 4:
+        raise ValueError("words come in blocks of 4")
+    z = np.zeros(w.size, dtype=np.float32)
+    fn = lib().orc_box_muller_portable_blocks if portable else lib().orc_box_muller_blocks
+    fn(_ptr(w), w.size // 4, _ptr(z))
+    return z
 
 
 def box_muller_portable(words) -> np.ndarray:

@@ -103,6 +103,19 @@ void orc_box_muller(const uint32_t w[4], double z[4])
     }
 }
 
+/* Box-Muller of n blocks of given words (4 per block), each z rounded once
+ * to fp32 as orc_z does: for checking a transform over chosen inputs. */
+void orc_box_muller_blocks(const uint32_t* w, uint64_t n_blocks, float* z)
+{
+    long long n = (long long)n_blocks;
+#pragma omp parallel for schedule(static)
+    for (long long b = 0; b < n; ++b) {
+        double zz[4];
+        orc_box_muller(w + 4 * b, zz);
+        for (int j = 0; j < 4; ++j) z[4 * b + j] = (float)zz[j];
+    }
+}
+
 float orc_z(orc_seed_t s, uint32_t tensor_id, uint64_t e)
 {
     uint32_t w[4];
@@ -399,6 +412,13 @@ void orc_box_muller_portable(const uint32_t w[4], float z[4])
 {
     box_muller_pair_portable(w[0], w[1], &z[0], &z[1]);
     box_muller_pair_portable(w[2], w[3], &z[2], &z[3]);
+}
+
+void orc_box_muller_portable_blocks(const uint32_t* w, uint64_t n_blocks, float* z)
+{
+    long long n = (long long)n_blocks;
+#pragma omp parallel for schedule(static)
+    for (long long b = 0; b < n; ++b) orc_box_muller_portable(w + 4 * b, z + 4 * b);
 }
 
 float orc_z_portable(orc_seed_t s, uint32_t tensor_id, uint64_t e)

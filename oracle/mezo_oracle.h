@@ -63,6 +63,8 @@ void orc_block_words(orc_seed_t s, uint32_t tensor_id, uint64_t e, uint32_t out[
 
 /* Box-Muller on one block of four words, fp64: z[0..3] (not rounded). */
 void orc_box_muller(const uint32_t w[4], double z[4]);
+/* orc_box_muller over n blocks of given words, each z rounded once to fp32. */
+void orc_box_muller_blocks(const uint32_t* w, uint64_t n_blocks, float* z);
 
 /* The fp32 Gaussian of element e: fl32 of the fp64 Box-Muller value. */
 float orc_z(orc_seed_t s, uint32_t tensor_id, uint64_t e);
@@ -134,6 +136,8 @@ int orc_replay(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
  * theta' = round_st(theta + acc) with the sum in binary32.
  */
 void  orc_box_muller_portable(const uint32_t w[4], float z[4]);
+/* orc_box_muller_portable over n blocks of given words. */
+void  orc_box_muller_portable_blocks(const uint32_t* w, uint64_t n_blocks, float* z);
 float orc_z_portable(orc_seed_t s, uint32_t tensor_id, uint64_t e);
 int   orc_generate_portable(orc_seed_t s, uint32_t tensor_id, uint64_t first, uint64_t count,
                             float* z);

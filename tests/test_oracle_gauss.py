@@ -111,3 +111,18 @@ def test_no_correlation_between_seeds_and_within_pairs(orc, big_sample):
     assert abs(np.corrcoef(pairs[:, 0], pairs[:, 1])[0, 1]) <= 5 / math.sqrt(n // 2)
     quads = big_sample.reshape(-1, 4)
     assert abs(np.corrcoef(quads[:, 0], quads[:, 2])[0, 1]) <= 5 / math.sqrt(n // 4)
+
+
+def test_block_array_forms_equal_the_single_block_forms(orc):
+    """The oracle's many-block Box-Muller (fast and portable) is its
+    single-block transform applied block by block (fp64 rounded once to fp32
+    for the fast one)."""
+    rng = np.random.Generator(np.random.PCG64(77))
+    w = rng.integers(0, 2**32, size=4 * 500, dtype=np.uint64).astype(np.uint32)
+    w[:8] = [0, 0, 0xFFFFFFFF, 0xFFFFFFFF, 0xFF, 0x100, 0x80000000, 0x7FFFFF00]
+    z = orc.box_muller_blocks(w)
+    zp = orc.box_muller_blocks(w, portable=True)
+    for b in range(500):
+        blk = w[4 * b:4 * b + 4]
+        assert np.array_equal(z[4 * b:4 * b + 4], orc.box_muller(blk).astype(np.float32))
+        assert np.array_equal(zp[4 * b:4 * b + 4], orc.box_muller_portable(blk))
