@@ -310,6 +310,14 @@ MEZO_API int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t 
                                  uint64_t count, uint32_t gaussian, uint32_t* words_dev,
                                  float* z_dev, void* stream);
 
+/* The Gaussian transform alone, on given words: z_dev[4b .. 4b+3] from
+ * words_dev[4b .. 4b+3] for b < n_blocks, computed as `gaussian` says — the
+ * pair transform above, so that it can be checked over chosen inputs (every
+ * value of u1, every value of u2). Both device arrays 16-byte aligned,
+ * n_blocks <= 2^32, a known `gaussian` (MEZO_EINVAL otherwise). */
+MEZO_API int mezo_debug_box_muller(const uint32_t* words_dev, uint64_t n_blocks, uint32_t gaussian,
+                                   float* z_dev, void* stream);
+
 MEZO_API const char* mezo_strerror(int code);
 
 /* The HIP runtime's message of the last MEZO_EHIP failure on this thread

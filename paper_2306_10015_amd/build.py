@@ -54,11 +54,13 @@ def build(verbose: bool = False) -> Path:
     BUILD_DIR.mkdir(exist_ok=True)
     cc = hipcc()
     k_obj = BUILD_DIR / "kernels.o"
+    i_obj = BUILD_DIR / "inspect.o"
     a_obj = BUILD_DIR / "api.o"
     _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / "kernels.hip"), "-o", str(k_obj)])
+    _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / "inspect.hip"), "-o", str(i_obj)])
     _run([cc, *COMMON, "-c", str(CSRC / "api.cpp"), "-o", str(a_obj)])
     tmp = LIB.with_suffix(".so.tmp")
-    _run([cc, "-shared", "-fPIC", *DEVICE, str(k_obj), str(a_obj), "-o", str(tmp)])
+    _run([cc, "-shared", "-fPIC", *DEVICE, str(k_obj), str(i_obj), str(a_obj), "-o", str(tmp)])
     os.replace(tmp, LIB)
     # the benchmark's issue-rate probe (measurement only, not part of libmezo)
     ptmp = PROBE_LIB.with_suffix(".so.tmp")

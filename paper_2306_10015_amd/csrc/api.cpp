@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "../../include/mezo.h"
+#include "inspect.hpp"
 #include "launch.hpp"
 #include "records.hpp"
 
@@ -591,6 +592,18 @@ int mezo_debug_generate(mezo_seed_t seed, uint32_t tensor_id, uint64_t first_ele
     a.words = words_dev;
     a.z = z_dev;
     MEZO_HIP(mezo::launch_generate(a, static_cast<hipStream_t>(stream)));
+    return MEZO_OK;
+}
+
+int mezo_debug_box_muller(const uint32_t* words_dev, uint64_t n_blocks, uint32_t gaussian, float* z_dev,
+                          void* stream)
+{
+    if (gaussian != MEZO_GAUSS_FAST && gaussian != MEZO_GAUSS_PORTABLE) return MEZO_EINVAL;
+    if (n_blocks == 0) return MEZO_OK;
+    if (!words_dev || !z_dev || n_blocks > (uint64_t(1) << 32)) return MEZO_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(words_dev) | reinterpret_cast<uintptr_t>(z_dev)) & 15u) return MEZO_EINVAL;
+    MEZO_HIP(mezo::launch_box_muller(words_dev, n_blocks, gaussian == MEZO_GAUSS_PORTABLE ? 1u : 0u, z_dev,
+                                     static_cast<hipStream_t>(stream)));
     return MEZO_OK;
 }
 

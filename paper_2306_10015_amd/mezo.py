@@ -64,7 +64,7 @@ EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel
            "mezo_paramset_set_gaussian",
            "mezo_perturb", "mezo_perturb_multi", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
            "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
-           "mezo_dequantize", "mezo_nf4_quantize", "mezo_nf4_dequantize", "mezo_debug_generate",
+           "mezo_dequantize", "mezo_nf4_quantize", "mezo_nf4_dequantize", "mezo_debug_generate", "mezo_debug_box_muller",
            "mezo_strerror", "mezo_last_error", "mezo_version")
 
 
@@ -111,6 +111,8 @@ def _load() -> ctypes.CDLL:
     L.mezo_nf4_dequantize.restype = i32
     L.mezo_debug_generate.argtypes = [Seed, u32, u64, u64, u32, vp, vp, vp]
     L.mezo_debug_generate.restype = i32
+    L.mezo_debug_box_muller.argtypes = [vp, u64, u32, vp, vp]
+    L.mezo_debug_box_muller.restype = i32
     L.mezo_strerror.argtypes = [i32]
     L.mezo_strerror.restype = ctypes.c_char_p
     L.mezo_last_error.argtypes = []
@@ -403,6 +405,18 @@ def debug_generate(seed, tensor_id: int, first: int, count: int, words=True, z=T
                                    None if zz is None else zz.data_ptr(), _stream_ptr(stream)),
            "mezo_debug_generate")
     return w, zz
+
+
+def debug_box_muller(words, gaussian: int = GAUSS_FAST, stream=None):
+    """z (float32 device tensor) of the given words (int32/uint32-bit device
+    tensor, a multiple of 4 long), through the library's Gaussian transform."""
+    import torch
+    if words.numel() % 4 or not words.is_contiguous() or words.element_size() != 4:
+        raise ValueError("words: contiguous 32-bit device tensor, a multiple of 4 long")
+    z = torch.empty(words.numel(), dtype=torch.float32, device=words.device)
+    _check(lib.mezo_debug_box_muller(words.data_ptr(), words.numel() // 4, int(gaussian), z.data_ptr(),
+                                     _stream_ptr(stream)), "mezo_debug_box_muller")
+    return z
 
 
 def version() -> int:
