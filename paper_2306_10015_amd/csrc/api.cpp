@@ -133,7 +133,10 @@ struct mezo_paramset {
     std::atomic<uint32_t> gaussian{MEZO_GAUSS_FAST};
     mezo::TensorDesc* d_table[kTypes] = {};
     uint32_t* d_tile_tensor[kTypes] = {};  // tensor index of every tile
-    hipEvent_t last = nullptr;  // after the latest launch that reads a table
+    // One event per stream the paramset's kernels ran on, recorded after the
+    // latest launch on that stream: destroy waits for all of them before it
+    // frees the tables (work on an earlier stream may still be running).
+    std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
 
     // Staging of record lists too long for the kernel arguments: a ring of
     // slots, each reused only after the launch that read it has completed.
@@ -182,7 +185,6 @@ int ensure_device(mezo_paramset* ps)
             e = hipMemcpy(ps->d_tile_tensor[dt], owner.data(), owner.size() * sizeof(uint32_t),
                           hipMemcpyHostToDevice);
     }
-    if (e == hipSuccess) e = hipEventCreateWithFlags(&ps->last, hipEventDisableTiming);
     if (e != hipSuccess) {
         for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
@@ -193,6 +195,21 @@ int ensure_device(mezo_paramset* ps)
         return hip_fail(e, "paramset device table");
     }
     ps->device = dev;
+    return MEZO_OK;
+}
+
+// Record that ps's tables are read by work enqueued so far on stream.
+int mark_use(mezo_paramset* ps, hipStream_t stream)
+{
+    for (auto& u : ps->uses)
+        if (u.first == stream) {
+            MEZO_HIP(hipEventRecord(u.second, stream));
+            return MEZO_OK;
+        }
+    hipEvent_t ev = nullptr;
+    MEZO_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+    ps->uses.emplace_back(stream, ev);
+    MEZO_HIP(hipEventRecord(ev, stream));
     return MEZO_OK;
 }
 
@@ -250,9 +267,9 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
         MEZO_HIP(mezo::launch_engine(args, dt, ps->gaussian.load() == MEZO_GAUSS_PORTABLE, stream));
     }
     if (slot) MEZO_HIP(hipEventRecord(slot->done, stream));
-    MEZO_HIP(hipEventRecord(ps->last, stream));
-    if (src && src != ps) MEZO_HIP(hipEventRecord(src->last, stream));
-    return MEZO_OK;
+    rc = mark_use(ps, stream);
+    if (rc == MEZO_OK && src && src != ps) rc = mark_use(src, stream);
+    return rc;
 }
 
 // Byte ranges [begin, end) of device memory a tensor occupies.
@@ -369,9 +386,9 @@ void mezo_paramset_destroy(mezo_paramset_t ps)
     if (!ps) return;
     {
         std::lock_guard<std::mutex> lock(ps->mu);
-        if (ps->last) {
-            (void)hipEventSynchronize(ps->last);
-            (void)hipEventDestroy(ps->last);
+        for (auto& u : ps->uses) {
+            (void)hipEventSynchronize(u.second);
+            (void)hipEventDestroy(u.second);
         }
         for (auto& s : ps->slots) {
             if (s.done) {
@@ -512,8 +529,7 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
     hipStream_t st = static_cast<hipStream_t>(stream);
     MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
                                    ps->device, st));
-    MEZO_HIP(hipEventRecord(ps->last, st));
-    return MEZO_OK;
+    return mark_use(ps, st);
 }
 
 namespace {

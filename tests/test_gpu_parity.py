@@ -516,3 +516,23 @@ def test_perturb_multi_nf4_portable_bit_exact(mz, orc):
     assert np.array_equal(t.codes.cpu().numpy(), nf4.pack(c))
     assert np.array_equal(t.absmax.cpu().numpy().view(np.uint32), am.view(np.uint32))
     ps.close()
+
+
+def test_destroy_waits_for_work_on_every_stream(mz):
+    """A paramset used on two streams: destroy returns only after the long
+    replay on the first stream has finished, not just the short perturb
+    enqueued last on the second."""
+    import torch
+    w = synth.WORKLOADS["opt125m"]
+    hosts = [synth.theta0_tensor((1 << 24,), synth.F32, 0, 1)]
+    devs, ps = make_set(mz, hosts)
+    a, b = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    log = [(synth.seeds(8, 4, step=t), synth.grads_int8(32, seed=t), 1e-6) for t in range(40)]
+    with torch.cuda.stream(a):
+        ps.replay(log)                      # 1280 records: tens of milliseconds
+    with torch.cuda.stream(b):
+        ps.perturb((1, 2, 3), w.eps)        # short, enqueued last
+    ps.close()
+    assert a.query() and b.query()
+    torch.cuda.synchronize()
