@@ -303,6 +303,7 @@ def main():
         out["issue_cycles_isolated"] = {k: round(v, 3) for k, v in issue_costs().items()}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, recs, calls, log, args.cpu_seconds)
+        out["gpu_over_cpu"] = value / out["cpu_baseline"]["value"]
     print(json.dumps(out))
 
 
@@ -464,17 +465,27 @@ def cpu_baseline(w, recs, calls, log, target_s):
         oracle.replay(th, 0, log)
         return time.perf_counter() - t0
 
-    n = 1 << 10
-    dt = run(n)
-    while dt < 0.5 and n < w.numel:
-        n *= 4
+    def sized(seconds):
+        n = 1 << 10
         dt = run(n)
-    n_full = int(min(max(n * target_s / max(dt, 1e-6), n), w.numel))
-    dt = run(n_full)
-    return {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,
-            "kind": "oracle",
-            "sample": f"first {n_full} elements of tensor 0 through the same step "
-                      f"({seeds_per_elem} param-seeds per element), {dt:.1f} s"}
+        while dt < 0.5 and n < w.numel:
+            n *= 4
+            dt = run(n)
+        n_full = int(min(max(n * seconds / max(dt, 1e-6), n), w.numel))
+        return n_full, run(n_full)
+
+    n_full, dt = sized(target_s)
+    out = {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,
+           "kind": "oracle",
+           "sample": f"first {n_full} elements of tensor 0 through the same step "
+                     f"({seeds_per_elem} param-seeds per element), {dt:.1f} s"}
+    # the same oracle on one thread (a shorter sample), for the per-core rate
+    oracle.set_threads(1)
+    n1, dt1 = sized(max(1.0, target_s / 4))
+    oracle.set_threads(n_threads)
+    out["value_1_thread"] = n1 * seeds_per_elem / dt1
+    out["sample_1_thread"] = f"first {n1} elements of tensor 0, {dt1:.1f} s"
+    return out
 
 
 if __name__ == "__main__":
