@@ -80,8 +80,8 @@ T_REPLAY = 4
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=100)
-    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--steps", type=int, default=400)
+    p.add_argument("--warmup", type=int, default=100)
     p.add_argument("--workload", default="opt125m")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-ops", action="store_true",
