@@ -81,7 +81,8 @@ extern "C" {
 #define MEZO_EOVERLAP -3  /* two tensors of a paramset share memory          */
 #define MEZO_EORDER   -4  /* seeds of one update not strictly ascending      */
 #define MEZO_ERANGE   -5  /* q = -128, NaN gradient, non-finite lr/scale,
-                             codec parameters out of range                   */
+                             codec parameters out of range, more than 2^32-1
+                             perturbation terms in one call                  */
 #define MEZO_EHIP     -6  /* HIP runtime failure (see mezo_last_error)       */
 
 /* ---- storage types and codecs ---------------------------------------- */

@@ -219,6 +219,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
                    mezo_paramset* src = nullptr)
 {
     if (recs.empty() && !src) return MEZO_OK;
+    if (recs.size() > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
     int rc = ensure_device(ps);
     if (rc) return rc;
     if (src && src != ps) {
