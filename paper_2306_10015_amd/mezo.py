@@ -222,8 +222,10 @@ def nf4_quantize(values, out: NF4Tensor | None = None, stream=None) -> NF4Tensor
     out = NF4Tensor.empty(n, values.device) if out is None else out
     if out.numel() != n or not values.is_contiguous():
         raise ValueError("size mismatch or non-contiguous values")
-    _check(lib.mezo_nf4_quantize(values.data_ptr(), _dtype_code(values), n, out.codes.data_ptr(),
-                                 out.absmax.data_ptr(), _stream_ptr(stream)), "mezo_nf4_quantize")
+    import torch
+    with torch.cuda.device(values.device):
+        _check(lib.mezo_nf4_quantize(values.data_ptr(), _dtype_code(values), n, out.codes.data_ptr(),
+                                     out.absmax.data_ptr(), _stream_ptr(stream)), "mezo_nf4_quantize")
     return out
 
 
@@ -234,8 +236,9 @@ def nf4_dequantize(t: NF4Tensor, dtype=None, out=None, stream=None):
         out = torch.empty(t.numel(), dtype=dtype or torch.float32, device=t.device)
     if out.numel() != t.numel() or not out.is_contiguous():
         raise ValueError("size mismatch or non-contiguous out")
-    _check(lib.mezo_nf4_dequantize(t.codes.data_ptr(), t.absmax.data_ptr(), t.numel(), out.data_ptr(),
-                                   _dtype_code(out), _stream_ptr(stream)), "mezo_nf4_dequantize")
+    with torch.cuda.device(t.device):
+        _check(lib.mezo_nf4_dequantize(t.codes.data_ptr(), t.absmax.data_ptr(), t.numel(), out.data_ptr(),
+                                       _dtype_code(out), _stream_ptr(stream)), "mezo_nf4_dequantize")
     return out
 
 
@@ -258,6 +261,17 @@ class ParamSet:
     def __init__(self, tensors: Sequence, tensor_ids: Iterable[int] | None = None,
                  gaussian: int = GAUSS_FAST):
         self.tensors = list(tensors)
+        devices = set()
+        for t in self.tensors:
+            devices.add(t.device)
+            if isinstance(t, NF4Tensor):
+                devices.add(t.absmax.device)
+        if len(devices) > 1:
+            raise ValueError(f"all tensors of a paramset must live on one device, got {sorted(map(str, devices))}")
+        #: the device every call of this paramset runs on (made current for the call)
+        self.device = devices.pop() if devices else None
+        import torch
+        self._switch = torch.cuda.device_count() > 1
         ids = list(range(len(self.tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
         if len(ids) != len(self.tensors):
             raise ValueError("one tensor_id per tensor")
@@ -276,6 +290,14 @@ class ParamSet:
         """GAUSS_FAST (hardware transcendentals) or GAUSS_PORTABLE (binary32
         operations only: bit-identical on any IEEE device)."""
         _check(lib.mezo_paramset_set_gaussian(self._h, int(gaussian)), "mezo_paramset_set_gaussian")
+
+    def _on_device(self):
+        """Make the paramset's device current for a call (a stream or pointer
+        of another device would not be valid for its kernels); with a single
+        visible device there is nothing to switch."""
+        import contextlib
+        import torch
+        return torch.cuda.device(self.device) if self._switch else contextlib.nullcontext()
 
     @property
     def handle(self) -> ctypes.c_void_p:
@@ -298,8 +320,9 @@ class ParamSet:
 
     def perturb(self, seed, scale: float, stream=None) -> None:
         """PerturbParameters: theta += scale * z(seed)."""
-        _check(lib.mezo_perturb(self._h, _seed(seed), float(scale), _stream_ptr(stream)),
-               "mezo_perturb")
+        with self._on_device():
+            _check(lib.mezo_perturb(self._h, _seed(seed), float(scale), _stream_ptr(stream)),
+                   "mezo_perturb")
 
     def perturb_multi(self, seeds, scales, stream=None) -> None:
         """Perturbs in sequence in one pass: theta += scales[i] * z(seeds[i]),
@@ -308,8 +331,9 @@ class ParamSet:
         sc = np.ascontiguousarray(scales, dtype=np.float32)
         if sa.size != sc.size:
             raise ValueError("seeds and scales differ in length")
-        _check(lib.mezo_perturb_multi(self._h, sa.ctypes.data, sc.ctypes.data, sa.size, _stream_ptr(stream)),
-               "mezo_perturb_multi")
+        with self._on_device():
+            _check(lib.mezo_perturb_multi(self._h, sa.ctypes.data, sc.ctypes.data, sa.size, _stream_ptr(stream)),
+                   "mezo_perturb_multi")
 
     def update_multi(self, seeds, q, lr: float, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
         """Apply loop of one iteration: theta -= lr * sum_k deq(q_k) z(seed_k)."""
@@ -317,14 +341,16 @@ class ParamSet:
         qa = np.ascontiguousarray(q, dtype=np.int8)
         if sa.size != qa.size:
             raise ValueError("seeds and q differ in length")
-        _check(lib.mezo_update_multi(self._h, sa.ctypes.data, qa.ctypes.data, sa.size,
-                                     ctypes.byref(codec_), float(lr), _stream_ptr(stream)),
-               "mezo_update_multi")
+        with self._on_device():
+            _check(lib.mezo_update_multi(self._h, sa.ctypes.data, qa.ctypes.data, sa.size,
+                                         ctypes.byref(codec_), float(lr), _stream_ptr(stream)),
+                   "mezo_update_multi")
 
     def perturb_from(self, src: "ParamSet", seed, scale: float, stream=None) -> None:
         """theta = theta_src + scale * z(seed), src unchanged (out of place)."""
-        _check(lib.mezo_perturb_from(self._h, src.handle, _seed(seed), float(scale),
-                                     _stream_ptr(stream)), "mezo_perturb_from")
+        with self._on_device():
+            _check(lib.mezo_perturb_from(self._h, src.handle, _seed(seed), float(scale),
+                                         _stream_ptr(stream)), "mezo_perturb_from")
 
     def update_multi_from(self, src: "ParamSet", seeds, q, lr: float,
                           codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
@@ -334,16 +360,18 @@ class ParamSet:
         qa = np.ascontiguousarray(q, dtype=np.int8)
         if sa.size != qa.size:
             raise ValueError("seeds and q differ in length")
-        _check(lib.mezo_update_multi_from(self._h, src.handle, sa.ctypes.data, qa.ctypes.data,
-                                          sa.size, ctypes.byref(codec_), float(lr),
-                                          _stream_ptr(stream)), "mezo_update_multi_from")
+        with self._on_device():
+            _check(lib.mezo_update_multi_from(self._h, src.handle, sa.ctypes.data, qa.ctypes.data,
+                                              sa.size, ctypes.byref(codec_), float(lr),
+                                              _stream_ptr(stream)), "mezo_update_multi_from")
 
     def checksum_into(self, out, stream=None) -> None:
         """Enqueue the 64-bit checksum of every tensor's bits into `out`, a
         device tensor of 8 bytes (ChecksumMatch, Algorithm 1)."""
         if out.numel() * out.element_size() != 8 or not out.is_cuda:
             raise ValueError("out must be an 8-byte device tensor")
-        _check(lib.mezo_checksum(self._h, out.data_ptr(), _stream_ptr(stream)), "mezo_checksum")
+        with self._on_device():
+            _check(lib.mezo_checksum(self._h, out.data_ptr(), _stream_ptr(stream)), "mezo_checksum")
 
     def checksum(self, stream=None) -> int:
         """The checksum as a Python int (synchronises with the stream)."""
@@ -363,8 +391,9 @@ class ParamSet:
                 raise ValueError(f"step {i}: seeds and q differ in length")
             keep.append((sa, qa))
             arr[i] = Step(sa.ctypes.data, qa.ctypes.data, sa.size, float(lr))
-        _check(lib.mezo_replay(self._h, arr, len(steps), ctypes.byref(codec_),
-                               _stream_ptr(stream)), "mezo_replay")
+        with self._on_device():
+            _check(lib.mezo_replay(self._h, arr, len(steps), ctypes.byref(codec_),
+                                   _stream_ptr(stream)), "mezo_replay")
 
 
 def step_lr(eta: float, n_grads: int, sqrt_scaling: bool = False) -> float:
