@@ -87,7 +87,7 @@ def main():
     lines = [f"# {a.name}", ""]
     summary = {"kernel_source_sha256": source_hash(), "alg_bytes_per_dispatch": alg}
     if a.commands:
-        lines += ["Commands (run from the repository root on the GPU box):", "", "```"]
+        lines += ["Commands (run from the repository root on an MI355X machine):", "", "```"]
         lines += [l.rstrip() for l in open(a.commands) if l.strip()]
         lines += ["```", ""]
     if a.trace:
