@@ -170,8 +170,38 @@ __device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint
 // from 2 atanh((m-1)/(m+1)) after an exact reduction of u1 to m 2^e with m in
 // [sqrt(1/2), sqrt(2)); sin and cos of 2 pi u2 from the eighth of a turn that
 // u2 falls in and Taylor polynomials on [0, pi/4] (coefficients 1/k! rounded
-// to binary32). Division and sqrt here are the compiler's correctly rounded
-// sequences (-fhip-fp32-correctly-rounded-divide-sqrt), not v_rcp / v_sqrt.
+// to binary32). Division and sqrt are correctly rounded (below), as IEEE
+// 754 requires of / and sqrt.
+
+// n / d correctly rounded for normal n, d with a normal quotient and no
+// overflow in the steps (here |n| < 0.5, d in [1.7, 2.5]): the reciprocal from
+// v_rcp_f32 refined once, then two residual corrections of the quotient —
+// the general sequence without its operand scaling and special-value fix-up,
+// which only act outside that range.
+__device__ __forceinline__ float div_rn_normal(float n, float d)
+{
+    float y = __builtin_amdgcn_rcpf(d);
+    y = __builtin_fmaf(__builtin_fmaf(-d, y, 1.0f), y, y);
+    float q = n * y;
+    q = __builtin_fmaf(__builtin_fmaf(-d, q, n), y, q);
+    return __builtin_fmaf(__builtin_fmaf(-d, q, n), y, q);
+}
+
+// sqrt(x) correctly rounded for x = 0 and normal x >= 2^-96 (here x = 0 or
+// x in [2^-23, 34]): v_sqrt_f32, then the neighbour below or above replaces
+// it when the residual shows it is nearer. At x = 0 the neighbour below is a
+// NaN and the one above squares to 0, so 0 stays.
+__device__ __forceinline__ float sqrt_rn_normal(float x)
+{
+    const float s = __builtin_amdgcn_sqrtf(x);
+    const float lo = __uint_as_float(__float_as_uint(s) - 1u);
+    const float hi = __uint_as_float(__float_as_uint(s) + 1u);
+    float r = s;
+    if (__builtin_fmaf(-lo, s, x) <= 0.0f) r = lo;
+    if (__builtin_fmaf(-hi, s, x) > 0.0f) r = hi;
+    return r;
+}
+
 __device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t wb, float& zc, float& zs)
 {
     const uint32_t n1 = (wa >> 8) + 1u;                     // u1 = n1 2^-24, n1 >= 1
@@ -182,7 +212,7 @@ __device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t w
         e = e + 1;
     }
     const float f = m - 1.0f;                               // exact
-    const float s = f / (f + 2.0f);
+    const float s = div_rn_normal(f, f + 2.0f);
     const float s2 = s * s;
     float p = __builtin_fmaf(s2, 0x1.c71c72p-4f, 0x1.24924ap-3f);  // 1/9, 1/7
     p = __builtin_fmaf(s2, p, 0x1.99999ap-3f);              // 1/5
@@ -190,7 +220,7 @@ __device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t w
     p = __builtin_fmaf(s2, p, 1.0f);
     const float ln_m = (s + s) * p;
     const float ln_u1 = __builtin_fmaf(float(e - 24), 0x1.62e430p-1f, ln_m);  // + (e-24) ln 2
-    const float r = sqrtf(-2.0f * ln_u1);
+    const float r = sqrt_rn_normal(-2.0f * ln_u1);
 
     const uint32_t t = wb >> 8;                             // u2 = t 2^-24
     const float v = __builtin_ldexpf(float(t), -21);        // 8 u2, exact, [0, 8)
