@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.orc_round_f32.restype = f32
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_uint16
+        L.orc_signed_log_qmax.argtypes = [f32]
+        L.orc_signed_log_qmax.restype = i32
         L.orc_quantize.argtypes = [vp, vp, u32, i32, f32, f32]
         L.orc_quantize.restype = i32
         L.orc_dequantize.argtypes = [vp, vp, u32, i32, f32, f32]
@@ -219,6 +221,11 @@ def round_f32(x: float) -> float:
 
 def round_bf16(x: float) -> int:
     return int(lib().orc_round_bf16(float(x)))
+
+
+def signed_log_qmax(alpha: float) -> int:
+    """Largest code magnitude of the signed-log code for slope alpha."""
+    return int(lib().orc_signed_log_qmax(float(alpha)))
 
 
 def quantize(g, kind: int = LINEAR, scale: float = 1.0 / 127.0, alpha: float = LOG2_ALPHA) -> np.ndarray:

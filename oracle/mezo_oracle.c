@@ -205,17 +205,29 @@ static void store_theta(void* theta, int dtype, uint64_t i, double v)
 /* never produced and rejected on input; rounding ties go to even.          */
 /* ------------------------------------------------------------------------ */
 
-/* The signed-log code must decode every q to a finite fp32 value: the largest
- * code, 127, decodes to exp(127/alpha) - 1, which needs alpha >= ~1.4314. The
- * default alpha = 1/ln 2 (a base-2 log) puts the clip at 127 just inside the
- * fp32 range: the reading taken of the paper's clip at +-127. */
+/* Largest code magnitude of the signed-log code: the paper's clip at 127, or
+ * less where a larger code would decode past fp32, i.e. fl32(exp(k/alpha) - 1)
+ * would be infinite (alpha < ~1.4314; the natural log, alpha = 1: 88). The
+ * default alpha = 1/ln 2 (a base-2 log) puts 127 just inside fp32. */
+int orc_signed_log_qmax(float alpha)
+{
+    int k = 127;
+    while (k > 0 && !isfinite((float)expm1((double)k / (double)alpha))) --k;
+    return k;
+}
+
 static int codec_ok(int kind, float scale, float alpha)
 {
     if (kind == ORC_CODEC_LINEAR) return isfinite(scale) && scale > 0.0f;
     if (kind == ORC_CODEC_SIGNED_LOG)
-        return isfinite(alpha) && alpha > 0.0f &&
-               isfinite((float)expm1(127.0 / (double)alpha));
+        return isfinite(alpha) && alpha > 0.0f && orc_signed_log_qmax(alpha) >= 1;
     return 0;
+}
+
+/* Largest |q| the codec produces and accepts. */
+static int code_max(int kind, float alpha)
+{
+    return kind == ORC_CODEC_SIGNED_LOG ? orc_signed_log_qmax(alpha) : 127;
 }
 
 int orc_quantize(const float* g, int8_t* q, uint32_t n, int kind, float scale, float alpha)
@@ -223,6 +235,7 @@ int orc_quantize(const float* g, int8_t* q, uint32_t n, int kind, float scale, f
     if (!codec_ok(kind, scale, alpha)) return -2;
     for (uint32_t i = 0; i < n; ++i)
         if (isnan(g[i])) return -2;
+    const double qmax = (double)code_max(kind, alpha);
     for (uint32_t i = 0; i < n; ++i) {
         double r;
         if (kind == ORC_CODEC_LINEAR) {
@@ -232,8 +245,8 @@ int orc_quantize(const float* g, int8_t* q, uint32_t n, int kind, float scale, f
             double mag = rint((double)alpha * log1p(fabs((double)g[i])));
             r = signbit(g[i]) ? -mag : mag;
         }
-        if (r > 127.0) r = 127.0;
-        if (r < -127.0) r = -127.0;
+        if (r > qmax) r = qmax;
+        if (r < -qmax) r = -qmax;
         q[i] = (int8_t)r;
     }
     return 0;
@@ -249,8 +262,9 @@ static float dequant_one(int8_t q, int kind, float scale, float alpha)
 int orc_dequantize(const int8_t* q, float* g, uint32_t n, int kind, float scale, float alpha)
 {
     if (!codec_ok(kind, scale, alpha)) return -2;
+    const int qmax = code_max(kind, alpha);
     for (uint32_t i = 0; i < n; ++i)
-        if (q[i] == -128) return -2;
+        if (q[i] == -128 || q[i] > qmax || q[i] < -qmax) return -2;
     for (uint32_t i = 0; i < n; ++i) g[i] = dequant_one(q[i], kind, scale, alpha);
     return 0;
 }

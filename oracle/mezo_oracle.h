@@ -78,12 +78,16 @@ int orc_generate(orc_seed_t s, uint32_t tensor_id, uint64_t first, uint64_t coun
 float    orc_round_f32(double x);
 uint16_t orc_round_bf16(double x);
 
-/* One-byte codec. LINEAR: q = clamp(rne(g/scale)), g~ = fl32(q*scale).
- * SIGNED_LOG: q = sign(g)*min(127, rne(alpha*ln(1+|g|))),
+/* One-byte codec. LINEAR: q = clamp(rne(g/scale), -127, 127),
+ *             g~ = fl32(q*scale).
+ * SIGNED_LOG: q = sign(g)*min(qmax, rne(alpha*ln(1+|g|))),
  *             g~ = fl32(sign(q)*(exp(|q|/alpha)-1)); alpha = 1/ln 2 is a
- *             base-2 log. NaN g, q = -128, non-positive or non-finite scale,
- *             and an alpha for which code 127 decodes past fp32 (alpha <
- *             ~1.4314) are rejected with -2. */
+ *             base-2 log, alpha = 1 the natural one. qmax is 127, or the
+ *             largest k whose decoding fl32(exp(k/alpha) - 1) is finite
+ *             when that is smaller (alpha = 1: 88).
+ * Rejected with -2: NaN g, q = -128 or |q| > qmax, a non-positive or
+ * non-finite scale or alpha, an alpha with qmax = 0. */
+int orc_signed_log_qmax(float alpha);
 int orc_quantize(const float* g, int8_t* q, uint32_t n, int kind, float scale, float alpha);
 int orc_dequantize(const int8_t* q, float* g, uint32_t n, int kind, float scale, float alpha);
 

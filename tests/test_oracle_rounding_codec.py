@@ -119,11 +119,44 @@ def test_signed_log_closed_form(orc):
                         alpha=10.0)[0] == 10
 
 
-def test_signed_log_rejects_alpha_that_overflows_fp32(orc):
-    """alpha = 1 (natural log) would decode codes >= 89 to infinity."""
-    with pytest.raises(oracle.OracleError):
-        orc.dequantize(np.array([1], dtype=np.int8), oracle.SIGNED_LOG, alpha=1.0)
-    orc.dequantize(np.array([127], dtype=np.int8), oracle.SIGNED_LOG, alpha=1.44)
+def qmax_brute(alpha):
+    """The largest k <= 127 with fl32(expm1(k / alpha)) finite, from numpy's
+    float32 conversion."""
+    best = 0
+    for k in range(1, 128):
+        with np.errstate(over="ignore"):
+            if np.isfinite(np.float32(np.expm1(k / np.float64(np.float32(alpha))))):
+                best = k
+    return best
+
+
+@pytest.mark.parametrize("alpha", [1.0, 0.5, 1.43, 1.4314, 1.44, oracle.LOG2_ALPHA, 0.02])
+def test_signed_log_clip_where_fp32_ends(orc, alpha):
+    """The code's range is +-127 or, below alpha ~1.4314, the largest code
+    that still decodes to a finite fp32 (the natural log, alpha = 1: 88)."""
+    qmax = orc.signed_log_qmax(alpha)
+    assert qmax == qmax_brute(alpha)
+    if alpha == 1.0:
+        assert qmax == 88
+    if alpha >= 1.44:
+        assert qmax == 127
+    codes = np.arange(-qmax, qmax + 1, dtype=np.int8)
+    g = orc.dequantize(codes, oracle.SIGNED_LOG, alpha=alpha)
+    assert np.all(np.isfinite(g)) and np.all(np.diff(g) > 0)
+    assert np.array_equal(orc.quantize(g, oracle.SIGNED_LOG, alpha=alpha), codes)
+    big = np.array([3.4e38, -np.inf, 1e30], dtype=np.float32)
+    q = orc.quantize(big, oracle.SIGNED_LOG, alpha=alpha)
+    assert q[0] == qmax and q[1] == -qmax
+    if qmax < 127:
+        with pytest.raises(oracle.OracleError):
+            orc.dequantize(np.array([qmax + 1], dtype=np.int8), oracle.SIGNED_LOG, alpha=alpha)
+
+
+def test_signed_log_natural_log_closed_form(orc):
+    """alpha = 1: g = e^k - 1 codes to k (the literal natural-log reading)."""
+    ks = np.arange(0, 60)
+    g = np.expm1(ks.astype(np.float64)).astype(np.float32)
+    assert np.array_equal(orc.quantize(g, oracle.SIGNED_LOG, alpha=1.0), ks.astype(np.int8))
 
 
 def test_codec_rejects_bad_input(orc):
@@ -135,6 +168,8 @@ def test_codec_rejects_bad_input(orc):
         orc.quantize(np.array([1.0], dtype=np.float32), oracle.LINEAR, 0.0)
     with pytest.raises(oracle.OracleError):
         orc.quantize(np.array([1.0], dtype=np.float32), oracle.SIGNED_LOG, alpha=-1.0)
+    with pytest.raises(oracle.OracleError):   # even code 1 would decode past fp32
+        orc.quantize(np.array([1.0], dtype=np.float32), oracle.SIGNED_LOG, alpha=1e-3)
 
 
 def test_coefficient_sign_and_value(orc):
