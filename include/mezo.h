@@ -98,12 +98,15 @@ extern "C" {
 
 #define MEZO_CODEC_LINEAR     0u  /* q = clamp(rne(g / scale), -127, 127);
                                      g~ = fl32(q * scale)                     */
-#define MEZO_CODEC_SIGNED_LOG 1u  /* q = sign(g) min(127, rne(alpha ln(1+|g|)));
+#define MEZO_CODEC_SIGNED_LOG 1u  /* q = sign(g) min(qmax, rne(alpha ln(1+|g|)));
                                      g~ = fl32(sign(q) (exp(|q|/alpha) - 1)).
-                                     alpha = 1/ln 2 (a base-2 log) puts code
-                                     127 just inside fp32; an alpha for which
-                                     code 127 would decode past fp32 (alpha <
-                                     ~1.4314) is MEZO_ERANGE.                 */
+                                     qmax = 127, or the largest k whose
+                                     decoding is a finite fp32 when that is
+                                     smaller: alpha = 1/ln 2 (a base-2 log)
+                                     puts 127 just inside fp32, the natural
+                                     log (alpha = 1) stops at 88. Codes with
+                                     |q| > qmax, and an alpha with qmax = 0,
+                                     are MEZO_ERANGE.                         */
 
 /* How z is computed (a property of a training run: every machine must use
  * the same one).

@@ -36,19 +36,27 @@ int hip_fail(hipError_t e, const char* where)
 
 // ---- codec (Section 3: the projected gradient in one byte) -------------------
 
+// Largest code magnitude: 127 (Section 3's clip), or for the signed log the
+// largest k whose decoding fl32(exp(k / alpha) - 1) is finite when that is
+// smaller (alpha < ~1.4314; the natural log, alpha = 1: 88).
+int code_max(const mezo_codec_t& c)
+{
+    if (c.kind != MEZO_CODEC_SIGNED_LOG) return 127;
+    int k = 127;
+    while (k > 0 && !std::isfinite(static_cast<float>(std::expm1(double(k) / double(c.alpha))))) --k;
+    return k;
+}
+
 bool codec_valid(const mezo_codec_t* c)
 {
     if (!c) return false;
     if (c->kind == MEZO_CODEC_LINEAR) return std::isfinite(c->scale) && c->scale > 0.0f;
-    if (c->kind == MEZO_CODEC_SIGNED_LOG) {
-        if (!(std::isfinite(c->alpha) && c->alpha > 0.0f)) return false;
-        // the largest code must decode to a finite fp32 value
-        return std::isfinite(static_cast<float>(std::expm1(127.0 / double(c->alpha))));
-    }
+    if (c->kind == MEZO_CODEC_SIGNED_LOG)
+        return std::isfinite(c->alpha) && c->alpha > 0.0f && code_max(*c) >= 1;
     return false;
 }
 
-int8_t encode(float g, const mezo_codec_t& c)
+int8_t encode(float g, const mezo_codec_t& c, double qmax)
 {
     double r;
     if (c.kind == MEZO_CODEC_LINEAR) {
@@ -57,7 +65,7 @@ int8_t encode(float g, const mezo_codec_t& c)
         const double mag = std::rint(double(c.alpha) * std::log1p(std::fabs(double(g))));
         r = std::signbit(g) ? -mag : mag;
     }
-    r = std::min(127.0, std::max(-127.0, r));
+    r = std::min(qmax, std::max(-qmax, r));
     return static_cast<int8_t>(r);
 }
 
@@ -103,8 +111,9 @@ int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mez
     if (!codec_valid(codec) || !std::isfinite(lr)) return MEZO_ERANGE;
     if (K == 0) return MEZO_OK;
     if (!seeds || !q) return MEZO_EINVAL;
+    const int qmax = code_max(*codec);
     for (uint32_t k = 0; k < K; ++k)
-        if (q[k] == -128) return MEZO_ERANGE;
+        if (q[k] > qmax || q[k] < -qmax) return MEZO_ERANGE;  // -128 included
     for (uint32_t k = 1; k < K; ++k)
         if (!seed_less(seeds[k - 1], seeds[k])) return MEZO_EORDER;
     const size_t first = out.size();
@@ -577,7 +586,8 @@ int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t*
     if (!g || !q) return MEZO_EINVAL;
     for (uint32_t i = 0; i < n; ++i)
         if (std::isnan(g[i])) return MEZO_ERANGE;
-    for (uint32_t i = 0; i < n; ++i) q[i] = encode(g[i], *codec);
+    const double qmax = code_max(*codec);
+    for (uint32_t i = 0; i < n; ++i) q[i] = encode(g[i], *codec, qmax);
     return MEZO_OK;
 }
 
@@ -587,8 +597,9 @@ int mezo_dequantize(const int8_t* q, float* g, uint32_t n, const mezo_codec_t* c
     if (!codec_valid(codec)) return MEZO_ERANGE;
     if (n == 0) return MEZO_OK;
     if (!g || !q) return MEZO_EINVAL;
+    const int qmax = code_max(*codec);
     for (uint32_t i = 0; i < n; ++i)
-        if (q[i] == -128) return MEZO_ERANGE;
+        if (q[i] > qmax || q[i] < -qmax) return MEZO_ERANGE;  // -128 included
     for (uint32_t i = 0; i < n; ++i) g[i] = decode(q[i], *codec);
     return MEZO_OK;
 }

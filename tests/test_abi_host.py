@@ -68,7 +68,8 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
 # ---- codec parity with the oracle -----------------------------------------
 
 CODECS = [(mezo.LINEAR, 1 / 127, 1.0), (mezo.LINEAR, 0.25, 1.0), (mezo.LINEAR, 3e-4, 1.0),
-          (mezo.SIGNED_LOG, 1.0, mezo.LOG2_ALPHA), (mezo.SIGNED_LOG, 1.0, 3.0),
+          (mezo.SIGNED_LOG, 1.0, mezo.LOG2_ALPHA), (mezo.SIGNED_LOG, 1.0, 3.0), (mezo.SIGNED_LOG, 1.0, 1.0),
+          (mezo.SIGNED_LOG, 1.0, 0.3),
           (mezo.SIGNED_LOG, 1.0, 17.5)]
 
 
@@ -87,7 +88,8 @@ def test_quantize_matches_oracle_bit_exact(kind, scale, alpha):
 
 @pytest.mark.parametrize("kind,scale,alpha", CODECS)
 def test_dequantize_matches_oracle_bit_exact(kind, scale, alpha):
-    q = np.arange(-127, 128, dtype=np.int8)
+    qmax = oracle.signed_log_qmax(alpha) if kind == mezo.SIGNED_LOG else 127
+    q = np.arange(-qmax, qmax + 1, dtype=np.int8)
     got = mezo.dequantize(q, mezo.codec(kind, scale, alpha))
     want = oracle.dequantize(q, kind, scale, alpha)
     assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
@@ -101,11 +103,17 @@ def test_codec_errors():
         mezo.dequantize([-128])
     assert e.value.code == mezo.ERANGE
     for bad in (mezo.codec(mezo.LINEAR, 0.0), mezo.codec(mezo.LINEAR, float("inf")),
-                mezo.codec(mezo.SIGNED_LOG, 1.0, 1.0), mezo.codec(7, 1.0, 1.0)):
+                mezo.codec(mezo.SIGNED_LOG, 1.0, 1e-3), mezo.codec(7, 1.0, 1.0)):
         with pytest.raises(mezo.MezoError) as e:
             mezo.quantize_projgrad([1.0], bad)
         assert e.value.code == mezo.ERANGE
     assert mezo.quantize_projgrad(np.zeros(0, dtype=np.float32)).size == 0
+    # the natural log's codes stop at 88: larger received codes are refused
+    nat = mezo.codec(mezo.SIGNED_LOG, 1.0, 1.0)
+    with pytest.raises(mezo.MezoError) as e:
+        mezo.dequantize([89], nat)
+    assert e.value.code == mezo.ERANGE
+    assert mezo.quantize_projgrad([3.4e38], nat)[0] == 88
 
 
 # ---- argument checks (no device is touched) -------------------------------

@@ -132,15 +132,17 @@ def test_update_multi_tiny(mz, orc, dtype, K):
     print(f"{dtype} update K={K}: {s}")
 
 
-def test_update_signed_log_codec(mz, orc):
+@pytest.mark.parametrize("alpha", [oracle.LOG2_ALPHA, 1.0])
+def test_update_signed_log_codec(mz, orc, alpha):
+    """The signed-log code with a base-2 log (default) and the natural log."""
     hosts = tiny_hosts(synth.F32)[:1]
     devs, ps = make_set(mz, hosts)
     seeds = synth.seeds(4, 2, step=11)
     q = synth.grads_int8(8, "normal40", seed=4) // 8
-    cd = mz.codec(mz.SIGNED_LOG, 1.0, mz.LOG2_ALPHA)
+    cd = mz.codec(mz.SIGNED_LOG, 1.0, alpha)
     ps.update_multi(seeds, q, 1e-4, cd)
     sync()
-    ref = orc.update(hosts[0].copy(), 0, seeds, q, 1e-4, oracle.SIGNED_LOG, 1.0, oracle.LOG2_ALPHA)
+    ref = orc.update(hosts[0].copy(), 0, seeds, q, 1e-4, oracle.SIGNED_LOG, 1.0, alpha)
     assert_theta_close(to_host(devs[0]), ref, "signed-log update")
 
 
