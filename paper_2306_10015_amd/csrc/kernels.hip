@@ -129,7 +129,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
         for (int j = 0; j < 4; ++j) acc[g][j] = 0.0f;
     }
 
-    for (uint32_t r = 0; r < a.n_rec; ++r) {
+    const auto accumulate = [&](uint32_t r) {
         const SeedRec& rec = rec_at<kInline>(a, r);
         const SeedUniform u = seed_uniform(rec, d.tensor_id);
         const float c = rec.coef;
@@ -139,7 +139,12 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
             philox_words(u, pre[g], w0, w1, w2, w3);
             accumulate4<kPortable>(c, w0, w1, w2, w3, acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
         }
-        if (rec.last) {
+    };
+    // the last record ends the call's last step: peeled off the loop, it
+    // needs no reset of acc afterwards
+    for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
+        accumulate(r);
+        if (rec_at<kInline>(a, r).last) {
 #pragma unroll
             for (int g = 0; g < kGroups; ++g)
 #pragma unroll
@@ -148,6 +153,13 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
                     acc[g][j] = 0.0f;
                 }
         }
+    }
+    if (a.n_rec > 0) {
+        accumulate(a.n_rec - 1);
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) th[g][j] = th[g][j] + acc[g][j];
     }
 
 #pragma unroll
@@ -182,7 +194,7 @@ __device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDes
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[g][j] = 0.0f;
     }
-    for (uint32_t r = 0; r < a.n_rec; ++r) {
+    const auto accumulate = [&](uint32_t r) {
         const SeedRec& rec = rec_at<kInline>(a, r);
         const SeedUniform u = seed_uniform(rec, d.tensor_id);
         const float c = rec.coef;
@@ -195,16 +207,29 @@ __device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDes
                 accumulate4<kPortable>(c, w0, w1, w2, w3, acc[g][4 * h + 0], acc[g][4 * h + 1],
                                        acc[g][4 * h + 2], acc[g][4 * h + 3]);
             }
-        if (rec.last) {
+    };
+    const auto step_end = [&]() {
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                th[g][j] = pack_bf16(bf16_lo(th[g][j]) + acc[g][2 * j], bf16_hi(th[g][j]) + acc[g][2 * j + 1]);
+    };
+    // the last record ends the call's last step: peeled off the loop, it
+    // needs no reset of acc afterwards
+    for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
+        accumulate(r);
+        if (rec_at<kInline>(a, r).last) {
+            step_end();
 #pragma unroll
             for (int g = 0; g < kGroups; ++g)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    th[g][j] = pack_bf16(bf16_lo(th[g][j]) + acc[g][2 * j], bf16_hi(th[g][j]) + acc[g][2 * j + 1]);
-                    acc[g][2 * j] = 0.0f;
-                    acc[g][2 * j + 1] = 0.0f;
-                }
+                for (int j = 0; j < 8; ++j) acc[g][j] = 0.0f;
         }
+    }
+    if (a.n_rec > 0) {
+        accumulate(a.n_rec - 1);
+        step_end();
     }
 }
 
