@@ -41,8 +41,8 @@
  * subnormals are kept.
  *
  * Errors. Every int-returning call returns MEZO_OK (0) or a negative MEZO_E*
- * code. All argument checks run before anything is enqueued, so a failed call
- * leaves the parameters untouched. Device faults surface at the caller's next
+ * code; no C++ exception leaves the library. All argument checks run before
+ * anything is enqueued, so a failed call leaves the parameters untouched. Device faults surface at the caller's next
  * synchronisation (HIP's convention). mezo_strerror() gives a description;
  * for MEZO_EHIP, mezo_last_error() gives the HIP runtime's message of the last
  * failure on the calling thread.
@@ -56,7 +56,11 @@
  * Threads and streams. Calls on one paramset may come from several host
  * threads (they serialise on a per-paramset lock). Work is ordered only by the
  * stream it is enqueued on: two calls on different streams that touch the
- * same parameters race unless the caller orders the streams.
+ * same parameters race unless the caller orders the streams. A paramset
+ * tracks the last 16 streams it was used on (destroy waits for their work);
+ * a call on a 17th stream first waits on the host for the work of the one
+ * used longest ago. mezo_paramset_destroy must not overlap other calls on
+ * the same paramset.
  */
 #ifndef MEZO_H
 #define MEZO_H
@@ -84,6 +88,8 @@ extern "C" {
                              codec parameters out of range, more than 2^32-1
                              perturbation terms in one call                  */
 #define MEZO_EHIP     -6  /* HIP runtime failure (see mezo_last_error)       */
+#define MEZO_ENOMEM   -7  /* host memory for the call's records or tables
+                             could not be allocated                          */
 
 /* ---- storage types and codecs ---------------------------------------- */
 #define MEZO_F32  0u      /* IEEE binary32                                    */
@@ -200,7 +206,9 @@ MEZO_API uint64_t mezo_paramset_numel(mezo_paramset_t ps);
  * default, or MEZO_GAUSS_PORTABLE; MEZO_EINVAL otherwise). For the *_from
  * calls the destination's setting applies. In portable mode the update is
  *   acc = fma(c_k, z_k, acc) (k ascending, binary32), theta' = round(theta + acc)
- * with the binary32 sum theta + acc rounded to the storage type. */
+ * with the binary32 sum theta + acc rounded to the storage type. A call
+ * made while the setting changes on another thread uses one setting
+ * throughout, the old or the new. */
 MEZO_API int mezo_paramset_set_gaussian(mezo_paramset_t ps, uint32_t gaussian);
 
 /* ---- the engine ------------------------------------------------------- */
@@ -324,8 +332,9 @@ MEZO_API int mezo_debug_box_muller(const uint32_t* words_dev, uint64_t n_blocks,
 
 MEZO_API const char* mezo_strerror(int code);
 
-/* The HIP runtime's message of the last MEZO_EHIP failure on this thread
- * ("" if none). */
+/* The message of the last MEZO_EHIP failure on this thread (the HIP
+ * runtime's), or of the last MEZO_ENOMEM or device-mismatch failure ("" if
+ * none). */
 MEZO_API const char* mezo_last_error(void);
 
 /* Library version, major*10000 + minor*100 + patch. */

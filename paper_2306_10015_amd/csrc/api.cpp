@@ -7,10 +7,13 @@
 #include <atomic>
 #include <cmath>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
+#include <exception>
+#include <memory>
 #include <mutex>
 #include <new>
-#include <string>
+#include <stdexcept>
 #include <vector>
 
 #include "../../include/mezo.h"
@@ -20,12 +23,41 @@
 
 namespace {
 
-thread_local std::string t_last_error;
+// The last failure's message on this thread (a fixed buffer: reporting an
+// error allocates nothing).
+thread_local char t_last_error[256];
+
+void set_error(const char* what, const char* detail = nullptr)
+{
+    std::snprintf(t_last_error, sizeof(t_last_error), detail ? "%s: %s" : "%s", what, detail);
+}
 
 int hip_fail(hipError_t e, const char* where)
 {
-    t_last_error = std::string(where) + ": " + hipGetErrorString(e);
+    set_error(where, hipGetErrorString(e));
     return MEZO_EHIP;
+}
+
+// Runs the body of a C entry point: no C++ exception crosses the C ABI. The
+// only ones the bodies can raise are host allocation failures (record lists,
+// tables) and, in principle, a failing mutex.
+template <class F>
+int guarded(const char* what, F&& body) noexcept
+{
+    try {
+        return body();
+    } catch (const std::bad_alloc&) {
+        set_error(what, "host allocation failed");
+    } catch (const std::length_error&) {
+        set_error(what, "host allocation failed");
+    } catch (const std::exception& e) {
+        set_error(what, e.what());
+        return MEZO_EINVAL;
+    } catch (...) {
+        set_error(what, "unexpected exception");
+        return MEZO_EINVAL;
+    }
+    return MEZO_ENOMEM;
 }
 
 #define MEZO_HIP(call)                                  \
@@ -144,8 +176,17 @@ struct mezo_paramset {
     uint32_t* d_tile_tensor[kTypes] = {};  // tensor index of every tile
     // One event per stream the paramset's kernels ran on, recorded after the
     // latest launch on that stream: destroy waits for all of them before it
-    // frees the tables (work on an earlier stream may still be running).
-    std::vector<std::pair<hipStream_t, hipEvent_t>> uses;
+    // frees the tables (work on an earlier stream may still be running). At
+    // most kUses streams are tracked; a further stream takes over the entry
+    // used longest ago, after waiting on the host for that entry's event.
+    struct Use {
+        hipStream_t stream;
+        hipEvent_t done;
+        uint64_t seq;  // when the entry was last recorded
+    };
+    static constexpr size_t kUses = 16;
+    std::vector<Use> uses;
+    uint64_t use_seq = 0;
 
     // Staging of record lists too long for the kernel arguments: a ring of
     // slots, each reused only after the launch that read it has completed.
@@ -162,7 +203,10 @@ struct mezo_paramset {
 
 namespace {
 
-bool fold_of(const mezo_paramset* ps) { return ps->gaussian.load() == MEZO_GAUSS_FAST; }
+// The Gaussian a call uses, read once per call: its records are made for it
+// (the fast kernels take the coefficient with sqrt(2 ln 2) folded in) and its
+// launches run it, even if mezo_paramset_set_gaussian runs meanwhile.
+bool portable_of(const mezo_paramset* ps) { return ps->gaussian.load() == MEZO_GAUSS_PORTABLE; }
 
 // Device resources are made on first use, on the device current then.
 int ensure_device(mezo_paramset* ps)
@@ -171,7 +215,7 @@ int ensure_device(mezo_paramset* ps)
     MEZO_HIP(hipGetDevice(&dev));
     if (ps->device >= 0) {
         if (dev != ps->device) {
-            t_last_error = "paramset used on a device other than the one it was first used on";
+            set_error("paramset used on a device other than the one it was first used on");
             return MEZO_EINVAL;
         }
         return MEZO_OK;
@@ -210,21 +254,32 @@ int ensure_device(mezo_paramset* ps)
 // Record that ps's tables are read by work enqueued so far on stream.
 int mark_use(mezo_paramset* ps, hipStream_t stream)
 {
+    mezo_paramset::Use* use = nullptr;
     for (auto& u : ps->uses)
-        if (u.first == stream) {
-            MEZO_HIP(hipEventRecord(u.second, stream));
-            return MEZO_OK;
-        }
-    hipEvent_t ev = nullptr;
-    MEZO_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
-    ps->uses.emplace_back(stream, ev);
-    MEZO_HIP(hipEventRecord(ev, stream));
+        if (u.stream == stream) use = &u;
+    if (!use && ps->uses.size() >= mezo_paramset::kUses) {
+        use = &*std::min_element(ps->uses.begin(), ps->uses.end(),
+                                 [](const mezo_paramset::Use& a, const mezo_paramset::Use& b) {
+                                     return a.seq < b.seq;
+                                 });
+        MEZO_HIP(hipEventSynchronize(use->done));
+        use->stream = stream;
+    }
+    if (!use) {
+        hipEvent_t ev = nullptr;
+        MEZO_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+        ps->uses.push_back({stream, ev, 0});
+        use = &ps->uses.back();
+    }
+    use->seq = ++ps->use_seq;
+    MEZO_HIP(hipEventRecord(use->done, stream));
     return MEZO_OK;
 }
 
-// Enqueue the engine over every storage type of ps. With src (same layout),
-// read src and write ps; that launch is made even with no records (a copy).
-int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hipStream_t stream,
+// Enqueue the engine over every storage type of ps, with the Gaussian the
+// records were made for. With src (same layout), read src and write ps; that
+// launch is made even with no records (a copy).
+int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bool portable, hipStream_t stream,
                    mezo_paramset* src = nullptr)
 {
     if (recs.empty() && !src) return MEZO_OK;
@@ -235,7 +290,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
         rc = ensure_device(src);
         if (rc) return rc;
         if (src->device != ps->device) {
-            t_last_error = "source and destination paramsets live on different devices";
+            set_error("source and destination paramsets live on different devices");
             return MEZO_EINVAL;
         }
     }
@@ -267,16 +322,23 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, hi
                                 hipMemcpyHostToDevice, stream));
         args.ext = slot->dev;
     }
-    for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
+    hipError_t e = hipSuccess;
+    for (uint32_t dt = 0; dt < mezo::kStorageTypes && e == hipSuccess; ++dt) {
         if (ps->table[dt].empty()) continue;
         args.tensors = ps->d_table[dt];
         args.tile_tensor = ps->d_tile_tensor[dt];
         args.src_tensors = src ? src->d_table[dt] : nullptr;
         args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
         args.total_tiles = ps->total_tiles[dt];
-        MEZO_HIP(mezo::launch_engine(args, dt, ps->gaussian.load() == MEZO_GAUSS_PORTABLE, stream));
+        e = mezo::launch_engine(args, dt, portable, stream);
     }
-    if (slot) MEZO_HIP(hipEventRecord(slot->done, stream));
+    // The slot is reused only after this event: recorded whenever its copy
+    // was enqueued, also when a launch failed.
+    if (slot) {
+        const hipError_t er = hipEventRecord(slot->done, stream);
+        if (e == hipSuccess) e = er;
+    }
+    if (e != hipSuccess) return hip_fail(e, "engine launch");
     rc = mark_use(ps, stream);
     if (rc == MEZO_OK && src && src != ps) rc = mark_use(src, stream);
     return rc;
@@ -341,64 +403,68 @@ extern "C" {
 
 int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* out)
 {
-    if (!t || !out || n == 0) return MEZO_EINVAL;
-    std::vector<Span> spans;
-    std::vector<uint32_t> ids;
-    spans.reserve(2 * size_t(n));
-    ids.reserve(n);
-    for (uint32_t i = 0; i < n; ++i) {
-        if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16 && t[i].dtype != MEZO_NF4) return MEZO_EDTYPE;
-        if (!t[i].data || (reinterpret_cast<uintptr_t>(t[i].data) & 15u)) return MEZO_EINVAL;
-        if (t[i].numel == 0 || t[i].numel > MEZO_MAX_NUMEL) return MEZO_EINVAL;
-        if (t[i].dtype == MEZO_NF4) {
-            if (!t[i].absmax || (reinterpret_cast<uintptr_t>(t[i].absmax) & 15u)) return MEZO_EINVAL;
-        } else if (t[i].absmax) {
-            return MEZO_EINVAL;
+    return guarded("mezo_paramset_create", [&]() -> int {
+        if (!t || !out || n == 0) return MEZO_EINVAL;
+        std::vector<Span> spans;
+        std::vector<uint32_t> ids;
+        spans.reserve(2 * size_t(n));
+        ids.reserve(n);
+        for (uint32_t i = 0; i < n; ++i) {
+            if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16 && t[i].dtype != MEZO_NF4) return MEZO_EDTYPE;
+            if (!t[i].data || (reinterpret_cast<uintptr_t>(t[i].data) & 15u)) return MEZO_EINVAL;
+            if (t[i].numel == 0 || t[i].numel > MEZO_MAX_NUMEL) return MEZO_EINVAL;
+            if (t[i].dtype == MEZO_NF4) {
+                if (!t[i].absmax || (reinterpret_cast<uintptr_t>(t[i].absmax) & 15u)) return MEZO_EINVAL;
+            } else if (t[i].absmax) {
+                return MEZO_EINVAL;
+            }
+            add_spans(reinterpret_cast<uint64_t>(t[i].data), reinterpret_cast<uint64_t>(t[i].absmax), t[i].numel,
+                      t[i].dtype, spans);
+            ids.push_back(t[i].tensor_id);
         }
-        add_spans(reinterpret_cast<uint64_t>(t[i].data), reinterpret_cast<uint64_t>(t[i].absmax), t[i].numel,
-                  t[i].dtype, spans);
-        ids.push_back(t[i].tensor_id);
-    }
-    std::sort(ids.begin(), ids.end());
-    if (std::adjacent_find(ids.begin(), ids.end()) != ids.end()) return MEZO_EINVAL;
-    if (!disjoint(spans)) return MEZO_EOVERLAP;
+        std::sort(ids.begin(), ids.end());
+        if (std::adjacent_find(ids.begin(), ids.end()) != ids.end()) return MEZO_EINVAL;
+        if (!disjoint(spans)) return MEZO_EOVERLAP;
 
-    mezo_paramset* ps = new (std::nothrow) mezo_paramset;
-    if (!ps) return MEZO_EINVAL;
-    uint64_t numel = 0;
-    for (uint32_t i = 0; i < n; ++i) {
-        const uint32_t dt = t[i].dtype;
-        mezo::TensorDesc d;
-        d.data = reinterpret_cast<uint64_t>(t[i].data);
-        d.aux = reinterpret_cast<uint64_t>(t[i].absmax);
-        d.numel = t[i].numel;
-        d.tensor_id = t[i].tensor_id;
-        d.dtype = dt;
-        d.tile_begin = ps->total_tiles[dt];
-        const uint64_t per = tile_of(dt);
-        ps->total_tiles[dt] += (t[i].numel + per - 1) / per;
-        ps->table[dt].push_back(d);
-        numel += t[i].numel;
-    }
-    ps->numel = numel;
-    for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
-        if (ps->total_tiles[dt] > 0x7FFFFFFFull) {
-            delete ps;  // more tiles than one launch can address
-            return MEZO_EINVAL;
+        std::unique_ptr<mezo_paramset> ps(new mezo_paramset);
+        uint64_t numel = 0;
+        for (uint32_t i = 0; i < n; ++i) {
+            const uint32_t dt = t[i].dtype;
+            mezo::TensorDesc d;
+            d.data = reinterpret_cast<uint64_t>(t[i].data);
+            d.aux = reinterpret_cast<uint64_t>(t[i].absmax);
+            d.numel = t[i].numel;
+            d.tensor_id = t[i].tensor_id;
+            d.dtype = dt;
+            d.tile_begin = ps->total_tiles[dt];
+            const uint64_t per = tile_of(dt);
+            ps->total_tiles[dt] += (t[i].numel + per - 1) / per;
+            ps->table[dt].push_back(d);
+            numel += t[i].numel;
         }
-    }
-    *out = ps;
-    return MEZO_OK;
+        ps->numel = numel;
+        for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
+            if (ps->total_tiles[dt] > 0x7FFFFFFFull) return MEZO_EINVAL;  // more tiles than one launch can address
+        }
+        *out = ps.release();
+        return MEZO_OK;
+    });
 }
 
 void mezo_paramset_destroy(mezo_paramset_t ps)
 {
     if (!ps) return;
     {
-        std::lock_guard<std::mutex> lock(ps->mu);
+        // taken so that a call still running on another thread finishes
+        // first; the caller must not start new ones
+        std::unique_lock<std::mutex> lock(ps->mu, std::defer_lock);
+        try {
+            lock.lock();
+        } catch (...) {
+        }
         for (auto& u : ps->uses) {
-            (void)hipEventSynchronize(u.second);
-            (void)hipEventDestroy(u.second);
+            (void)hipEventSynchronize(u.done);
+            (void)hipEventDestroy(u.done);
         }
         for (auto& s : ps->slots) {
             if (s.done) {
@@ -421,125 +487,145 @@ uint64_t mezo_paramset_numel(mezo_paramset_t ps) { return ps ? ps->numel : 0; }
 int mezo_paramset_set_gaussian(mezo_paramset_t ps, uint32_t gaussian)
 {
     if (!ps || (gaussian != MEZO_GAUSS_FAST && gaussian != MEZO_GAUSS_PORTABLE)) return MEZO_EINVAL;
-    std::lock_guard<std::mutex> lock(ps->mu);
     ps->gaussian.store(gaussian);
     return MEZO_OK;
 }
 
 int mezo_perturb(mezo_paramset_t ps, mezo_seed_t seed, float scale, void* stream)
 {
-    if (!ps) return MEZO_EINVAL;
-    if (!std::isfinite(scale)) return MEZO_ERANGE;
-    if (scale == 0.0f) return MEZO_OK;
-    std::vector<mezo::SeedRec> recs(1, make_rec(seed, scale, true, fold_of(ps)));
-    std::lock_guard<std::mutex> lock(ps->mu);
-    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+    return guarded("mezo_perturb", [&]() -> int {
+        if (!ps) return MEZO_EINVAL;
+        if (!std::isfinite(scale)) return MEZO_ERANGE;
+        if (scale == 0.0f) return MEZO_OK;
+        const bool portable = portable_of(ps);
+        std::vector<mezo::SeedRec> recs(1, make_rec(seed, scale, true, !portable));
+        std::lock_guard<std::mutex> lock(ps->mu);
+        return launch_records(ps, recs, portable, static_cast<hipStream_t>(stream));
+    });
 }
 
 int mezo_perturb_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const float* scales, uint32_t n,
                        void* stream)
 {
-    if (!ps) return MEZO_EINVAL;
-    if (n == 0) return MEZO_OK;
-    if (!seeds || !scales) return MEZO_EINVAL;
-    for (uint32_t i = 0; i < n; ++i)
-        if (!std::isfinite(scales[i])) return MEZO_ERANGE;
-    std::vector<mezo::SeedRec> recs;
-    recs.reserve(n);
-    for (uint32_t i = 0; i < n; ++i)
-        if (scales[i] != 0.0f) recs.push_back(make_rec(seeds[i], scales[i], true, fold_of(ps)));
-    std::lock_guard<std::mutex> lock(ps->mu);
-    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+    return guarded("mezo_perturb_multi", [&]() -> int {
+        if (!ps) return MEZO_EINVAL;
+        if (n == 0) return MEZO_OK;
+        if (!seeds || !scales) return MEZO_EINVAL;
+        for (uint32_t i = 0; i < n; ++i)
+            if (!std::isfinite(scales[i])) return MEZO_ERANGE;
+        const bool portable = portable_of(ps);
+        std::vector<mezo::SeedRec> recs;
+        recs.reserve(n);
+        for (uint32_t i = 0; i < n; ++i)
+            if (scales[i] != 0.0f) recs.push_back(make_rec(seeds[i], scales[i], true, !portable));
+        std::lock_guard<std::mutex> lock(ps->mu);
+        return launch_records(ps, recs, portable, static_cast<hipStream_t>(stream));
+    });
 }
 
 int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, const int8_t* q, uint32_t K,
                       const mezo_codec_t* codec, float lr, void* stream)
 {
-    if (!ps) return MEZO_EINVAL;
-    std::vector<mezo::SeedRec> recs;
-    recs.reserve(K);
-    int rc = append_step(seeds, q, K, codec, lr, fold_of(ps), recs);
-    if (rc) return rc;
-    std::lock_guard<std::mutex> lock(ps->mu);
-    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+    return guarded("mezo_update_multi", [&]() -> int {
+        if (!ps) return MEZO_EINVAL;
+        const bool portable = portable_of(ps);
+        std::vector<mezo::SeedRec> recs;
+        recs.reserve(K);
+        int rc = append_step(seeds, q, K, codec, lr, !portable, recs);
+        if (rc) return rc;
+        std::lock_guard<std::mutex> lock(ps->mu);
+        return launch_records(ps, recs, portable, static_cast<hipStream_t>(stream));
+    });
 }
 
 int mezo_perturb_from(mezo_paramset_t dst, mezo_paramset_t src, mezo_seed_t seed, float scale,
                       void* stream)
 {
-    if (!dst || !src) return MEZO_EINVAL;
-    if (!std::isfinite(scale)) return MEZO_ERANGE;
-    int rc = check_pair(dst, src);
-    if (rc) return rc;
-    std::vector<mezo::SeedRec> recs;
-    if (scale != 0.0f) recs.push_back(make_rec(seed, scale, true, fold_of(dst)));
-    if (dst == src) {
-        std::lock_guard<std::mutex> lock(dst->mu);
-        return launch_records(dst, recs, static_cast<hipStream_t>(stream));
-    }
-    std::scoped_lock lock(dst->mu, src->mu);
-    return launch_records(dst, recs, static_cast<hipStream_t>(stream), src);
+    return guarded("mezo_perturb_from", [&]() -> int {
+        if (!dst || !src) return MEZO_EINVAL;
+        if (!std::isfinite(scale)) return MEZO_ERANGE;
+        int rc = check_pair(dst, src);
+        if (rc) return rc;
+        const bool portable = portable_of(dst);
+        std::vector<mezo::SeedRec> recs;
+        if (scale != 0.0f) recs.push_back(make_rec(seed, scale, true, !portable));
+        if (dst == src) {
+            std::lock_guard<std::mutex> lock(dst->mu);
+            return launch_records(dst, recs, portable, static_cast<hipStream_t>(stream));
+        }
+        std::scoped_lock lock(dst->mu, src->mu);
+        return launch_records(dst, recs, portable, static_cast<hipStream_t>(stream), src);
+    });
 }
 
 int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src, const mezo_seed_t* seeds,
                            const int8_t* q, uint32_t K, const mezo_codec_t* codec, float lr, void* stream)
 {
-    if (!dst || !src) return MEZO_EINVAL;
-    std::vector<mezo::SeedRec> recs;
-    recs.reserve(K);
-    int rc = append_step(seeds, q, K, codec, lr, fold_of(dst), recs);
-    if (rc) return rc;
-    rc = check_pair(dst, src);
-    if (rc) return rc;
-    if (dst == src) {
-        std::lock_guard<std::mutex> lock(dst->mu);
-        return launch_records(dst, recs, static_cast<hipStream_t>(stream));
-    }
-    std::scoped_lock lock(dst->mu, src->mu);
-    return launch_records(dst, recs, static_cast<hipStream_t>(stream), src);
+    return guarded("mezo_update_multi_from", [&]() -> int {
+        if (!dst || !src) return MEZO_EINVAL;
+        const bool portable = portable_of(dst);
+        std::vector<mezo::SeedRec> recs;
+        recs.reserve(K);
+        int rc = append_step(seeds, q, K, codec, lr, !portable, recs);
+        if (rc) return rc;
+        rc = check_pair(dst, src);
+        if (rc) return rc;
+        if (dst == src) {
+            std::lock_guard<std::mutex> lock(dst->mu);
+            return launch_records(dst, recs, portable, static_cast<hipStream_t>(stream));
+        }
+        std::scoped_lock lock(dst->mu, src->mu);
+        return launch_records(dst, recs, portable, static_cast<hipStream_t>(stream), src);
+    });
 }
 
 int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const mezo_codec_t* codec,
                 void* stream)
 {
-    if (!ps || !codec) return MEZO_EINVAL;
-    if (!codec_valid(codec)) return MEZO_ERANGE;
-    if (T == 0) return MEZO_OK;
-    if (!steps) return MEZO_EINVAL;
-    std::vector<mezo::SeedRec> recs;
-    size_t total = 0;
-    for (uint32_t t = 0; t < T; ++t) total += steps[t].K;
-    recs.reserve(total);
-    for (uint32_t t = 0; t < T; ++t) {
-        int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, fold_of(ps), recs);
-        if (rc) return rc;
-    }
-    std::lock_guard<std::mutex> lock(ps->mu);
-    return launch_records(ps, recs, static_cast<hipStream_t>(stream));
+    return guarded("mezo_replay", [&]() -> int {
+        if (!ps || !codec) return MEZO_EINVAL;
+        if (!codec_valid(codec)) return MEZO_ERANGE;
+        if (T == 0) return MEZO_OK;
+        if (!steps) return MEZO_EINVAL;
+        const bool portable = portable_of(ps);
+        std::vector<mezo::SeedRec> recs;
+        uint64_t total = 0;
+        for (uint32_t t = 0; t < T; ++t) total += steps[t].K;
+        if (total > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
+        recs.reserve(total);
+        for (uint32_t t = 0; t < T; ++t) {
+            int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, !portable, recs);
+            if (rc) return rc;
+        }
+        std::lock_guard<std::mutex> lock(ps->mu);
+        return launch_records(ps, recs, portable, static_cast<hipStream_t>(stream));
+    });
 }
 
 int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
 {
-    if (!ps || !out_dev || (reinterpret_cast<uintptr_t>(out_dev) & 7u)) return MEZO_EINVAL;
-    std::lock_guard<std::mutex> lock(ps->mu);
-    int rc = ensure_device(ps);
-    if (rc) return rc;
-    mezo::ChecksumArgs tabs[mezo_paramset::kTypes];
-    uint32_t dts[mezo_paramset::kTypes];
-    int n = 0;
-    for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
-        if (ps->table[dt].empty()) continue;
-        tabs[n].tensors = ps->d_table[dt];
-        tabs[n].tile_tensor = ps->d_tile_tensor[dt];
-        tabs[n].total_tiles = ps->total_tiles[dt];
-        tabs[n].out = reinterpret_cast<unsigned long long*>(out_dev);
-        dts[n] = dt;
-        ++n;
-    }
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
-                                   ps->device, st));
-    return mark_use(ps, st);
+    return guarded("mezo_checksum", [&]() -> int {
+        if (!ps || !out_dev || (reinterpret_cast<uintptr_t>(out_dev) & 7u)) return MEZO_EINVAL;
+        std::lock_guard<std::mutex> lock(ps->mu);
+        int rc = ensure_device(ps);
+        if (rc) return rc;
+        mezo::ChecksumArgs tabs[mezo_paramset::kTypes];
+        uint32_t dts[mezo_paramset::kTypes];
+        int n = 0;
+        for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
+            if (ps->table[dt].empty()) continue;
+            tabs[n].tensors = ps->d_table[dt];
+            tabs[n].tile_tensor = ps->d_tile_tensor[dt];
+            tabs[n].total_tiles = ps->total_tiles[dt];
+            tabs[n].out = reinterpret_cast<unsigned long long*>(out_dev);
+            dts[n] = dt;
+            ++n;
+        }
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
+                                       ps->device, st));
+        return mark_use(ps, st);
+    });
 }
 
 namespace {
@@ -569,13 +655,14 @@ int nf4_convert(const void* values, uint32_t dtype, uint64_t n, const void* code
 
 int mezo_nf4_quantize(const void* src, uint32_t src_dtype, uint64_t n, void* codes, float* absmax, void* stream)
 {
-    return nf4_convert(src, src_dtype, n, codes, absmax, true, stream);
+    return guarded("mezo_nf4_quantize", [&] { return nf4_convert(src, src_dtype, n, codes, absmax, true, stream); });
 }
 
 int mezo_nf4_dequantize(const void* codes, const float* absmax, uint64_t n, void* dst, uint32_t dst_dtype,
                         void* stream)
 {
-    return nf4_convert(dst, dst_dtype, n, codes, absmax, false, stream);
+    return guarded("mezo_nf4_dequantize",
+                   [&] { return nf4_convert(dst, dst_dtype, n, codes, absmax, false, stream); });
 }
 
 int quantize_projgrad(const float* g, int8_t* q, uint32_t n, const mezo_codec_t* codec)
@@ -645,12 +732,13 @@ const char* mezo_strerror(int code)
     case MEZO_EORDER: return "seeds not strictly ascending by (machine, step, sample)";
     case MEZO_ERANGE: return "value out of range (q = -128, NaN gradient, non-finite lr/scale, bad codec)";
     case MEZO_EHIP: return "HIP runtime failure";
+    case MEZO_ENOMEM: return "host memory allocation failed";
     default: return "unknown error code";
     }
 }
 
-const char* mezo_last_error(void) { return t_last_error.c_str(); }
+const char* mezo_last_error(void) { return t_last_error; }
 
-int mezo_version(void) { return 200; }
+int mezo_version(void) { return 300; }
 
 }  // extern "C"

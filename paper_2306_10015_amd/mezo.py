@@ -25,7 +25,7 @@ import numpy as np
 
 LIB_PATH = Path(__file__).resolve().parent / "libmezo.so"
 
-OK, EINVAL, EDTYPE, EOVERLAP, EORDER, ERANGE, EHIP = 0, -1, -2, -3, -4, -5, -6
+OK, EINVAL, EDTYPE, EOVERLAP, EORDER, ERANGE, EHIP, ENOMEM = 0, -1, -2, -3, -4, -5, -6, -7
 F32, BF16, NF4 = 0, 1, 2
 #: NF4 elements per absmax value.
 NF4_BLOCK = 64
@@ -128,7 +128,7 @@ lib = _load()
 class MezoError(RuntimeError):
     def __init__(self, code: int, what: str):
         msg = lib.mezo_strerror(code).decode()
-        if code == EHIP:
+        if code in (EHIP, ENOMEM):
             msg += f" ({lib.mezo_last_error().decode()})"
         super().__init__(f"{what}: {msg} [code {code}]")
         self.code = code

@@ -238,6 +238,11 @@ def test_perturb_and_replay_argument_checks(fake_ps):
     assert lib.mezo_replay(fake_ps, None, 2, c, None) == mezo.EINVAL
     steps[1] = mezo.Step(s0.ctypes.data, q.ctypes.data, 2, float("nan"))
     assert lib.mezo_replay(fake_ps, steps, 2, c, None) == mezo.ERANGE
+    # more than 2^32 - 1 terms in one call: rejected from the step counts
+    # alone, before any seed or code is read
+    steps[0] = mezo.Step(s0.ctypes.data, q.ctypes.data, 1 << 31, 1e-3)
+    steps[1] = mezo.Step(s0.ctypes.data, q.ctypes.data, 1 << 31, 1e-3)
+    assert lib.mezo_replay(fake_ps, steps, 2, c, None) == mezo.ERANGE
 
 
 def test_perturb_multi_argument_checks(fake_ps):
@@ -276,7 +281,7 @@ def test_gaussian_mode_setter():
 
 def test_strerror_covers_every_code():
     for code in (mezo.OK, mezo.EINVAL, mezo.EDTYPE, mezo.EOVERLAP, mezo.EORDER, mezo.ERANGE,
-                 mezo.EHIP):
+                 mezo.EHIP, mezo.ENOMEM):
         assert mezo.lib.mezo_strerror(code).decode() not in ("", "unknown error code")
     assert mezo.lib.mezo_strerror(-99).decode() == "unknown error code"
 

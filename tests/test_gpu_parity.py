@@ -520,6 +520,30 @@ def test_perturb_multi_nf4_portable_bit_exact(mz, orc):
     ps.close()
 
 
+def test_more_streams_than_tracked(mz, orc):
+    """One paramset driven from 20 streams in a chain (each waits for the one
+    before): more streams than the paramset tracks, so later streams take over
+    the entries used longest ago. The result is the chain's, bit for bit (the
+    portable Gaussian), and destroy returns with every stream drained."""
+    import torch
+    hosts = tiny_hosts(synth.F32)[:1]
+    devs, ps = make_set(mz, hosts)
+    ps.set_gaussian(mz.GAUSS_PORTABLE)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(20)]
+    prev = torch.cuda.current_stream()
+    ref = hosts[0].copy()
+    for i, s in enumerate(streams):
+        s.wait_stream(prev)
+        with torch.cuda.stream(s):
+            ps.perturb((i, 1, 0), 1e-3)
+        orc.perturb(ref, 0, (i, 1, 0), 1e-3, portable=True)
+        prev = s
+    ps.close()
+    assert all(s.query() for s in streams)
+    assert np.array_equal(to_host(devs[0]).view(np.uint32), ref.view(np.uint32))
+
+
 def test_destroy_waits_for_work_on_every_stream(mz):
     """A paramset used on two streams: destroy returns only after the long
     replay on the first stream has finished, not just the short perturb
