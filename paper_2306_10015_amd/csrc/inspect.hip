@@ -27,9 +27,14 @@ hipError_t launch_box_muller(const uint32_t* words, uint64_t n_blocks, uint32_t 
     for (uint64_t done = 0; done < n_blocks; done += kChunk) {
         const uint64_t n = n_blocks - done < kChunk ? n_blocks - done : kChunk;
         const uint64_t grid = (n + kThreads - 1) / kThreads;
-        hipLaunchKernelGGL(box_muller_kernel, dim3(uint32_t(grid)), dim3(kThreads), 0, stream, words + 4 * done,
-                           n, portable, z + 4 * done);
-        const hipError_t e = hipGetLastError();
+        const uint32_t* w = words + 4 * done;
+        float* zo = z + 4 * done;
+        uint64_t cnt = n;
+        uint32_t pt = portable;
+        // the status of this launch itself, not the thread's last HIP error
+        void* params[] = {&w, &cnt, &pt, &zo};
+        const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(box_muller_kernel), dim3(uint32_t(grid)),
+                                             dim3(kThreads), params, 0, stream);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

@@ -734,21 +734,22 @@ __global__ void zero_u64_kernel(unsigned long long* out)
 // ---- host-side launchers ----------------------------------------------------
 
 namespace {
-template <bool kInline, uint32_t kDtype, bool kPortable>
-void launch_one(const EngineArgs& args, dim3 g, dim3 b, hipStream_t stream)
+// Launch a one-argument kernel and return the status of this launch itself
+// (not the thread's last HIP error, which may hold an earlier failure of
+// another caller's call).
+template <class Arg>
+hipError_t launch1(void (*kernel)(Arg), dim3 g, dim3 b, hipStream_t stream, Arg arg)
 {
-    hipLaunchKernelGGL((engine_kernel<kInline, kDtype, kPortable>), g, b, 0, stream, args);
+    void* params[] = {&arg};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kernel), g, b, params, 0, stream);
 }
 
 template <bool kInline, bool kPortable>
-void launch_dtype(const EngineArgs& args, uint32_t dtype, dim3 g, dim3 b, hipStream_t stream)
+hipError_t launch_dtype(const EngineArgs& args, uint32_t dtype, dim3 g, dim3 b, hipStream_t stream)
 {
-    if (dtype == kF32)
-        launch_one<kInline, kF32, kPortable>(args, g, b, stream);
-    else if (dtype == kBF16)
-        launch_one<kInline, kBF16, kPortable>(args, g, b, stream);
-    else
-        launch_one<kInline, kNF4, kPortable>(args, g, b, stream);
+    if (dtype == kF32) return launch1(engine_kernel<kInline, kF32, kPortable>, g, b, stream, args);
+    if (dtype == kBF16) return launch1(engine_kernel<kInline, kBF16, kPortable>, g, b, stream, args);
+    return launch1(engine_kernel<kInline, kNF4, kPortable>, g, b, stream, args);
 }
 }  // namespace
 
@@ -759,18 +760,11 @@ hipError_t launch_engine(const EngineArgs& args, uint32_t dtype, bool portable, 
     const bool inl = args.n_rec <= kInlineRecs;
     const dim3 g{uint32_t(args.total_tiles)};
     const dim3 b{uint32_t(kThreads)};
-    if (inl) {
-        if (portable)
-            launch_dtype<true, true>(args, dtype, g, b, stream);
-        else
-            launch_dtype<true, false>(args, dtype, g, b, stream);
-    } else {
-        if (portable)
-            launch_dtype<false, true>(args, dtype, g, b, stream);
-        else
-            launch_dtype<false, false>(args, dtype, g, b, stream);
-    }
-    return hipGetLastError();
+    if (inl)
+        return portable ? launch_dtype<true, true>(args, dtype, g, b, stream)
+                        : launch_dtype<true, false>(args, dtype, g, b, stream);
+    return portable ? launch_dtype<false, true>(args, dtype, g, b, stream)
+                    : launch_dtype<false, false>(args, dtype, g, b, stream);
 }
 
 hipError_t launch_generate(const GenArgs& args, hipStream_t stream)
@@ -789,8 +783,7 @@ hipError_t launch_generate(const GenArgs& args, hipStream_t stream)
         a.z = args.z ? args.z + done : nullptr;
         const uint64_t nblk = ((first + n - 1) >> 2) - (first >> 2) + 1;
         const uint64_t grid = (nblk + kThreads - 1) / kThreads;
-        hipLaunchKernelGGL(generate_kernel, dim3(uint32_t(grid)), dim3(kThreads), 0, stream, a);
-        hipError_t e = hipGetLastError();
+        const hipError_t e = launch1(generate_kernel, dim3(uint32_t(grid)), dim3(kThreads), stream, a);
         if (e != hipSuccess) return e;
         left -= n;
         first += n;
@@ -814,8 +807,7 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
         if (e != hipSuccess) return e;
         g_cus[device].store(cus, std::memory_order_relaxed);
     }
-    hipLaunchKernelGGL(zero_u64_kernel, dim3(1), dim3(64), 0, stream, out);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch1(zero_u64_kernel, dim3(1), dim3(64), stream, out);
     if (e != hipSuccess) return e;
     for (int i = 0; i < n_tables; ++i) {
         if (tables[i].total_tiles == 0) continue;
@@ -828,12 +820,11 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
         const dim3 g{uint32_t(grid)};
         const dim3 b{uint32_t(kThreads)};
         if (dtypes[i] == kF32)
-            hipLaunchKernelGGL(checksum_kernel<kF32>, g, b, 0, stream, tables[i]);
+            e = launch1(checksum_kernel<kF32>, g, b, stream, tables[i]);
         else if (dtypes[i] == kBF16)
-            hipLaunchKernelGGL(checksum_kernel<kBF16>, g, b, 0, stream, tables[i]);
+            e = launch1(checksum_kernel<kBF16>, g, b, stream, tables[i]);
         else
-            hipLaunchKernelGGL(checksum_nf4_kernel, g, b, 0, stream, tables[i]);
-        e = hipGetLastError();
+            e = launch1(checksum_nf4_kernel, g, b, stream, tables[i]);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -846,11 +837,7 @@ hipError_t launch_nf4(const NF4ConvArgs& args, bool quantize, hipStream_t stream
     if (tiles > uint64_t(0x7FFFFFFF)) return hipErrorInvalidValue;
     const dim3 g{uint32_t(tiles)};
     const dim3 b{uint32_t(kThreads)};
-    if (quantize)
-        hipLaunchKernelGGL(nf4_quantize_kernel, g, b, 0, stream, args);
-    else
-        hipLaunchKernelGGL(nf4_dequantize_kernel, g, b, 0, stream, args);
-    return hipGetLastError();
+    return launch1(quantize ? nf4_quantize_kernel : nf4_dequantize_kernel, g, b, stream, args);
 }
 
 }  // namespace mezo
