@@ -114,12 +114,10 @@ def projected_grads(n: int, seed: int = 3, spread: float = 0.5) -> np.ndarray:
     return rng.normal(0.0, spread, size=n).astype(np.float32)
 
 
-def fp32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round-to-nearest-even fp32 -> bf16 bit patterns (input preparation only;
-    finite inputs)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    u = u + 0x7FFF + ((u >> 16) & 1)
-    return (u >> 16).astype(np.uint16)
+def bf16_bits_truncated(x: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns of fp32 draws: the top 16 bits of each (truncation;
+    starting weights only, not the method's rounding)."""
+    return (np.ascontiguousarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
 
 
 def bf16_bits_to_fp32(b: np.ndarray) -> np.ndarray:
@@ -128,10 +126,10 @@ def bf16_bits_to_fp32(b: np.ndarray) -> np.ndarray:
 
 def theta0_tensor(shape, dtype: str, tensor_id: int, seed: int = 0) -> np.ndarray:
     """Starting weights of one tensor: N(0, 0.02) fp32 from PCG64(seed, tensor_id);
-    bf16 storage as RNE bit patterns (uint16)."""
+    bf16 storage as the truncated bit patterns of those draws (uint16)."""
     rng = np.random.Generator(np.random.PCG64([seed, tensor_id]))
     x = rng.standard_normal(size=int(np.prod(shape)), dtype=np.float32) * np.float32(0.02)
-    return x if dtype == F32 else fp32_to_bf16_bits(x)
+    return x if dtype == F32 else bf16_bits_truncated(x)
 
 
 def nf4_theta0_tensor(numel: int, tensor_id: int, seed: int = 0):

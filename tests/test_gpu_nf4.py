@@ -58,7 +58,7 @@ def test_quantize_kernel_bit_exact(mz, nf4, n, dtype):
     from gpu_util import to_device
     w = values_of(n, n, zero_block=True)
     if dtype == "bf16":
-        bits = synth.fp32_to_bf16_bits(w)
+        bits = synth.bf16_bits_truncated(w)
         src = to_device(bits)
         w = synth.bf16_bits_to_fp32(bits)
     else:
