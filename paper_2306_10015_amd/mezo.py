@@ -374,10 +374,16 @@ class ParamSet:
             _check(lib.mezo_checksum(self._h, out.data_ptr(), _stream_ptr(stream)), "mezo_checksum")
 
     def checksum(self, stream=None) -> int:
-        """The checksum as a Python int (synchronises with the stream)."""
+        """The checksum as a Python int (waits for the stream it ran on)."""
         import torch
-        out = torch.empty(1, dtype=torch.int64, device=self.tensors[0].device)
+        out = torch.empty(1, dtype=torch.int64, device=self.device)
         self.checksum_into(out, stream)
+        if stream is not None:
+            # .item() reads on the current stream, which does not wait for `stream`
+            if isinstance(stream, torch.cuda.Stream):
+                stream.synchronize()
+            else:
+                torch.cuda.synchronize(self.device)
         return int(out.item()) & 0xFFFFFFFFFFFFFFFF
 
     def replay(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:

@@ -388,6 +388,21 @@ def test_checksum_detects_one_flipped_bit(mz):
     assert ps.checksum() == base
 
 
+def test_checksum_on_a_side_stream(mz, orc):
+    """checksum(stream=s) returns the checksum of theta after the work queued
+    before it on s (it waits for s, not for the current stream)."""
+    import torch
+    hosts = tiny_hosts(synth.F32)
+    devs, ps = make_set(mz, hosts)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        ps.replay([(synth.seeds(8, 4, step=t), synth.grads_int8(32, seed=t), 1e-4) for t in range(40)])
+    got = ps.checksum(stream=s)
+    torch.cuda.synchronize()
+    assert got == orc.checksum([to_host(d) for d in devs])
+
+
 def test_checksum_full_125m_set(mz, orc):
     import torch
     from gpu_util import theta_on_device
