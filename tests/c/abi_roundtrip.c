@@ -2,9 +2,10 @@
  * abi_roundtrip.c — the engine driven from plain C through include/mezo.h
  * alone (no Python, no torch): device memory from the HIP runtime's C API,
  * one fp32 and one bf16 tensor, a perturb (Algorithm 1, PerturbParameters), a
- * fused 4-seed update (the apply loop) and a checksum (ChecksumMatch), each
- * compared with the CPU oracle (test infrastructure, linked here only).
- * Exit status 0 when every check passes.
+ * fused 4-seed update (the apply loop), a 3-step replay (Appendix B), an
+ * update with the portable Gaussian (bit-exact) and a checksum
+ * (ChecksumMatch), each compared with the CPU oracle (test infrastructure,
+ * linked here only). Exit status 0 when every check passes.
  */
 #include <math.h>
 #include <stdint.h>
@@ -78,8 +79,31 @@ int main(void)
     mezo_seed_t seeds[K] = {{0u, 5u, 0u}, {1u, 5u, 0u}, {2u, 5u, 0u}, {3u, 5u, 0u}};
     int8_t q[K] = {17, -90, 127, -3};
     mezo_codec_t codec = {MEZO_CODEC_LINEAR, 1.0f / 127.0f, 1.0f};
+    /* a log of T steps of K seeds each, packed step after step */
+    enum { T = 3 };
+    orc_seed_t olog[T * K];
+    mezo_seed_t mlog[T * K];
+    int8_t qlog[T * K];
+    uint32_t klog[T];
+    float lrlog[T];
+    mezo_step_t steps[T];
+    for (int t = 0; t < T; ++t) {
+        for (int k = 0; k < K; ++k) {
+            const int i = t * K + k;
+            olog[i].machine = mlog[i].machine = (uint64_t)k;
+            olog[i].step = mlog[i].step = 10u + (uint32_t)t;
+            olog[i].sample = mlog[i].sample = 0u;
+            qlog[i] = (int8_t)(((t * 37 + k * 53) % 255) - 127);
+        }
+        klog[t] = K;
+        lrlog[t] = 1e-3f * (float)(t + 1);
+        steps[t].seeds = mlog + t * K;
+        steps[t].q = qlog + t * K;
+        steps[t].K = K;
+        steps[t].lr = lrlog[t];
+    }
 
-    for (int step = 0; step < 2; ++step) {
+    for (int step = 0; step < 4; ++step) {
         /* the oracle starts from what the GPU holds before the step */
         CHECK(hipMemcpy(rf, df, NF * sizeof(float), hipMemcpyDeviceToHost) == hipSuccess, "copy back");
         CHECK(hipMemcpy(rb, db, NB * sizeof(uint16_t), hipMemcpyDeviceToHost) == hipSuccess, "copy back");
@@ -88,16 +112,36 @@ int main(void)
             CHECK(mezo_perturb(ps, s, 1e-3f, NULL) == MEZO_OK, "perturb");
             CHECK(orc_perturb(rf, ORC_F32, 7u, NULL, 0, NF, os, 1e-3f) == 0, "oracle perturb");
             CHECK(orc_perturb(rb, ORC_BF16, 2u, NULL, 0, NB, os, 1e-3f) == 0, "oracle perturb");
-        } else {
+        } else if (step == 1) {
             CHECK(mezo_update_multi(ps, seeds, q, K, &codec, 1e-3f, NULL) == MEZO_OK, "update");
             CHECK(orc_update(rf, ORC_F32, 7u, NULL, 0, NF, oseeds, q, K, ORC_CODEC_LINEAR, 1.0f / 127.0f,
                              1.0f, 1e-3f) == 0, "oracle update");
             CHECK(orc_update(rb, ORC_BF16, 2u, NULL, 0, NB, oseeds, q, K, ORC_CODEC_LINEAR, 1.0f / 127.0f,
                              1.0f, 1e-3f) == 0, "oracle update");
+        } else if (step == 2) {
+            CHECK(mezo_replay(ps, steps, T, &codec, NULL) == MEZO_OK, "replay");
+            CHECK(orc_replay(rf, ORC_F32, 7u, NULL, 0, NF, olog, qlog, klog, lrlog, T, ORC_CODEC_LINEAR,
+                             1.0f / 127.0f, 1.0f) == 0, "oracle replay");
+            CHECK(orc_replay(rb, ORC_BF16, 2u, NULL, 0, NB, olog, qlog, klog, lrlog, T, ORC_CODEC_LINEAR,
+                             1.0f / 127.0f, 1.0f) == 0, "oracle replay");
+        } else {
+            CHECK(mezo_paramset_set_gaussian(ps, MEZO_GAUSS_PORTABLE) == MEZO_OK, "set_gaussian");
+            CHECK(mezo_update_multi(ps, seeds, q, K, &codec, 1e-3f, NULL) == MEZO_OK, "portable update");
+            CHECK(orc_update_portable(rf, ORC_F32, 7u, NULL, 0, NF, oseeds, q, K, ORC_CODEC_LINEAR,
+                                      1.0f / 127.0f, 1.0f, 1e-3f) == 0, "oracle portable update");
+            CHECK(orc_update_portable(rb, ORC_BF16, 2u, NULL, 0, NB, oseeds, q, K, ORC_CODEC_LINEAR,
+                                      1.0f / 127.0f, 1.0f, 1e-3f) == 0, "oracle portable update");
         }
         CHECK(hipDeviceSynchronize() == hipSuccess, "sync");
         CHECK(hipMemcpy(gf, df, NF * sizeof(float), hipMemcpyDeviceToHost) == hipSuccess, "copy back");
         CHECK(hipMemcpy(gb, db, NB * sizeof(uint16_t), hipMemcpyDeviceToHost) == hipSuccess, "copy back");
+        if (step == 3) {
+            /* the portable Gaussian: every bit */
+            CHECK(memcmp(gf, rf, NF * sizeof(float)) == 0, "portable update: fp32 not bit-exact");
+            CHECK(memcmp(gb, rb, NB * sizeof(uint16_t)) == 0, "portable update: bf16 not bit-exact");
+            printf("step 3 ok: portable update bit-exact\n");
+            continue;
+        }
         /* fp32: max |diff| <= 1e-6 max |ref| */
         double scale = 0.0, err = 0.0;
         for (int i = 0; i < NF; ++i) {
