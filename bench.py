@@ -28,6 +28,7 @@ import argparse
 import json
 import math
 import os
+import statistics
 import sys
 import time
 
@@ -44,10 +45,11 @@ sys.path.insert(0, ROOT)
 CLOCK_GHZ = 2.4
 VALU_LANE_INSTR_PER_S = 256 * 4 * 16 * CLOCK_GHZ * 1e9
 HBM_PEAK_GBS = 8000.0
-# each call timed alone: repeated for about this long (at least 3, at most
-# OPS_MAX_REPS launches)
+# each call timed alone: OPS_BATCHES batches of back-to-back launches, each
+# lasting about OPS_LOOP_MS (at most OPS_MAX_REPS launches); the median batch
 OPS_LOOP_MS = 30.0
 OPS_MAX_REPS = 400
+OPS_BATCHES = 10
 
 #: VALU instructions per Philox block (4 Gaussians) per seed in the engine's
 #: inner loop, the method's minimal sequence on gfx950: round 1 and the
@@ -370,13 +372,14 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         return a.elapsed_time(b) / reps
 
     def timed(fn):
-        # warm up, then repeat for about OPS_LOOP_MS so that short calls are
-        # timed over many launches at the clock a long run settles at
+        # warm up, then batches of about OPS_LOOP_MS so that short calls are
+        # timed over many launches at the clock a long run settles at; the
+        # median batch's average launch
         fn()
         torch.cuda.synchronize()
         once = loop(fn, 1)
-        reps = max(3, min(OPS_MAX_REPS, math.ceil(OPS_LOOP_MS / max(once, 1e-3))))
-        return loop(fn, reps)
+        reps = max(1, min(OPS_MAX_REPS, math.ceil(OPS_LOOP_MS / max(once, 1e-3))))
+        return statistics.median(loop(fn, reps) for _ in range(OPS_BATCHES))
 
     def entry(records, ms, nbytes=bytes_per_launch):
         t_s = ms / 1e3
