@@ -153,13 +153,23 @@ typedef struct {
  * after the step, a' = max |w'|, r = fl32(1 / a') (0 when a' = 0),
  * x = fl32(w' * r), and the new code is the number of NF4 midpoints
  * fl32((v_i + v_{i+1}) / 2) strictly below x (the nearest value, ties to the
- * lower code). For MEZO_F32 and MEZO_BF16 `absmax` must be NULL. */
+ * lower code). For MEZO_F32 and MEZO_BF16 `absmax` must be NULL.
+ *
+ * `first` is the index, within the logical tensor `tensor_id`, of the element
+ * at `data`: 0 for a whole tensor; for a shard of a tensor split across
+ * GPUs by element range, the shard's first element. A shard holding elements
+ * [first, first + numel) computes exactly the z and the weights of those
+ * elements of the whole tensor, and the shards' checksums add up to the whole
+ * tensor's. first must be a multiple of 8 with first + numel <=
+ * MEZO_MAX_NUMEL; MEZO_NF4 tensors are split by whole tensors only
+ * (first = 0). */
 typedef struct {
     void*    data;
     uint64_t numel;
     uint32_t tensor_id;
     uint32_t dtype;
     void*    absmax;
+    uint64_t first;
 } mezo_tensor_t;
 
 /* One-byte gradient code (Section 3). `scale` is used by LINEAR, `alpha` by
@@ -185,7 +195,8 @@ typedef struct mezo_paramset* mezo_paramset_t;
 /* ---- parameter sets --------------------------------------------------- */
 
 /* Register n tensors (copied; the array may be reused). Checks: t and out
- * non-null, n >= 1, every data non-null and 16-byte aligned, 1 <= numel <=
+ * non-null, n >= 1, every data non-null and 16-byte aligned, numel >= 1,
+ * first a multiple of 8 (0 for MEZO_NF4) and first + numel <=
  * MEZO_MAX_NUMEL, absmax 16-byte aligned for MEZO_NF4 and NULL otherwise
  * (else MEZO_EINVAL), dtype known (MEZO_EDTYPE), tensor_ids unique
  * (MEZO_EINVAL), no two tensors (codes and absmax arrays included)
@@ -255,7 +266,7 @@ MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t 
  *   mezo_perturb_from:      theta_dst = round(theta_src + scale * z(seed))
  *   mezo_update_multi_from: theta_dst = round(theta_src + sum_k c_k z(seed_k))
  * src is left unchanged. dst and src must describe the same tensors in the
- * same order (per storage type: numel and tensor_id; else MEZO_EINVAL) and
+ * same order (per storage type: numel, tensor_id and first; else MEZO_EINVAL) and
  * share no memory except where a tensor is its own source (MEZO_EOVERLAP);
  * src == dst is the in-place call. Arguments are checked as for the in-place
  * calls. Unlike those, zero weights still enqueue one pass: theta_dst =
@@ -278,7 +289,10 @@ MEZO_API int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src,
  * mod 2^64, fmix64 being MurmurHash3's 64-bit finalizer. The sum does not
  * depend on how tensors are grouped into paramsets or in which order they were
  * registered (the checksum of a model split over several paramsets is the sum
- * of theirs). An MEZO_NF4 tensor's bytes are its ceil(numel / 2) code bytes
+ * of theirs). Chunks are numbered from the start of the logical tensor: a
+ * shard (first > 0) starts at chunk first * sizeof(element) / 8, so the
+ * checksums of a tensor's shards add up to the whole tensor's. An MEZO_NF4
+ * tensor's bytes are its ceil(numel / 2) code bytes
  * zero-padded to a multiple of 8, followed by its absmax values (chunk numbers
  * continue). Written asynchronously to out_dev, a device pointer to 8 bytes
  * (8-byte aligned; MEZO_EINVAL otherwise), on stream. */

@@ -376,7 +376,7 @@ uint64_t tile_of(uint32_t dtype)
     return dtype == MEZO_F32 ? mezo::kTileF32 : (dtype == MEZO_BF16 ? mezo::kTileBF16 : mezo::kTileNF4);
 }
 
-// dst and src describe the same tensors (count, ids, sizes, storage types, in
+// dst and src describe the same tensors (count, ids, sizes, offsets, storage types, in
 // registration order per storage type) and share no memory except where a
 // tensor is its own source.
 int check_pair(const mezo_paramset* dst, const mezo_paramset* src)
@@ -388,7 +388,8 @@ int check_pair(const mezo_paramset* dst, const mezo_paramset* src)
         const auto& b = src->table[dt];
         if (a.size() != b.size()) return MEZO_EINVAL;
         for (size_t i = 0; i < a.size(); ++i) {
-            if (a[i].numel != b[i].numel || a[i].tensor_id != b[i].tensor_id) return MEZO_EINVAL;
+            if (a[i].numel != b[i].numel || a[i].tensor_id != b[i].tensor_id || a[i].first != b[i].first)
+                return MEZO_EINVAL;
             const bool same = b[i].data == a[i].data && b[i].aux == a[i].aux;
             add_spans(a[i].data, a[i].aux, a[i].numel, a[i].dtype, spans);
             if (!same) add_spans(b[i].data, b[i].aux, b[i].numel, b[i].dtype, spans);
@@ -413,6 +414,9 @@ int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* ou
             if (t[i].dtype != MEZO_F32 && t[i].dtype != MEZO_BF16 && t[i].dtype != MEZO_NF4) return MEZO_EDTYPE;
             if (!t[i].data || (reinterpret_cast<uintptr_t>(t[i].data) & 15u)) return MEZO_EINVAL;
             if (t[i].numel == 0 || t[i].numel > MEZO_MAX_NUMEL) return MEZO_EINVAL;
+            // a shard's first element: block-aligned, inside the counter's range
+            if ((t[i].first & 7u) || t[i].first > MEZO_MAX_NUMEL - t[i].numel) return MEZO_EINVAL;
+            if (t[i].dtype == MEZO_NF4 && t[i].first != 0) return MEZO_EINVAL;
             if (t[i].dtype == MEZO_NF4) {
                 if (!t[i].absmax || (reinterpret_cast<uintptr_t>(t[i].absmax) & 15u)) return MEZO_EINVAL;
             } else if (t[i].absmax) {
@@ -436,6 +440,7 @@ int mezo_paramset_create(const mezo_tensor_t* t, uint32_t n, mezo_paramset_t* ou
             d.numel = t[i].numel;
             d.tensor_id = t[i].tensor_id;
             d.dtype = dt;
+            d.first = t[i].first;
             d.tile_begin = ps->total_tiles[dt];
             const uint64_t per = tile_of(dt);
             ps->total_tiles[dt] += (t[i].numel + per - 1) / per;
@@ -739,6 +744,6 @@ const char* mezo_strerror(int code)
 
 const char* mezo_last_error(void) { return t_last_error; }
 
-int mezo_version(void) { return 300; }
+int mezo_version(void) { return 400; }
 
 }  // extern "C"

@@ -124,7 +124,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
 #pragma unroll
             for (int j = 0; j < 4; ++j) th[g][j] = (e0[g] + j < numel) ? in[e0[g] + j] : 0.0f;
         }
-        pre[g] = block_pre(uint32_t(grp));
+        pre[g] = block_pre(uint32_t((d.first >> 2) + grp));  // block of the logical tensor
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[g][j] = 0.0f;
     }
@@ -189,8 +189,9 @@ __device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDes
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         const uint64_t grp = group_index<kGroups>(tile, g);
-        pre[g][0] = block_pre(uint32_t(2 * grp));
-        pre[g][1] = block_pre(uint32_t(2 * grp + 1));
+        const uint64_t blk = (d.first >> 2) + 2 * grp;  // block of the logical tensor
+        pre[g][0] = block_pre(uint32_t(blk));
+        pre[g][1] = block_pre(uint32_t(blk + 1));
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[g][j] = 0.0f;
     }
@@ -408,8 +409,9 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
     float acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-    const BlockPre pre0 = block_pre(uint32_t(e0 >> 2));
-    const BlockPre pre1 = block_pre(uint32_t((e0 >> 2) + 1));
+    const uint64_t blk = (d.first + e0) >> 2;  // block of the logical tensor
+    const BlockPre pre0 = block_pre(uint32_t(blk));
+    const BlockPre pre1 = block_pre(uint32_t(blk + 1));
     const auto accumulate = [&](uint32_t r) {
         const SeedRec& rec = rec_at<kInline>(a, r);
         const SeedUniform u = seed_uniform(rec, d.tensor_id);
@@ -629,11 +631,12 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
         const uint64_t local = tile - d.tile_begin;
         const uint64_t nbytes = d.numel * kEsz;
         const uint64_t nchunks = (nbytes + 7) / 8;
+        const uint64_t cbase = d.first * kEsz / 8;  // chunk number of the shard's first byte
         const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
             const uint64_t grp = group_index<kGroups>(local, g);
-            const uint64_t c0 = grp * 2;  // index of the group's first chunk
+            const uint64_t c0 = grp * 2;  // the group's first chunk within the shard
             if (c0 >= nchunks) continue;
             uint4 v;
             if ((grp + 1) * kPer <= d.numel) {
@@ -656,8 +659,8 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
             }
             const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
             const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
-            sum += fmix64(lo ^ (c0 * kChunkPos) ^ tmix);
-            if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((c0 + 1) * kChunkPos) ^ tmix);
+            sum += fmix64(lo ^ ((cbase + c0) * kChunkPos) ^ tmix);
+            if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((cbase + c0 + 1) * kChunkPos) ^ tmix);
         }
     }
     add_workgroup_sum(sum, a.out);

@@ -29,6 +29,7 @@ struct alignas(16) TensorDesc {
     uint32_t tensor_id;
     uint32_t dtype;       // 0 = fp32, 1 = bf16, 2 = NF4
     uint64_t aux;         // NF4: device address of the per-block absmax values
+    uint64_t first;       // index of element 0 within the logical tensor (a shard's offset)
 };
 
 constexpr uint32_t kF32 = 0u;

@@ -47,7 +47,7 @@ class Seed(ctypes.Structure):
 class Tensor(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("numel", ctypes.c_uint64),
                 ("tensor_id", ctypes.c_uint32), ("dtype", ctypes.c_uint32),
-                ("absmax", ctypes.c_void_p)]
+                ("absmax", ctypes.c_void_p), ("first", ctypes.c_uint64)]
 
 
 class Codec(ctypes.Structure):
@@ -242,12 +242,12 @@ def nf4_dequantize(t: NF4Tensor, dtype=None, out=None, stream=None):
     return out
 
 
-def _tensor_struct(t, tid: int) -> Tensor:
+def _tensor_struct(t, tid: int, first: int = 0) -> Tensor:
     if isinstance(t, NF4Tensor):
-        return Tensor(t.codes.data_ptr(), t.numel(), tid, NF4, t.absmax.data_ptr())
+        return Tensor(t.codes.data_ptr(), t.numel(), tid, NF4, t.absmax.data_ptr(), first)
     if not t.is_cuda or not t.is_contiguous():
         raise ValueError("parameters must be contiguous CUDA tensors")
-    return Tensor(t.data_ptr(), t.numel(), tid, _dtype_code(t), None)
+    return Tensor(t.data_ptr(), t.numel(), tid, _dtype_code(t), None, first)
 
 
 class ParamSet:
@@ -255,11 +255,14 @@ class ParamSet:
     fp32 / bf16 torch tensors or NF4Tensor objects.
 
     ``tensor_ids`` default to the position in ``tensors``; they select each
-    tensor's noise stream and must be the same on every machine.
+    tensor's noise stream and must be the same on every machine. ``firsts``
+    (default all 0) give, for a shard of a tensor split by element range, the
+    index of its first element within the whole tensor (a multiple of 8): the
+    shard then computes exactly those elements of the whole tensor.
     """
 
     def __init__(self, tensors: Sequence, tensor_ids: Iterable[int] | None = None,
-                 gaussian: int = GAUSS_FAST):
+                 gaussian: int = GAUSS_FAST, firsts: Iterable[int] | None = None):
         self.tensors = list(tensors)
         devices = set()
         for t in self.tensors:
@@ -275,9 +278,12 @@ class ParamSet:
         ids = list(range(len(self.tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
         if len(ids) != len(self.tensors):
             raise ValueError("one tensor_id per tensor")
+        offs = [0] * len(self.tensors) if firsts is None else [int(f) for f in firsts]
+        if len(offs) != len(self.tensors):
+            raise ValueError("one first-element offset per tensor")
         arr = (Tensor * max(1, len(self.tensors)))()
-        for i, (t, tid) in enumerate(zip(self.tensors, ids)):
-            arr[i] = _tensor_struct(t, tid)
+        for i, (t, tid, f) in enumerate(zip(self.tensors, ids, offs)):
+            arr[i] = _tensor_struct(t, tid, f)
         h = ctypes.c_void_p()
         _check(lib.mezo_paramset_create(arr, len(self.tensors), ctypes.byref(h)),
                "mezo_paramset_create")

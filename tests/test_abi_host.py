@@ -122,7 +122,7 @@ def create(entries):
     arr = (mezo.Tensor * max(1, len(entries)))()
     for i, e in enumerate(entries):
         ptr, n, tid, dt = e[:4]
-        arr[i] = mezo.Tensor(ptr, n, tid, dt, e[4] if len(e) > 4 else None)
+        arr[i] = mezo.Tensor(ptr, n, tid, dt, e[4] if len(e) > 4 else None, e[5] if len(e) > 5 else 0)
     h = ctypes.c_void_p()
     rc = mezo.lib.mezo_paramset_create(arr, len(entries), ctypes.byref(h))
     return rc, h
@@ -144,11 +144,21 @@ def create(entries):
     ([(0x1000, 16, 0, mezo.NF4, 0x1000)], mezo.EOVERLAP),          # codes and absmax overlap
     ([(0x1000, 260, 0, mezo.NF4, 0x2000), (0x2010, 4, 1, mezo.F32)], mezo.EOVERLAP),  # 5 absmax = 20 B
     ([(0x1000, 33, 0, mezo.NF4, 0x2000), (0x1010, 4, 1, mezo.F32)], mezo.EOVERLAP),   # 17 code bytes
+    ([(0x1000, 16, 0, mezo.F32, None, 4)], mezo.EINVAL),           # shard offset not a multiple of 8
+    ([(0x1000, 16, 0, mezo.F32, None, (1 << 34) - 8)], mezo.EINVAL),  # shard past the counter's range
+    ([(0x1000, 16, 0, mezo.NF4, 0x2000, 64)], mezo.EINVAL),        # NF4 split by whole tensors only
 ])
 def test_paramset_create_rejects(entries, code):
     rc, h = create(entries)
     assert rc == code
     assert not h.value
+
+
+def test_paramset_create_accepts_shards():
+    # the last 16 elements of the counter's range, and a shard at offset 8
+    rc, h = create([(0x1000, 16, 0, mezo.F32, None, (1 << 34) - 16), (0x2000, 8, 1, mezo.BF16, None, 8)])
+    assert rc == mezo.OK
+    mezo.lib.mezo_paramset_destroy(h)
 
 
 def test_paramset_create_accepts_adjacent_and_reports_numel():
@@ -183,8 +193,9 @@ def test_nf4_conversion_argument_checks():
 
 
 def test_tensor_struct_layout():
-    assert ctypes.sizeof(mezo.Tensor) == 32
+    assert ctypes.sizeof(mezo.Tensor) == 40
     assert mezo.Tensor.absmax.offset == 24
+    assert mezo.Tensor.first.offset == 32
 
 
 @pytest.fixture

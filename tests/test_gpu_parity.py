@@ -416,6 +416,60 @@ def test_checksum_full_125m_set(mz, orc):
     torch.cuda.empty_cache()
 
 
+# ---- element-range shards ---------------------------------------------------
+
+SHARD_CUTS = [0, 24000, 50016, 70001]   # multiples of 8; the last shard ragged
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_shards_compute_the_whole_tensors(mz, orc, dtype):
+    """Two tensors split by element range into three shards each, shard k of
+    both in paramset k (what one GPU of a sharded run holds). A perturb, a
+    staged 40-seed update and a replay give on the shards, bit for bit, the
+    whole tensors' result; the shards' checksums add up to the whole set's;
+    and a shard's perturb matches the oracle at its elements' global
+    indices."""
+    n = SHARD_CUTS[-1]
+    hosts = [synth.theta0_tensor((n,), dtype, 5 + i, 0) for i in range(2)]
+    ids = [11, 4]
+    whole_devs, whole = make_set(mz, hosts, ids)
+    shard_devs, shards = [], []
+    for k in range(3):
+        a, b = SHARD_CUTS[k], SHARD_CUTS[k + 1]
+        devs = [to_device(h[a:b].copy()) for h in hosts]
+        shard_devs.append(devs)
+        shards.append(mz.ParamSet(devs, ids, firsts=[a, a]))
+    # one perturb: the middle shard against the oracle at global indices
+    for ps in [whole] + shards:
+        ps.perturb((3, 1, 0), 1e-3)
+    sync()
+    a, b = SHARD_CUTS[1], SHARD_CUTS[2]
+    for i, tid in enumerate(ids):
+        ref = orc.perturb(hosts[i][a:b].copy(), tid, (3, 1, 0), 1e-3, first=a)
+        assert_theta_close(to_host(shard_devs[1][i]), ref, f"shard at {a}", inp=hosts[i][a:b])
+    seeds = synth.seeds(8, 5, step=2)
+    q = synth.grads_int8(40, seed=8)
+    log = [(synth.seeds(4, 2, step=t), synth.grads_int8(8, seed=30 + t), 1e-3) for t in range(3)]
+    for ps in [whole] + shards:
+        ps.update_multi(seeds, q, 1e-3)
+        ps.replay(log)
+    sync()
+    for i in range(len(hosts)):
+        got = np.concatenate([to_host(shard_devs[k][i]) for k in range(3)])
+        assert np.array_equal(got.view(np.uint8), to_host(whole_devs[i]).view(np.uint8))
+    assert sum(ps.checksum() for ps in shards) & 0xFFFFFFFFFFFFFFFF == whole.checksum()
+
+
+def test_shard_offset_is_part_of_the_backup_layout(mz):
+    """The out-of-place calls need the same offsets in source and destination."""
+    h = synth.theta0_tensor((64,), synth.F32, 0, 0)
+    _, a = make_set(mz, [h])
+    b = mz.ParamSet([to_device(h)], [0], firsts=[8])
+    with pytest.raises(mz.MezoError) as e:
+        b.perturb_from(a, (1, 1, 1), 1e-3)
+    assert e.value.code == mz.EINVAL
+
+
 # ---- log edge cases and concurrent callers ---------------------------------
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
