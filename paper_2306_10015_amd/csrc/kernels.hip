@@ -96,11 +96,34 @@ __device__ __forceinline__ void load_tile(const TensorDesc& d, uint64_t src, uin
     }
 }
 
+// A tile that lies wholly inside its tensor (every tile but a tensor's last):
+// no per-lane bounds, and each access is the tile's (uniform) base address
+// plus a 32-bit lane offset.
+template <uint32_t kDtype>
+__device__ __forceinline__ void load_tile_full(uint64_t src, uint64_t tile, TileRaw<Layout<kDtype>::kGroups>& raw)
+{
+    constexpr int kGroups = Layout<kDtype>::kGroups;
+    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(src) + tile * (kThreads * kGroups);
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const u32x4_t v = __builtin_nontemporal_load(base + (uint32_t(g * kThreads) + threadIdx.x));
+        raw.g[g] = make_uint4(v.x, v.y, v.z, v.w);
+    }
+}
+
+template <int kGroups>
+__device__ __forceinline__ void store_group_full(uint64_t dst, uint64_t tile, int g, uint4 v)
+{
+    gu32x4_t* base = reinterpret_cast<gu32x4_t*>(dst) + tile * (kThreads * kGroups);
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, base + (uint32_t(g * kThreads) + threadIdx.x));
+}
+
 // One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
 // (one Philox block each).
 template <bool kInline, bool kPortable>
 __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& d, uint64_t src,
-                                         uint64_t tile, const TileRaw<kGroupsF32>& raw)
+                                         uint64_t tile, bool full, const TileRaw<kGroupsF32>& raw)
 {
     constexpr int kGroups = kGroupsF32;
     const gfloat_t* in = reinterpret_cast<const gfloat_t*>(src);
@@ -115,7 +138,7 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
     for (int g = 0; g < kGroups; ++g) {
         const uint64_t grp = group_index<kGroups>(tile, g);
         e0[g] = grp * 4;
-        if (e0[g] + 4 <= numel) {
+        if (full || e0[g] + 4 <= numel) {
             th[g][0] = __uint_as_float(raw.g[g].x);
             th[g][1] = __uint_as_float(raw.g[g].y);
             th[g][2] = __uint_as_float(raw.g[g].z);
@@ -162,6 +185,14 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
             for (int j = 0; j < 4; ++j) th[g][j] = th[g][j] + acc[g][j];
     }
 
+    if (full) {
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+            store_group_full<kGroups>(d.data, tile, g,
+                                      make_uint4(__float_as_uint(th[g][0]), __float_as_uint(th[g][1]),
+                                                 __float_as_uint(th[g][2]), __float_as_uint(th[g][3])));
+        return;
+    }
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         if (e0[g] + 4 <= numel) {
@@ -237,7 +268,7 @@ __device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDes
 // One tile of a bf16 tensor: each lane owns kGroupsBF16 groups of 8 elements.
 template <bool kInline, bool kPortable>
 __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc& d, uint64_t src,
-                                          uint64_t tile, const TileRaw<kGroupsBF16>& raw)
+                                          uint64_t tile, bool full, const TileRaw<kGroupsBF16>& raw)
 {
     constexpr int kGroups = kGroupsBF16;
     const gu16_t* in = reinterpret_cast<const gu16_t*>(src);
@@ -248,7 +279,7 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         e0[g] = group_index<kGroups>(tile, g) * 8;
-        if (e0[g] + 8 <= numel) {
+        if (full || e0[g] + 8 <= numel) {
             th[g][0] = raw.g[g].x;
             th[g][1] = raw.g[g].y;
             th[g][2] = raw.g[g].z;
@@ -263,6 +294,12 @@ __device__ __forceinline__ void tile_bf16(const EngineArgs& a, const TensorDesc&
         }
     }
     groups_bf16<kInline, kPortable>(a, d, tile, th);
+    if (full) {
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g)
+            store_group_full<kGroups>(d.data, tile, g, make_uint4(th[g][0], th[g][1], th[g][2], th[g][3]));
+        return;
+    }
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         if (e0[g] + 8 <= numel) {
@@ -473,12 +510,18 @@ __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
     } else {
         // out of place: read tensor ti of the source set (same layout), write d
         const uint64_t src = a.src_tensors ? a.src_tensors[ti].data : d.data;
+        const uint64_t local = tile - d.tile_begin;
+        constexpr uint64_t kTileElems = kThreads * Layout<kDtype>::kGroups * Layout<kDtype>::kPerGroup;
+        const bool full = (local + 1) * kTileElems <= d.numel;  // uniform: all but a tensor's last tile
         TileRaw<Layout<kDtype>::kGroups> raw;
-        load_tile<kDtype>(d, src, tile - d.tile_begin, raw);
-        if constexpr (kDtype == kF32)
-            tile_f32<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
+        if (full)
+            load_tile_full<kDtype>(src, local, raw);
         else
-            tile_bf16<kInline, kPortable>(a, d, src, tile - d.tile_begin, raw);
+            load_tile<kDtype>(d, src, local, raw);
+        if constexpr (kDtype == kF32)
+            tile_f32<kInline, kPortable>(a, d, src, local, full, raw);
+        else
+            tile_bf16<kInline, kPortable>(a, d, src, local, full, raw);
     }
 }
 
