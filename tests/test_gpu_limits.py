@@ -86,3 +86,45 @@ def test_max_size_nf4(mz, orc):
     ps.close()
     del codes, absmax
     torch.cuda.empty_cache()
+
+
+def test_generate_across_its_launch_chunks(mz, orc):
+    """mezo_debug_generate splits a range into launches of 2^28 elements: a
+    range starting mid-block just below 2^28 and longer than one launch gives
+    the oracle's words and z at its ends and around the split."""
+    import torch
+    from gpu_util import Z_REL
+    first, count = (1 << 28) - 6, (1 << 28) + 20
+    seed = (2 ** 40 + 3, 9, 4)
+    w, z = mz.debug_generate(seed, 17, first, count)
+    torch.cuda.synchronize()
+    # the start, the split (local element 2^28) and the end, inside [0, count)
+    for a, n in ((0, 64), ((1 << 28) - 32, 48), (count - 64, 64)):
+        assert a + n <= count
+        ww, zz = orc.generate(seed, 17, first + a, n)
+        assert np.array_equal(w[a:a + n].cpu().numpy().view(np.uint32), ww)
+        ref = zz.astype(np.float64)
+        err = np.abs(z[a:a + n].cpu().numpy().astype(np.float64) - ref)
+        assert err.max() <= Z_REL * max(np.abs(ref).max(), 1.0)
+    del w, z
+    torch.cuda.empty_cache()
+
+
+def test_box_muller_across_its_launch_chunks(mz, orc):
+    """mezo_debug_box_muller splits its blocks into launches of 2^26: blocks on
+    both sides of the split match the oracle (the portable transform bit for
+    bit)."""
+    import torch
+    n_blocks = (1 << 26) + 5
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    words = torch.randint(-(1 << 31), 1 << 31, (4 * n_blocks,), dtype=torch.int64, device="cuda",
+                          generator=g).to(torch.int32)
+    z = mz.debug_box_muller(words, mz.GAUSS_PORTABLE)
+    torch.cuda.synchronize()
+    for b0 in (0, (1 << 26) - 3, n_blocks - 4):
+        wb = words[4 * b0:4 * (b0 + 4)].cpu().numpy().view(np.uint32)
+        got = z[4 * b0:4 * (b0 + 4)].cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), orc.box_muller_blocks(wb, portable=True).view(np.uint32))
+    del words, z
+    torch.cuda.empty_cache()
