@@ -50,6 +50,8 @@ HBM_PEAK_GBS = 8000.0
 OPS_LOOP_MS = 30.0
 OPS_MAX_REPS = 400
 OPS_BATCHES = 10
+# projected gradients per machine per iteration in the paper's runs (Section 3)
+SAMPLES_PER_MACHINE = 16
 
 #: VALU instructions per Philox block (4 Gaussians) per seed in the engine's
 #: inner loop, the method's minimal sequence on gfx950: round 1 and the
@@ -399,6 +401,24 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         ops["restore_and_next_perturb"] = entry(
             2, timed(lambda: ps.perturb_multi([(0, 0, 0), (0, 0, 1)], [w.eps, w.eps])))
         ops["update"] = entry(K, timed(lambda: ps.update_multi(seeds_t[0], q0, lr)))
+        # one iteration of Algorithm 1 on one machine without its forward
+        # passes: SAMPLES_PER_MACHINE samples (Section 3: 16 per machine), each
+        # perturbed by -2 eps, the restore of sample j fused with +eps of
+        # sample j + 1, then the K-seed update
+        samples = [(0, 1, j) for j in range(SAMPLES_PER_MACHINE)]
+
+        def iteration():
+            ps.perturb(samples[0], w.eps)
+            for j, s in enumerate(samples):
+                ps.perturb(s, -2 * w.eps)
+                if j + 1 < len(samples):
+                    ps.perturb_multi([s, samples[j + 1]], [w.eps, w.eps])
+                else:
+                    ps.perturb(s, w.eps)
+            ps.update_multi(seeds_t[0], q0, lr)
+        it_records = 1 + SAMPLES_PER_MACHINE + 2 * (SAMPLES_PER_MACHINE - 1) + 1 + K
+        ops["iteration_16_samples"] = entry(it_records, timed(iteration),
+                                            bytes_per_launch * (2 * SAMPLES_PER_MACHINE + 2))
     ops["replay"] = entry(recs["replay"], timed(lambda: ps.replay(log)))
     ck = torch.empty(1, dtype=torch.int64, device="cuda")
     ops["checksum"] = entry(0, timed(lambda: ps.checksum_into(ck)), bytes_per_launch / 2)
