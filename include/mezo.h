@@ -61,6 +61,15 @@
  * a call on a 17th stream first waits on the host for the work of the one
  * used longest ago. mezo_paramset_destroy must not overlap other calls on
  * the same paramset.
+ *
+ * Graph capture. After a paramset's first call (which creates its device
+ * tables), calls that apply at most 32 records, the checksum and the NF4
+ * conversions are plain kernel launches and can be captured into a HIP
+ * graph; every launch of the graph applies the same records again. The
+ * library does not track a graph's launches: synchronize with them before
+ * mezo_paramset_destroy. During capture, a paramset's first call and a
+ * call with more than 32 records (staged through host memory) fail with
+ * MEZO_EINVAL before enqueuing anything.
  */
 #ifndef MEZO_H
 #define MEZO_H

@@ -251,6 +251,25 @@ int ensure_device(mezo_paramset* ps)
     return MEZO_OK;
 }
 
+// Whether work enqueued on stream is being captured into a graph (then it
+// runs only when the graph is launched, possibly many times).
+int capturing(hipStream_t stream, bool& out)
+{
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    MEZO_HIP(hipStreamIsCapturing(stream, &st));
+    out = st != hipStreamCaptureStatusNone;
+    return MEZO_OK;
+}
+
+// A paramset's first call creates its device tables (allocations and
+// copies), which a graph capture cannot record.
+int refuse_first_use_in_capture(const mezo_paramset* ps)
+{
+    if (ps->device >= 0) return MEZO_OK;
+    set_error("a paramset's first call allocates its device tables and cannot be captured into a graph");
+    return MEZO_EINVAL;
+}
+
 // Record that ps's tables are read by work enqueued so far on stream.
 int mark_use(mezo_paramset* ps, hipStream_t stream)
 {
@@ -284,7 +303,21 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
 {
     if (recs.empty() && !src) return MEZO_OK;
     if (recs.size() > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
-    int rc = ensure_device(ps);
+    bool capture = false;
+    int rc = capturing(stream, capture);
+    if (rc) return rc;
+    if (capture) {
+        rc = refuse_first_use_in_capture(ps);
+        if (rc == MEZO_OK && src) rc = refuse_first_use_in_capture(src);
+        if (rc) return rc;
+        if (recs.size() > mezo::kInlineRecs) {
+            // a graph would copy the records from a host slot that later
+            // calls reuse
+            set_error("record lists longer than 32 are staged through host memory and cannot be captured");
+            return MEZO_EINVAL;
+        }
+    }
+    rc = ensure_device(ps);
     if (rc) return rc;
     if (src && src != ps) {
         rc = ensure_device(src);
@@ -339,6 +372,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
         if (e == hipSuccess) e = er;
     }
     if (e != hipSuccess) return hip_fail(e, "engine launch");
+    if (capture) return MEZO_OK;  // a graph's launches are the caller's to wait for
     rc = mark_use(ps, stream);
     if (rc == MEZO_OK && src && src != ps) rc = mark_use(src, stream);
     return rc;
@@ -612,7 +646,12 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
     return guarded("mezo_checksum", [&]() -> int {
         if (!ps || !out_dev || (reinterpret_cast<uintptr_t>(out_dev) & 7u)) return MEZO_EINVAL;
         std::lock_guard<std::mutex> lock(ps->mu);
-        int rc = ensure_device(ps);
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        bool capture = false;
+        int rc = capturing(st, capture);
+        if (rc == MEZO_OK && capture) rc = refuse_first_use_in_capture(ps);
+        if (rc) return rc;
+        rc = ensure_device(ps);
         if (rc) return rc;
         mezo::ChecksumArgs tabs[mezo_paramset::kTypes];
         uint32_t dts[mezo_paramset::kTypes];
@@ -626,10 +665,9 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
             dts[n] = dt;
             ++n;
         }
-        hipStream_t st = static_cast<hipStream_t>(stream);
         MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
                                        ps->device, st));
-        return mark_use(ps, st);
+        return capture ? MEZO_OK : mark_use(ps, st);
     });
 }
 

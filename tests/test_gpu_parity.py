@@ -470,6 +470,47 @@ def test_shard_offset_is_part_of_the_backup_layout(mz):
     assert e.value.code == mz.EINVAL
 
 
+# ---- HIP graph capture ------------------------------------------------------
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")  # the refused capture records nothing
+def test_graph_capture_of_inline_calls(mz):
+    """A perturb, a 4-seed update and a checksum captured into a HIP graph
+    (after the paramset's first call): each of three replays, with eager work
+    and synchronisations in between, applies them again, bit-identical to the
+    same calls made eagerly on a twin set. During capture a staged record
+    list is refused before anything is enqueued."""
+    import torch
+    hosts = [tiny_hosts(synth.F32)[0], tiny_hosts(synth.BF16)[1]]
+    devs, ps = make_set(mz, hosts)
+    twin_devs, twin = make_set(mz, hosts)
+    seeds, q = synth.seeds(4, 1, step=7), synth.grads_int8(4, seed=3)
+    for p in (ps, twin):
+        p.perturb((9, 9, 9), 1e-3)   # the first call creates the device tables
+    ck = torch.zeros(1, dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ps.perturb((1, 2, 3), 1e-3)
+        ps.update_multi(seeds, q, 1e-3)
+        ps.checksum_into(ck)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        g.replay()
+        twin.perturb((1, 2, 3), 1e-3)
+        twin.update_multi(seeds, q, 1e-3)
+        torch.cuda.synchronize()
+        torch.randn(4096, device="cuda").sum().item()   # eager work between replays
+        for d, t in zip(devs, twin_devs):
+            assert torch.equal(d.view(torch.int16), t.view(torch.int16))
+        assert int(ck.item()) & 0xFFFFFFFFFFFFFFFF == twin.checksum()
+    g2 = torch.cuda.CUDAGraph()
+    with pytest.raises(mz.MezoError) as e:
+        with torch.cuda.graph(g2):
+            ps.update_multi(synth.seeds(8, 5), synth.grads_int8(40, seed=1), 1e-3)
+    assert e.value.code == mz.EINVAL
+    torch.cuda.synchronize()
+
+
 # ---- log edge cases and concurrent callers ---------------------------------
 
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
