@@ -269,6 +269,11 @@ def main():
     ps_per_launch = ps_per_step / n_launch
     achieved = ps_per_launch * INSTR_PER_PARAM_SEED / avg_launch_s / 1e12
     peak = VALU_LANE_INSTR_PER_S / 1e12
+    # the step's launches bind differently (the sweeps HBM, the updates the
+    # VALU): its ideal time puts every launch at its own roofline, the larger
+    # of bytes / HBM peak and instructions / VALU peak
+    ideal_ms = 1e3 * sum(max(bytes_per_launch / (HBM_PEAK_GBS * 1e9),
+                             N * recs[c] * INSTR_PER_PARAM_SEED / VALU_LANE_INSTR_PER_S) for c in calls)
     ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args,
                                                recs, proj, seeds_t, log, bytes_per_launch)
 
@@ -301,7 +306,9 @@ def main():
                                f" records, {w.dtype}>",
                      "instr_per_param_seed": INSTR_PER_PARAM_SEED,
                      "param_seeds_per_launch": ps_per_launch,
-                     "avg_launch_ms": avg_launch_s * 1e3},
+                     "avg_launch_ms": avg_launch_s * 1e3,
+                     "step_ideal_ms": ideal_ms,
+                     "combined_frac": ideal_ms / ms_per_step},
         "wall_s_timed": wall,
     }
     if ops is not None:
