@@ -30,11 +30,18 @@ def mz():
     return mezo
 
 
-def test_algorithm1_replicas_late_joiner_and_descent(mz):
+def bits(t):
     import torch
+    return t.view(torch.int16)
+
+
+@pytest.mark.parametrize("storage", ["f32", "bf16"])
+def test_algorithm1_replicas_late_joiner_and_descent(mz, storage):
+    import torch
+    dtype = torch.float32 if storage == "f32" else torch.bfloat16
     rng = np.random.Generator(np.random.PCG64(11))
     targets = [torch.from_numpy(rng.standard_normal(s)).cuda() for s in SHAPES]   # fp64
-    theta0 = [torch.zeros(s, dtype=torch.float32, device="cuda") for s in SHAPES]
+    theta0 = [torch.zeros(s, dtype=dtype, device="cuda") for s in SHAPES]
 
     def loss(ts):
         return sum(float(((t.double() - tg) ** 2).sum()) for t, tg in zip(ts, targets))
@@ -77,13 +84,13 @@ def test_algorithm1_replicas_late_joiner_and_descent(mz):
     theta = replicas[0][0]
     for other, _, _, _ in replicas[1:]:
         for a, b in zip(theta, other):
-            assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+            assert torch.equal(bits(a), bits(b))
     late = [t.clone() for t in theta0]
     joiner = mz.ParamSet(late)
     joiner.replay(log, codec)
     assert joiner.checksum() == replicas[0][2].checksum()
     for a, b in zip(late, theta):
-        assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+        assert torch.equal(bits(a), bits(b))
     ratio = loss(theta) / l0
-    print(f"loss {l0:.1f} -> {loss(theta):.1f} after {STEPS} iterations (ratio {ratio:.4f})")
+    print(f"{storage}: loss {l0:.1f} -> {loss(theta):.1f} after {STEPS} iterations (ratio {ratio:.4f})")
     assert ratio < 0.97
