@@ -95,8 +95,12 @@ def parse():
     p.add_argument("--gaussian", choices=["fast", "portable"], default="fast",
                    help="how z is computed (portable: binary32 operations only, bit-identical "
                         "on any IEEE device)")
-    p.add_argument("--probe", choices=["copy"], default=None,
-                   help="copy: time a plain device copy of the parameter buffer instead")
+    p.add_argument("--probe", choices=["copy", "rmw"], default=None,
+                   help="copy: time a plain device copy of the parameter buffer instead; rmw: an in-place "
+                        "streaming read-modify-write of it with the engine's access pattern (the sweep's "
+                        "memory ceiling)")
+    p.add_argument("--rmw-groups", type=int, choices=[1, 2], default=None,
+                   help="rmw probe: 16-byte groups per lane (default: the engine's, 2 for fp32 and 1 for bf16)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU work of the oracle baseline sample")
     return p.parse_args()
@@ -210,6 +214,9 @@ def main():
             return mezo.ParamSet([b[a:a + n] for a, n in offs], gaussian=gauss), b
     if args.probe == "copy":
         copy_probe(torch, flat, args)
+        return
+    if args.probe == "rmw":
+        rmw_probe(torch, flat, args)
         return
     ps = mezo.ParamSet(views, gaussian=gauss)
     eps, lr = w.eps, w.lr
@@ -438,6 +445,40 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         backup.close()
         del keep
     return ops
+
+
+def rmw_probe(torch, flat, args):
+    """The parameter buffer read and written in place once per pass by
+    libisa_probe.so's stream_rmw (one add per word, the engine's tile shape
+    for the storage type and non-temporal 16-byte accesses): what HBM
+    delivers to a sweep with no RNG work."""
+    import ctypes
+    from paper_2306_10015_amd import build as b
+    L = ctypes.CDLL(str(b.PROBE_LIB))
+    L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_float, ctypes.c_int, ctypes.c_void_p]
+    L.stream_rmw.restype = ctypes.c_int
+    nbytes = (flat.numel() * flat.element_size()) // 16 * 16
+    groups = args.rmw_groups or (2 if flat.element_size() == 4 else 1)  # the engine's fp32 / bf16 tile shapes
+    stream = torch.cuda.current_stream()
+
+    def run(n):
+        for _ in range(n):
+            rc = L.stream_rmw(flat.data_ptr(), nbytes, 0.0, groups, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError(f"stream_rmw failed ({rc})")
+    run(args.warmup)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    run(args.steps)
+    e.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(e) / args.steps
+    moved = 2 * nbytes
+    print(json.dumps({"probe": "rmw", "groups_per_lane": groups, "bytes_per_pass": moved, "ms": ms,
+                      "GBps": moved / (ms / 1e3) / 1e9,
+                      "hbm_frac": moved / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 
 
 def copy_probe(torch, flat, args):

@@ -67,6 +67,29 @@ PROBE_F32(p_sin, asm volatile("v_sin_f32 %0, %0" : "+v"(x[i]));)
 PROBE_F32(p_cos, asm volatile("v_cos_f32 %0, %0" : "+v"(x[i]));)
 PROBE_U32(p_mov, asm volatile("v_mov_b32 %0, %1" : "=v"(x[i]) : "v"(x[(i + 1) % kChains]));)
 
+// In-place streaming read-modify-write with the engine's access pattern: one
+// 256-lane workgroup per tile of kGroups 16-byte groups per lane (fp32: 2,
+// bf16: 1), the groups strided by 256, non-temporal loads and stores, and one
+// add per 32-bit word as the only arithmetic: the memory ceiling of a sweep.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) f32x4_t gf32x4_t;
+
+template <int kGroups>
+__global__ __launch_bounds__(256) void stream_rmw_kernel(uint64_t addr, uint64_t n_groups, float add)
+{
+    gf32x4_t* data = reinterpret_cast<gf32x4_t*>(addr);
+    const uint64_t base = uint64_t(blockIdx.x) * (256 * kGroups);
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const uint64_t i = base + uint64_t(g) * 256 + threadIdx.x;
+        if (i < n_groups) {
+            f32x4_t v = __builtin_nontemporal_load(data + i);
+            v += add;
+            __builtin_nontemporal_store(v, data + i);
+        }
+    }
+}
+
 typedef void (*probe_fn)(uint32_t*, uint32_t);
 
 struct Probe {
@@ -123,4 +146,26 @@ extern "C" __attribute__((visibility("default"))) int isa_probe_run(double* cycl
     if (b) (void)hipEventDestroy(b);
     (void)hipFree(out);
     return rc;
+}
+
+// Enqueue one pass of stream_rmw_kernel<groups_per_lane> (1 or 2) over the
+// first nbytes (a multiple of 16) of data (16-byte aligned device memory) on
+// stream. Returns 0, -1 for bad arguments, or a negative HIP error code.
+extern "C" __attribute__((visibility("default"))) int stream_rmw(void* data, uint64_t nbytes, float add,
+                                                                 int groups_per_lane, void* stream)
+{
+    if (!data || (nbytes & 15u) || (reinterpret_cast<uintptr_t>(data) & 15u)) return -1;
+    if (groups_per_lane != 1 && groups_per_lane != 2) return -1;
+    const uint64_t groups = nbytes / 16;
+    const uint64_t per_tile = 256 * uint64_t(groups_per_lane);
+    const uint64_t tiles = (groups + per_tile - 1) / per_tile;
+    if (tiles == 0 || tiles > 0x7FFFFFFFull) return -1;
+    uint64_t addr = reinterpret_cast<uint64_t>(data);
+    uint64_t n = groups;
+    void* params[] = {&addr, &n, &add};
+    const void* fn = groups_per_lane == 1 ? reinterpret_cast<const void*>(stream_rmw_kernel<1>)
+                                          : reinterpret_cast<const void*>(stream_rmw_kernel<2>);
+    const hipError_t e = hipLaunchKernel(fn, dim3(uint32_t(tiles)), dim3(256), params, 0,
+                                         static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? 0 : -int(e);
 }

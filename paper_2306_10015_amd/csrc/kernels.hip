@@ -9,8 +9,8 @@
 // In place, or out of place from a source set of the same layout (theta =
 // backup + sum c z: the restore of Algorithm 1 fused into the update).
 //
-// Launch shape: one launch per storage type, one workgroup per 2048-element
-// tile; the workgroup finds its tensor with two scalar loads (tile -> tensor
+// Launch shape: one launch per storage type, one workgroup per 4 KiB tile
+// (1024 fp32 or 2048 bf16 elements); the workgroup finds its tensor with two scalar loads (tile -> tensor
 // index -> descriptor). theta streams through with non-temporal 16-byte loads
 // and stores (it is touched once per call, so it should not displace anything
 // in the caches). Per lane, the seed-independent round-1 Philox product of each

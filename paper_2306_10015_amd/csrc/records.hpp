@@ -37,14 +37,14 @@ constexpr uint32_t kBF16 = 1u;
 constexpr uint32_t kNF4 = 2u;
 constexpr uint32_t kStorageTypes = 3u;
 
-// Work decomposition: a workgroup of kThreads lanes handles one tile per
-// iteration; each lane owns a few 16-byte groups of the tile, strided by
-// kThreads groups so that every wave touches one contiguous 1 KiB run per
-// group. A 16-byte group is 4 fp32 elements (one Philox block) or 8 bf16
-// elements (two blocks), so both storage types give every lane two
-// independent Philox blocks per record and 2048-element tiles.
+// Work decomposition: a workgroup of kThreads lanes handles one tile; each
+// lane owns kGroups 16-byte groups of the tile, strided by kThreads groups so
+// that every wave touches one contiguous 1 KiB run per group. A 16-byte group
+// is 4 fp32 elements (one Philox block) or 8 bf16 elements (two blocks). One
+// group per lane (4 KiB tiles: 1024 fp32 or 2048 bf16 elements) streams
+// faster than two: more workgroups in flight per byte.
 constexpr int kThreads = 256;
-constexpr int kGroupsF32 = 2;
+constexpr int kGroupsF32 = 1;
 constexpr int kGroupsBF16 = 1;
 constexpr uint64_t kTileF32 = uint64_t(kThreads) * kGroupsF32 * 4;
 constexpr uint64_t kTileBF16 = uint64_t(kThreads) * kGroupsBF16 * 8;
