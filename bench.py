@@ -100,7 +100,7 @@ def parse():
                         "streaming read-modify-write of it with the engine's access pattern (the sweep's "
                         "memory ceiling)")
     p.add_argument("--rmw-groups", type=int, choices=[1, 2], default=None,
-                   help="rmw probe: 16-byte groups per lane (default: the engine's, 2 for fp32 and 1 for bf16)")
+                   help="rmw probe: 16-byte groups per lane (default 1, the engine's)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU work of the oracle baseline sample")
     return p.parse_args()
@@ -458,7 +458,7 @@ def rmw_probe(torch, flat, args):
     L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_float, ctypes.c_int, ctypes.c_void_p]
     L.stream_rmw.restype = ctypes.c_int
     nbytes = (flat.numel() * flat.element_size()) // 16 * 16
-    groups = args.rmw_groups or (2 if flat.element_size() == 4 else 1)  # the engine's fp32 / bf16 tile shapes
+    groups = args.rmw_groups or 1  # the engine's tile shape: one 16-byte group per lane
     stream = torch.cuda.current_stream()
 
     def run(n):
