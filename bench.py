@@ -101,6 +101,8 @@ def parse():
                         "memory ceiling)")
     p.add_argument("--rmw-groups", type=int, choices=[1, 2], default=None,
                    help="rmw probe: 16-byte groups per lane (default 1, the engine's)")
+    p.add_argument("--rmw-lanes", type=int, choices=[128, 256, 512], default=256,
+                   help="rmw probe: lanes per workgroup (default 256, the engine's)")
     p.add_argument("--cpu-seconds", type=float, default=12.0,
                    help="target CPU work of the oracle baseline sample")
     return p.parse_args()
@@ -455,7 +457,8 @@ def rmw_probe(torch, flat, args):
     import ctypes
     from paper_2306_10015_amd import build as b
     L = ctypes.CDLL(str(b.PROBE_LIB))
-    L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_float, ctypes.c_int, ctypes.c_void_p]
+    L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+                             ctypes.c_void_p]
     L.stream_rmw.restype = ctypes.c_int
     nbytes = (flat.numel() * flat.element_size()) // 16 * 16
     groups = args.rmw_groups or 1  # the engine's tile shape: one 16-byte group per lane
@@ -463,7 +466,7 @@ def rmw_probe(torch, flat, args):
 
     def run(n):
         for _ in range(n):
-            rc = L.stream_rmw(flat.data_ptr(), nbytes, 0.0, groups, stream.cuda_stream)
+            rc = L.stream_rmw(flat.data_ptr(), nbytes, 0.0, groups, args.rmw_lanes, stream.cuda_stream)
             if rc != 0:
                 raise RuntimeError(f"stream_rmw failed ({rc})")
     run(args.warmup)
@@ -476,7 +479,8 @@ def rmw_probe(torch, flat, args):
     torch.cuda.synchronize()
     ms = a.elapsed_time(e) / args.steps
     moved = 2 * nbytes
-    print(json.dumps({"probe": "rmw", "groups_per_lane": groups, "bytes_per_pass": moved, "ms": ms,
+    print(json.dumps({"probe": "rmw", "groups_per_lane": groups, "lanes": args.rmw_lanes, "bytes_per_pass": moved,
+                      "ms": ms,
                       "GBps": moved / (ms / 1e3) / 1e9,
                       "hbm_frac": moved / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 

@@ -74,14 +74,14 @@ PROBE_U32(p_mov, asm volatile("v_mov_b32 %0, %1" : "=v"(x[i]) : "v"(x[(i + 1) % 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(1))) f32x4_t gf32x4_t;
 
-template <int kGroups>
-__global__ __launch_bounds__(256) void stream_rmw_kernel(uint64_t addr, uint64_t n_groups, float add)
+template <int kGroups, int kLanes>
+__global__ __launch_bounds__(kLanes) void stream_rmw_kernel(uint64_t addr, uint64_t n_groups, float add)
 {
     gf32x4_t* data = reinterpret_cast<gf32x4_t*>(addr);
-    const uint64_t base = uint64_t(blockIdx.x) * (256 * kGroups);
+    const uint64_t base = uint64_t(blockIdx.x) * (kLanes * kGroups);
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
-        const uint64_t i = base + uint64_t(g) * 256 + threadIdx.x;
+        const uint64_t i = base + uint64_t(g) * kLanes + threadIdx.x;
         if (i < n_groups) {
             f32x4_t v = __builtin_nontemporal_load(data + i);
             v += add;
@@ -148,24 +148,33 @@ extern "C" __attribute__((visibility("default"))) int isa_probe_run(double* cycl
     return rc;
 }
 
-// Enqueue one pass of stream_rmw_kernel<groups_per_lane> (1 or 2) over the
-// first nbytes (a multiple of 16) of data (16-byte aligned device memory) on
-// stream. Returns 0, -1 for bad arguments, or a negative HIP error code.
+// Enqueue one pass of stream_rmw_kernel<groups_per_lane (1 or 2), lanes (128,
+// 256 or 512 per workgroup)> over the first nbytes (a multiple of 16) of data
+// (16-byte aligned device memory) on stream. Returns 0, -1 for bad arguments,
+// or a negative HIP error code.
 extern "C" __attribute__((visibility("default"))) int stream_rmw(void* data, uint64_t nbytes, float add,
-                                                                 int groups_per_lane, void* stream)
+                                                                 int groups_per_lane, int lanes, void* stream)
 {
     if (!data || (nbytes & 15u) || (reinterpret_cast<uintptr_t>(data) & 15u)) return -1;
     if (groups_per_lane != 1 && groups_per_lane != 2) return -1;
+    if (lanes != 128 && lanes != 256 && lanes != 512) return -1;
     const uint64_t groups = nbytes / 16;
-    const uint64_t per_tile = 256 * uint64_t(groups_per_lane);
+    const uint64_t per_tile = uint64_t(lanes) * uint64_t(groups_per_lane);
     const uint64_t tiles = (groups + per_tile - 1) / per_tile;
     if (tiles == 0 || tiles > 0x7FFFFFFFull) return -1;
     uint64_t addr = reinterpret_cast<uint64_t>(data);
     uint64_t n = groups;
     void* params[] = {&addr, &n, &add};
-    const void* fn = groups_per_lane == 1 ? reinterpret_cast<const void*>(stream_rmw_kernel<1>)
-                                          : reinterpret_cast<const void*>(stream_rmw_kernel<2>);
-    const hipError_t e = hipLaunchKernel(fn, dim3(uint32_t(tiles)), dim3(256), params, 0,
+    const void* fn = nullptr;
+    if (groups_per_lane == 1)
+        fn = lanes == 128 ? reinterpret_cast<const void*>(stream_rmw_kernel<1, 128>)
+           : lanes == 256 ? reinterpret_cast<const void*>(stream_rmw_kernel<1, 256>)
+                          : reinterpret_cast<const void*>(stream_rmw_kernel<1, 512>);
+    else
+        fn = lanes == 128 ? reinterpret_cast<const void*>(stream_rmw_kernel<2, 128>)
+           : lanes == 256 ? reinterpret_cast<const void*>(stream_rmw_kernel<2, 256>)
+                          : reinterpret_cast<const void*>(stream_rmw_kernel<2, 512>);
+    const hipError_t e = hipLaunchKernel(fn, dim3(uint32_t(tiles)), dim3(uint32_t(lanes)), params, 0,
                                          static_cast<hipStream_t>(stream));
     return e == hipSuccess ? 0 : -int(e);
 }
