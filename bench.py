@@ -438,6 +438,19 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         ops["iteration_16_samples"] = entry(it_records, timed(iteration),
                                             bytes_per_launch * (2 * SAMPLES_PER_MACHINE + 2))
     ops["replay"] = entry(recs["replay"], timed(lambda: ps.replay(log)))
+    if w.dtype == synth.NF4:
+        # the standalone conversions on the largest tensor (the embedding): a
+        # QLoRA-style forward pass dequantizes the weights it reads
+        big = max(ps.tensors, key=lambda t: t.numel())
+        n = big.numel()
+        vals = torch.empty(n, dtype=torch.bfloat16, device=big.device)
+        spare = mezo.NF4Tensor.empty(n, big.device)
+        moved = (n + 1) // 2 + 4 * ((n + 63) // 64) + 2 * n
+        ops["nf4_dequantize_to_bf16"] = entry(0, timed(lambda: mezo.nf4_dequantize(big, out=vals, stream=stream)),
+                                              moved)
+        ops["nf4_quantize_from_bf16"] = entry(0, timed(lambda: mezo.nf4_quantize(vals, out=spare, stream=stream)),
+                                              moved)
+        del vals, spare
     ck = torch.empty(1, dtype=torch.int64, device="cuda")
     ops["checksum"] = entry(0, timed(lambda: ps.checksum_into(ck)), bytes_per_launch / 2)
     if w.T == 0:
