@@ -284,7 +284,7 @@ def main():
     ideal_ms = 1e3 * sum(max(bytes_per_launch / (HBM_PEAK_GBS * 1e9),
                              N * recs[c] * INSTR_PER_PARAM_SEED / VALU_LANE_INSTR_PER_S) for c in calls)
     ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args,
-                                               recs, proj, seeds_t, log, bytes_per_launch)
+                                               recs, proj, seeds_t, log, bytes_per_launch, flat)
 
     out = {
         "metric": "param-seed updates/sec (params x K per s)",
@@ -322,6 +322,10 @@ def main():
     }
     if ops is not None:
         out["ops"] = ops
+        if "perturb" in ops and "stream_rmw_no_rng" in ops:
+            # the memory-bound sweep against the same buffer's streaming ceiling
+            out["roofline"]["sweep_frac_of_stream_ceiling"] = (ops["perturb"]["alg_GBps"]
+                                                               / ops["stream_rmw_no_rng"]["alg_GBps"])
         out["issue_cycles_isolated"] = {k: round(v, 3) for k, v in issue_costs().items()}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, recs, calls, log, args.cpu_seconds)
@@ -376,7 +380,7 @@ def measured_traffic(workload: str, gaussian: str = "fast"):
 
 
 def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj, seeds_t, log,
-                bytes_per_launch):
+                bytes_per_launch, flat):
     """Each operation alone, repeated back to back between two events on the
     kernels' stream (after the timed region, not part of the step)."""
     N, K, lr = w.numel, w.K, w.lr
@@ -451,6 +455,11 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         ops["nf4_quantize_from_bf16"] = entry(0, timed(lambda: mezo.nf4_quantize(vals, out=spare, stream=stream)),
                                               moved)
         del vals, spare
+    if w.dtype != synth.NF4:
+        # the sweep's memory ceiling on the same buffer: the same tile shape and
+        # accesses with no RNG work (every bit kept)
+        one, moved = rmw_pass(flat, stream)
+        ops["stream_rmw_no_rng"] = entry(0, timed(one), moved)
     ck = torch.empty(1, dtype=torch.int64, device="cuda")
     ops["checksum"] = entry(0, timed(lambda: ps.checksum_into(ck)), bytes_per_launch / 2)
     if w.T == 0:
@@ -462,26 +471,36 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
     return ops
 
 
-def rmw_probe(torch, flat, args):
-    """The parameter buffer read and written in place once per pass by
-    libisa_probe.so's stream_rmw (one add per word, the engine's tile shape
-    for the storage type and non-temporal 16-byte accesses): what HBM
-    delivers to a sweep with no RNG work."""
+def rmw_pass(flat, stream, groups: int = 1, lanes: int = 256):
+    """A callable enqueuing one pass of libisa_probe.so's stream_rmw over the
+    parameter buffer on stream: read and written in place, an xor with 0 per
+    word (every bit kept), the engine's tile shape by default and non-temporal
+    16-byte accesses; and the bytes it moves."""
     import ctypes
     from paper_2306_10015_amd import build as b
     L = ctypes.CDLL(str(b.PROBE_LIB))
-    L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_float, ctypes.c_int, ctypes.c_int,
+    L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_int,
                              ctypes.c_void_p]
     L.stream_rmw.restype = ctypes.c_int
     nbytes = (flat.numel() * flat.element_size()) // 16 * 16
+
+    def one():
+        rc = L.stream_rmw(flat.data_ptr(), nbytes, 0, groups, lanes, stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"stream_rmw failed ({rc})")
+    return one, 2 * nbytes
+
+
+def rmw_probe(torch, flat, args):
+    """What HBM delivers to a sweep with no RNG work: the parameter buffer
+    through rmw_pass."""
     groups = args.rmw_groups or 1  # the engine's tile shape: one 16-byte group per lane
     stream = torch.cuda.current_stream()
+    one, moved = rmw_pass(flat, stream, groups, args.rmw_lanes)
 
     def run(n):
         for _ in range(n):
-            rc = L.stream_rmw(flat.data_ptr(), nbytes, 0.0, groups, args.rmw_lanes, stream.cuda_stream)
-            if rc != 0:
-                raise RuntimeError(f"stream_rmw failed ({rc})")
+            one()
     run(args.warmup)
     torch.cuda.synchronize()
     a = torch.cuda.Event(enable_timing=True)
@@ -491,7 +510,6 @@ def rmw_probe(torch, flat, args):
     e.record(stream)
     torch.cuda.synchronize()
     ms = a.elapsed_time(e) / args.steps
-    moved = 2 * nbytes
     print(json.dumps({"probe": "rmw", "groups_per_lane": groups, "lanes": args.rmw_lanes, "bytes_per_pass": moved,
                       "ms": ms,
                       "GBps": moved / (ms / 1e3) / 1e9,

@@ -68,23 +68,24 @@ PROBE_F32(p_cos, asm volatile("v_cos_f32 %0, %0" : "+v"(x[i]));)
 PROBE_U32(p_mov, asm volatile("v_mov_b32 %0, %1" : "=v"(x[i]) : "v"(x[(i + 1) % kChains]));)
 
 // In-place streaming read-modify-write with the engine's access pattern: one
-// 256-lane workgroup per tile of kGroups 16-byte groups per lane (fp32: 2,
-// bf16: 1), the groups strided by 256, non-temporal loads and stores, and one
-// add per 32-bit word as the only arithmetic: the memory ceiling of a sweep.
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(1))) f32x4_t gf32x4_t;
+// kLanes-lane workgroup per tile of kGroups 16-byte groups per lane, the
+// groups strided by kLanes, non-temporal loads and stores, and one xor per
+// 32-bit word with a runtime key as the only arithmetic (key 0 leaves every
+// bit as it was): the memory ceiling of a sweep.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) u32x4_t gu32x4_t;
 
 template <int kGroups, int kLanes>
-__global__ __launch_bounds__(kLanes) void stream_rmw_kernel(uint64_t addr, uint64_t n_groups, float add)
+__global__ __launch_bounds__(kLanes) void stream_rmw_kernel(uint64_t addr, uint64_t n_groups, uint32_t key)
 {
-    gf32x4_t* data = reinterpret_cast<gf32x4_t*>(addr);
+    gu32x4_t* data = reinterpret_cast<gu32x4_t*>(addr);
     const uint64_t base = uint64_t(blockIdx.x) * (kLanes * kGroups);
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         const uint64_t i = base + uint64_t(g) * kLanes + threadIdx.x;
         if (i < n_groups) {
-            f32x4_t v = __builtin_nontemporal_load(data + i);
-            v += add;
+            u32x4_t v = __builtin_nontemporal_load(data + i);
+            v ^= key;
             __builtin_nontemporal_store(v, data + i);
         }
     }
@@ -152,7 +153,7 @@ extern "C" __attribute__((visibility("default"))) int isa_probe_run(double* cycl
 // 256 or 512 per workgroup)> over the first nbytes (a multiple of 16) of data
 // (16-byte aligned device memory) on stream. Returns 0, -1 for bad arguments,
 // or a negative HIP error code.
-extern "C" __attribute__((visibility("default"))) int stream_rmw(void* data, uint64_t nbytes, float add,
+extern "C" __attribute__((visibility("default"))) int stream_rmw(void* data, uint64_t nbytes, uint32_t key,
                                                                  int groups_per_lane, int lanes, void* stream)
 {
     if (!data || (nbytes & 15u) || (reinterpret_cast<uintptr_t>(data) & 15u)) return -1;
@@ -164,7 +165,7 @@ extern "C" __attribute__((visibility("default"))) int stream_rmw(void* data, uin
     if (tiles == 0 || tiles > 0x7FFFFFFFull) return -1;
     uint64_t addr = reinterpret_cast<uint64_t>(data);
     uint64_t n = groups;
-    void* params[] = {&addr, &n, &add};
+    void* params[] = {&addr, &n, &key};
     const void* fn = nullptr;
     if (groups_per_lane == 1)
         fn = lanes == 128 ? reinterpret_cast<const void*>(stream_rmw_kernel<1, 128>)
