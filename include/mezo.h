@@ -89,7 +89,9 @@ extern "C" {
 /* ---- return codes ---------------------------------------------------- */
 #define MEZO_OK        0
 #define MEZO_EINVAL   -1  /* null/misaligned pointer, empty or oversized tensor,
-                             duplicated tensor_id, bad count                  */
+                             duplicated tensor_id, bad shard offset, bad
+                             count, a paramset used on another device, a
+                             call that a graph capture cannot record         */
 #define MEZO_EDTYPE   -2  /* unknown storage type                            */
 #define MEZO_EOVERLAP -3  /* two tensors of a paramset share memory          */
 #define MEZO_EORDER   -4  /* seeds of one update not strictly ascending      */
@@ -130,8 +132,11 @@ extern "C" {
  *  PORTABLE: z and the update from IEEE binary32 +, -, *, fma, correctly
  *            rounded / and sqrt only (Appendix B: noise every device
  *            reproduces), so any IEEE machine computes bit-identical z and
- *            weights; about 2.5x the arithmetic of FAST. The steps are listed
- *            in the design notes and mirrored by the CPU reference. */
+ *            weights; about 2.5x the arithmetic of FAST. Per pair of words:
+ *            ln u1 from an exact reduction u1 = m 2^e and the series
+ *            2 atanh((m-1)/(m+1)), r = sqrt(-2 ln u1), and cos/sin of 2 pi u2
+ *            from its octant and Taylor polynomials on [0, pi/4]; every
+ *            coefficient and step is fixed in binary32. */
 #define MEZO_GAUSS_FAST     0u
 #define MEZO_GAUSS_PORTABLE 1u
 
