@@ -20,7 +20,7 @@
  *  - late-joiner catch-up (Appendix B): apply every logged projected gradient
  *    of the missed iterations.
  *
- * Readings where the paper is silent (each restated in the design notes):
+ * Readings where the paper is silent:
  *  - the RNG is Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), keyed by
  *    the machine id, with counter (element>>2, tensor_id, sample, step);
  *  - a Gaussian is Box-Muller on exact 24-bit uniforms, evaluated in fp64 and
