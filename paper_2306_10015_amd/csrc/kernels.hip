@@ -413,7 +413,7 @@ __device__ __forceinline__ uint32_t nf4_nibble_mask(uint32_t valid)
 // Every lane of the wave must call it (the block maximum is exchanged across
 // lanes).
 template <bool kNext>
-__device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, float (&w)[8], uint32_t& packed,
+__device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, float (&w)[8], uint32_t& packed,
                                             float& am)
 {
     float m = 0.0f;
@@ -427,7 +427,7 @@ __device__ __forceinline__ void nf4_requant(const NF4Lds& s, uint32_t valid, flo
         const float x = w[j] * r;
         int b = static_cast<int>(__builtin_fmaf(x, 64.0f, 64.0f));
         b = b < 0 ? 0 : (b > kNF4Bins - 1 ? kNF4Bins - 1 : b);
-        const NF4Bin e = s.bin[b];
+        const NF4Bin e = bins[b];
         const bool up = x > e.mid;
         if constexpr (kNext) w[j] = (up ? e.v_hi : e.v_lo) * m;
         p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
@@ -481,12 +481,12 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
         accumulate(r);
         if (rec_at<kInline>(a, r).last) {
             step_end();
-            nf4_requant<true>(s, valid, w, packed, am);
+            nf4_requant<true>(s.bin, valid, w, packed, am);
         }
     }
     accumulate(a.n_rec - 1);
     step_end();
-    nf4_requant<false>(s, valid, w, packed, am);
+    nf4_requant<false>(s.bin, valid, w, packed, am);
     nf4_store(d.data, d.aux, e0, d.numel, packed, am);
 }
 
@@ -528,7 +528,17 @@ __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
 // Standalone NF4 conversions (one tile of 2048 elements per workgroup).
 __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
 {
-    __shared__ NF4Lds lds;
+    // one copy of the bin table per wave: a wave fills its own and reads it
+    // after its writes (one wave's LDS accesses complete in order), so the
+    // waves of a workgroup never wait for each other
+    __shared__ NF4Bin wave_bins[kThreads / 64][kNF4Bins];
+    NF4Bin* bins = wave_bins[threadIdx.x >> 6];
+    const uint32_t lane = threadIdx.x & 63u;
+    bins[lane] = kNF4Table.bin[lane];
+    bins[lane + 64] = kNF4Table.bin[lane + 64];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
     const uint32_t valid = nf4_valid(e0, a.n);
     float w[8];
@@ -563,24 +573,45 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
                 if ((valid >> j) & 1u) w[j] = __uint_as_float(uint32_t(in[e0 + j]) << 16);
         }
     }
-    nf4_lds_init(lds);
     uint32_t packed;
     float am;
-    nf4_requant<false>(lds, valid, w, packed, am);
+    nf4_requant<false>(bins, valid, w, packed, am);
     nf4_store(a.codes, a.absmax, e0, a.n, packed, am);
+}
+
+// The 16 values held by lanes 0..15 of every wave (lane l: value l mod 16).
+__device__ __forceinline__ uint32_t nf4_value_lanes()
+{
+    return __float_as_uint(kNF4Values[threadIdx.x & 15u]);
+}
+
+// nf4_dequant with the value of each code fetched from the lane that holds it
+// (a lane permute: no LDS table to fill, no workgroup barrier).
+__device__ __forceinline__ void nf4_dequant_lanes(uint32_t table, uint32_t packed, float am, uint32_t valid,
+                                                  float (&w)[8])
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int addr = int(((packed >> (4 * j)) & 15u) << 2);  // byte address of the code's lane
+        w[j] = __uint_as_float(uint32_t(__builtin_amdgcn_ds_bpermute(addr, int(table)))) * am;
+    }
+    if (valid != 0xFFu) {  // a tensor's last lanes only
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
 {
-    __shared__ NF4Lds lds;
     const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
     const uint32_t valid = nf4_valid(e0, a.n);
+    const uint32_t table = nf4_value_lanes();
     uint32_t packed;
     float am;
     nf4_load(a.codes, a.absmax, e0, a.n, packed, am);
-    nf4_lds_init(lds);
     float w[8];
-    nf4_dequant(lds, packed, am, valid, w);
+    nf4_dequant_lanes(table, packed, am, valid, w);
     if (a.dtype == kF32) {
         gfloat_t* out = reinterpret_cast<gfloat_t*>(a.values);
         if (valid == 0xFFu) {
