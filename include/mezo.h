@@ -270,7 +270,12 @@ MEZO_API int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, con
 /* Late-joiner catch-up — Appendix B: apply T logged steps in order, each as
  * mezo_update_multi would (rounding to storage after every step), in one pass
  * over the parameters. Each step is checked as in mezo_update_multi; T = 0
- * enqueues nothing. The result is bit-identical to T mezo_update_multi calls. */
+ * enqueues nothing. The result is bit-identical to T mezo_update_multi calls.
+ * A log of more than 65536 records runs as several passes, split at step ends
+ * (each pass holds at most 65536 records, or one longer step alone); the
+ * result is the same, since every step ends rounded to storage anyway. Logs
+ * longer than 32 records are staged through host memory in a ring of 4
+ * slots: with more passes in flight the call waits on the host for a slot. */
 MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T,
                 const mezo_codec_t* codec, void* stream);
 

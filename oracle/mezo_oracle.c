@@ -11,6 +11,7 @@
 #include "mezo_oracle.h"
 
 #include <math.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -325,13 +326,15 @@ int orc_update(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
 {
     if (!elems_ok(dtype, idx, first, n)) return -1;
     if (K > 0 && (!seeds || !q)) return -1;
-    float c[4096];
-    if (K > 4096) return -1;
+    float* c = (float*)malloc(((size_t)K + 1) * sizeof(float));
+    if (!c) return -1;
     int rc = orc_coefficients(q, K, kind, scale, alpha, lr, c);
-    if (rc) return rc;
     uint32_t live = 0;
-    for (uint32_t k = 0; k < K; ++k) live += (c[k] != 0.0f);
-    if (live == 0) return 0; /* a zero weight perturbs nothing */
+    for (uint32_t k = 0; rc == 0 && k < K; ++k) live += (c[k] != 0.0f);
+    if (rc || live == 0) { /* a zero weight perturbs nothing */
+        free(c);
+        return rc;
+    }
     long long nn = (long long)n;
 #pragma omp parallel for schedule(static)
     for (long long i = 0; i < nn; ++i) {
@@ -344,6 +347,7 @@ int orc_update(void* theta, int dtype, uint32_t tensor_id, const uint64_t* idx,
         double v = load_theta(theta, dtype, (uint64_t)i) + acc;
         store_theta(theta, dtype, (uint64_t)i, v);
     }
+    free(c);
     return 0;
 }
 
@@ -482,13 +486,15 @@ int orc_update_portable(void* theta, int dtype, uint32_t tensor_id, const uint64
 {
     if (!elems_ok(dtype, idx, first, n)) return -1;
     if (K > 0 && (!seeds || !q)) return -1;
-    float c[4096];
-    if (K > 4096) return -1;
+    float* c = (float*)malloc(((size_t)K + 1) * sizeof(float));
+    if (!c) return -1;
     int rc = orc_coefficients(q, K, kind, scale, alpha, lr, c);
-    if (rc) return rc;
     uint32_t live = 0;
-    for (uint32_t k = 0; k < K; ++k) live += (c[k] != 0.0f);
-    if (live == 0) return 0;
+    for (uint32_t k = 0; rc == 0 && k < K; ++k) live += (c[k] != 0.0f);
+    if (rc || live == 0) { /* a zero weight perturbs nothing */
+        free(c);
+        return rc;
+    }
     long long nn = (long long)n;
 #pragma omp parallel for schedule(static)
     for (long long i = 0; i < nn; ++i) {
@@ -501,6 +507,7 @@ int orc_update_portable(void* theta, int dtype, uint32_t tensor_id, const uint64
         float v = load_theta_f32(theta, dtype, (uint64_t)i) + acc;
         store_theta(theta, dtype, (uint64_t)i, (double)v);
     }
+    free(c);
     return 0;
 }
 

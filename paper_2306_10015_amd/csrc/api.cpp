@@ -295,14 +295,26 @@ int mark_use(mezo_paramset* ps, hipStream_t stream)
     return MEZO_OK;
 }
 
+// Records one engine launch applies at most when a call can split its list
+// at step ends (a replay): a long catch-up then runs as launches of bounded
+// length instead of one kernel of arbitrary length.
+constexpr size_t kMaxLaunchRecords = size_t(1) << 16;
+
+// A run of records of a call: [data, data + size).
+struct RecSpan {
+    const mezo::SeedRec* data;
+    size_t size;
+    bool empty() const { return size == 0; }
+};
+
 // Enqueue the engine over every storage type of ps, with the Gaussian the
 // records were made for. With src (same layout), read src and write ps; that
 // launch is made even with no records (a copy).
-int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bool portable, hipStream_t stream,
+int launch_records(mezo_paramset* ps, RecSpan recs, bool portable, hipStream_t stream,
                    mezo_paramset* src = nullptr)
 {
     if (recs.empty() && !src) return MEZO_OK;
-    if (recs.size() > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
+    if (recs.size > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
     bool capture = false;
     int rc = capturing(stream, capture);
     if (rc) return rc;
@@ -310,7 +322,7 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
         rc = refuse_first_use_in_capture(ps);
         if (rc == MEZO_OK && src) rc = refuse_first_use_in_capture(src);
         if (rc) return rc;
-        if (recs.size() > mezo::kInlineRecs) {
+        if (recs.size > mezo::kInlineRecs) {
             // a graph would copy the records from a host slot that later
             // calls reuse
             set_error("record lists longer than 32 are staged through host memory and cannot be captured");
@@ -329,18 +341,18 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
     }
     mezo::EngineArgs args;
     std::memset(&args, 0, sizeof(args));
-    args.n_rec = static_cast<uint32_t>(recs.size());
+    args.n_rec = static_cast<uint32_t>(recs.size);
     mezo_paramset::Slot* slot = nullptr;
-    if (recs.size() <= mezo::kInlineRecs) {
-        std::copy(recs.begin(), recs.end(), args.inl);
+    if (recs.size <= mezo::kInlineRecs) {
+        std::copy(recs.data, recs.data + recs.size, args.inl);
     } else {
         slot = &ps->slots[ps->next_slot++ % mezo_paramset::kSlots];
         if (slot->done)
             MEZO_HIP(hipEventSynchronize(slot->done));
         else
             MEZO_HIP(hipEventCreateWithFlags(&slot->done, hipEventDisableTiming));
-        if (slot->cap < recs.size()) {
-            size_t cap = std::max<size_t>(recs.size(), 2 * slot->cap);
+        if (slot->cap < recs.size) {
+            size_t cap = std::max<size_t>(recs.size, 2 * slot->cap);
             if (slot->host) MEZO_HIP(hipHostFree(slot->host));
             if (slot->dev) MEZO_HIP(hipFree(slot->dev));
             slot->host = nullptr;
@@ -350,8 +362,8 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
             MEZO_HIP(hipMalloc(reinterpret_cast<void**>(&slot->dev), cap * sizeof(mezo::SeedRec)));
             slot->cap = cap;
         }
-        std::memcpy(slot->host, recs.data(), recs.size() * sizeof(mezo::SeedRec));
-        MEZO_HIP(hipMemcpyAsync(slot->dev, slot->host, recs.size() * sizeof(mezo::SeedRec),
+        std::memcpy(slot->host, recs.data, recs.size * sizeof(mezo::SeedRec));
+        MEZO_HIP(hipMemcpyAsync(slot->dev, slot->host, recs.size * sizeof(mezo::SeedRec),
                                 hipMemcpyHostToDevice, stream));
         args.ext = slot->dev;
     }
@@ -376,6 +388,12 @@ int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bo
     rc = mark_use(ps, stream);
     if (rc == MEZO_OK && src && src != ps) rc = mark_use(src, stream);
     return rc;
+}
+
+int launch_records(mezo_paramset* ps, const std::vector<mezo::SeedRec>& recs, bool portable, hipStream_t stream,
+                   mezo_paramset* src = nullptr)
+{
+    return launch_records(ps, RecSpan{recs.data(), recs.size()}, portable, stream, src);
 }
 
 // Byte ranges [begin, end) of device memory a tensor occupies.
@@ -632,12 +650,28 @@ int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const 
         for (uint32_t t = 0; t < T; ++t) total += steps[t].K;
         if (total > UINT32_MAX) return MEZO_ERANGE;  // the kernels count records in 32 bits
         recs.reserve(total);
+        std::vector<size_t> step_ends;  // record count after each step that kept records
         for (uint32_t t = 0; t < T; ++t) {
+            const size_t before = recs.size();
             int rc = append_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr, !portable, recs);
             if (rc) return rc;
+            if (recs.size() > before) step_ends.push_back(recs.size());
         }
+        // launches of at most kMaxLaunchRecords records, split at step ends
+        // (where every step rounds to storage anyway: the result is the same);
+        // a longer single step runs alone
         std::lock_guard<std::mutex> lock(ps->mu);
-        return launch_records(ps, recs, portable, static_cast<hipStream_t>(stream));
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        size_t start = 0, end = 0;
+        for (size_t e : step_ends) {
+            if (e - start > kMaxLaunchRecords && end > start) {
+                int rc = launch_records(ps, RecSpan{recs.data() + start, end - start}, portable, st);
+                if (rc) return rc;
+                start = end;
+            }
+            end = e;
+        }
+        return launch_records(ps, RecSpan{recs.data() + start, end - start}, portable, st);
     });
 }
 

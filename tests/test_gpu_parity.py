@@ -237,6 +237,37 @@ def test_replay_long_log_staged(mz, orc):
     assert np.array_equal(to_host(devs[0]), to_host(devs_seq[0]))
 
 
+def test_replay_split_into_launches_at_step_ends(mz, orc):
+    """A log of more records than one launch takes (65536) runs as several
+    launches split at step ends, and a single step longer than that runs as a
+    launch of its own: the result is bit-identical to the same steps applied
+    one update_multi call at a time, and sampled elements after the long step
+    match the oracle."""
+    n = 1 << 16
+    hosts = [synth.theta0_tensor((n,), synth.F32, 0, 8)]
+    steps = [(synth.seeds(32, 32, step=t), synth.grads_int8(1024, seed=300 + t), 1e-5)
+             for t in range(66)]                       # 67584 records in all
+    devs, ps = make_set(mz, hosts)
+    ps.replay(steps)
+    devs_seq, ps_seq = make_set(mz, hosts)
+    for s, q, lr in steps:
+        ps_seq.update_multi(s, q, lr)
+    sync()
+    assert np.array_equal(to_host(devs[0]).view(np.uint32), to_host(devs_seq[0]).view(np.uint32))
+    long_step = (synth.seeds(70, 1000, step=900), synth.grads_int8(70000, seed=901), 1e-6)
+    tail = [(synth.seeds(4, 4, step=902 + t), synth.grads_int8(16, seed=903 + t), 1e-4) for t in range(3)]
+    idx = np.random.Generator(np.random.PCG64(5)).choice(n, 96, replace=False).astype(np.uint64)
+    before = to_host(devs[0])[idx.astype(np.int64)]
+    ps.replay([tail[0], long_step] + tail[1:])
+    for s, q, lr in [tail[0], long_step] + tail[1:]:
+        ps_seq.update_multi(s, q, lr)
+    sync()
+    got = to_host(devs[0])
+    assert np.array_equal(got.view(np.uint32), to_host(devs_seq[0]).view(np.uint32))
+    ref = orc.replay(before.copy(), 0, [tail[0], long_step] + tail[1:], idx=idx)
+    assert_theta_close(got[idx.astype(np.int64)], ref, "replay with a 70000-record step", inp=before)
+
+
 @pytest.mark.parametrize("case", ["lr0", "q0", "K0", "scale0"])
 def test_identity_cases_bit_exact(mz, case):
     hosts = tiny_hosts(synth.F32)[:2]

@@ -133,6 +133,27 @@ def test_update_equals_sum_of_weighted_gaussians(orc):
     assert np.array_equal(th, want)
 
 
+def test_update_with_many_seeds_equals_sum_of_weighted_gaussians(orc):
+    """More seeds than a small fixed buffer would hold (K = 5000), with the
+    weights of all but a few set to zero: the terms that are left decide the
+    result alone."""
+    n, K = 257, 5000
+    th = theta_f32(n, 6)
+    seeds = synth.seeds(50, 100, step=2)
+    q = np.zeros(K, dtype=np.int8)
+    live = [0, 1234, 4097, 4999]
+    q[live] = [5, -17, 90, -127]
+    lr = 1e-3
+    c = orc.coefficients(q, lr)
+    acc = np.zeros(n, dtype=np.float64)
+    for k in live:
+        _, z = orc.generate(seeds[k], 4, 0, n)
+        acc += np.float64(c[k]) * z.astype(np.float64)
+    want = (th.astype(np.float64) + acc).astype(np.float32)
+    orc.update(th, 4, seeds, q, lr)
+    assert np.array_equal(th, want)
+
+
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 def test_sequential_single_seed_perturbs_equal_fused_update(orc, dtype):
     """Applying each (seed, weight) by PerturbParameters one after another is
