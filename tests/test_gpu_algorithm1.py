@@ -10,7 +10,9 @@ all machines' (seed, byte) records in canonical order from its backup in one
 pass (the fused restore-and-update). Checked: the replicas stay bit-identical
 (ChecksumMatch every iteration), a late joiner that replays the log from the
 starting weights ends bit-identical to them (Appendix B), and the loss falls
-(the sign and scale of the update are those of SPSA descent).
+(the sign and scale of the update are those of SPSA descent). A second test
+drops a machine from the set for some iterations and brings it back through a
+replay of what it missed.
 """
 import numpy as np
 import pytest
@@ -94,3 +96,69 @@ def test_algorithm1_replicas_late_joiner_and_descent(mz, storage):
     ratio = loss(theta) / l0
     print(f"{storage}: loss {l0:.1f} -> {loss(theta):.1f} after {STEPS} iterations (ratio {ratio:.4f})")
     assert ratio < 0.97
+
+
+@pytest.mark.parametrize("storage", ["f32", "bf16"])
+def test_machine_that_drops_out_rejoins_by_replaying_what_it_missed(mz, storage):
+    """Algorithm 1 removes machines that miss the sync from the set whose
+    gradients are applied. Three machines; machine 2 drops out after
+    iteration DROP (the others' apply loop then holds two machines' records,
+    with the learning rate divided by the gradients actually received) and
+    comes back at REJOIN: it replays the iterations it missed from its own
+    last weights (Appendix B) and is then bit-identical to the others, and
+    stays so to the end."""
+    import torch
+    dtype = torch.float32 if storage == "f32" else torch.bfloat16
+    steps, drop, rejoin = 10, 3, 7
+    rng = np.random.Generator(np.random.PCG64(12))
+    targets = [torch.from_numpy(rng.standard_normal(s)).cuda() for s in SHAPES]
+
+    def loss(ts):
+        return sum(float(((t.double() - tg) ** 2).sum()) for t, tg in zip(ts, targets))
+
+    codec = mz.codec(mz.LINEAR, scale=4.0)
+    theta0 = [torch.zeros(s, dtype=dtype, device="cuda") for s in SHAPES]
+    replicas = []
+    for _ in range(3):
+        theta = [t.clone() for t in theta0]
+        backup = [t.clone() for t in theta0]
+        replicas.append((theta, backup, mz.ParamSet(theta), mz.ParamSet(backup)))
+    log = []
+    for step in range(steps):
+        if step == rejoin:
+            theta, backup, ps, _ = replicas[2]
+            ps.replay(log[drop:rejoin], codec)
+            for t, b in zip(theta, backup):
+                b.copy_(t)
+            assert ps.checksum() == replicas[0][2].checksum(), "the rejoined machine differs"
+        active = [0, 1] if drop <= step < rejoin else [0, 1, 2]
+        seeds, q = [], []
+        for m in active:
+            theta, _, ps, _ = replicas[m]
+            g = []
+            for j in range(SAMPLES):
+                s = (m, step, j)
+                ps.perturb(s, EPS)
+                lp = loss(theta)
+                ps.perturb(s, -2 * EPS)
+                lm = loss(theta)
+                ps.perturb(s, EPS)
+                g.append((lp - lm) / (2 * EPS))
+                seeds.append(s)
+            q.extend(mz.quantize_projgrad(np.array(g, dtype=np.float32), codec))
+        q = np.array(q, dtype=np.int8)
+        lr = mz.step_lr(ETA, len(seeds))
+        for m in active:
+            theta, backup, ps, bk = replicas[m]
+            ps.update_multi_from(bk, seeds, q, lr, codec)
+            for t, b in zip(theta, backup):
+                b.copy_(t)
+        log.append((seeds, q, lr))
+        sums = {replicas[m][2].checksum() for m in active}
+        assert len(sums) == 1, f"replicas diverged at iteration {step}"
+        if drop <= step < rejoin:
+            # the absent machine still holds the weights it had when it dropped out
+            assert replicas[2][2].checksum() != replicas[0][2].checksum()
+    for other in replicas[1:]:
+        for a, b in zip(replicas[0][0], other[0]):
+            assert torch.equal(bits(a), bits(b))
