@@ -540,7 +540,8 @@ def copy_probe(torch, flat, args):
 
 def cpu_baseline(w, recs, calls, log, target_s):
     """The oracle, as it stands, on a bounded element sample of the same step:
-    the first elements of tensor 0, sized to about `target_s` of CPU time."""
+    elements 0 .. n-1 of one tensor (tensor_id 0, the workload's value
+    distribution), n sized to about `target_s` of CPU time."""
     import oracle
     from paper_2306_10015_amd import synth
     n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
@@ -585,14 +586,14 @@ def cpu_baseline(w, recs, calls, log, target_s):
     n_full, dt = sized(target_s)
     out = {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,
            "kind": "oracle",
-           "sample": f"first {n_full} elements of tensor 0 through the same step "
+           "sample": f"elements 0..{n_full - 1} of one tensor (id 0) through the same step "
                      f"({seeds_per_elem} param-seeds per element), {dt:.1f} s"}
     # the same oracle on one thread (a shorter sample), for the per-core rate
     oracle.set_threads(1)
     n1, dt1 = sized(max(1.0, target_s / 4))
     oracle.set_threads(n_threads)
     out["value_1_thread"] = n1 * seeds_per_elem / dt1
-    out["sample_1_thread"] = f"first {n1} elements of tensor 0, {dt1:.1f} s"
+    out["sample_1_thread"] = f"elements 0..{n1 - 1} of one tensor (id 0), {dt1:.1f} s"
     return out
 
 
