@@ -693,12 +693,43 @@ __device__ __forceinline__ void add_workgroup_sum(uint64_t sum, unsigned long lo
     }
 }
 
+// One lane's share of a tile that lies wholly inside its tensor (every tile
+// but a tensor's last): no bounds, the tile's scalar base plus a 32-bit lane
+// offset, and chunk numbers as a uniform part plus the lane's constant one.
+template <int kGroups>
+__device__ __forceinline__ uint64_t checksum_full_tile(uint64_t data, uint64_t local, uint64_t cpos_tile,
+                                                       uint64_t tmix, const uint64_t (&cpos_lane)[kGroups])
+{
+    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(data) + local * (kThreads * kGroups);
+    uint64_t sum = 0;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const u32x4_t v = __builtin_nontemporal_load(base + (uint32_t(g * kThreads) + threadIdx.x));
+        const uint64_t p0 = cpos_tile + cpos_lane[g];  // (its first chunk's number) * kChunkPos
+        const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+        const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+        sum += fmix64(lo ^ p0 ^ tmix);
+        sum += fmix64(hi ^ (p0 + kChunkPos) ^ tmix);
+    }
+    return sum;
+}
+
 template <uint32_t kDtype>
 __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
 {
     constexpr int kGroups = Layout<kDtype>::kGroups;
     constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
     constexpr uint64_t kEsz = 16 / kPer;
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kGroups * kPer;
+    // chunk number of a lane's group g within its tile, times kChunkPos
+    uint64_t cpos_lane[kGroups];
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        cpos_lane[g] = 2 * (uint64_t(g) * kThreads + threadIdx.x) * kChunkPos;
+        // opaque from here on: otherwise the compiler folds uniform + lane
+        // constant back into one per-lane 64-bit multiply in every tile
+        asm("" : "+v"(cpos_lane[g]));
+    }
     uint64_t sum = 0;
     for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
         const TensorDesc d = a.tensors[a.tile_tensor[tile]];
@@ -707,6 +738,11 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
         const uint64_t nchunks = (nbytes + 7) / 8;
         const uint64_t cbase = d.first * kEsz / 8;  // chunk number of the shard's first byte
         const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+        if ((local + 1) * kTileElems <= d.numel) {  // uniform
+            const uint64_t cpos_tile = (cbase + 2 * local * (kThreads * kGroups)) * kChunkPos;
+            sum += checksum_full_tile<kGroups>(d.data, local, cpos_tile, tmix, cpos_lane);
+            continue;
+        }
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
             const uint64_t grp = group_index<kGroups>(local, g);
