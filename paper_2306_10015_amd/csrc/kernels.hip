@@ -785,6 +785,13 @@ __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
     constexpr uint32_t kWaves = kThreads / 64;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t lane = threadIdx.x & 63u;
+    // position terms of a lane's chunks within a tile, computed once (opaque
+    // to the compiler, as in checksum_kernel): code chunks 2 lane, 2 lane + 1;
+    // absmax chunk lane (lanes 0..15)
+    uint64_t cpos_code = 2 * uint64_t(lane) * kChunkPos;
+    uint64_t cpos_abs = uint64_t(lane & 15u) * kChunkPos;
+    asm("" : "+v"(cpos_code));
+    asm("" : "+v"(cpos_abs));
     uint64_t sum = 0;
     for (uint64_t tile = uint64_t(blockIdx.x) * kWaves + wave; tile < a.total_tiles;
          tile += uint64_t(gridDim.x) * kWaves) {
@@ -794,6 +801,20 @@ __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
         const uint64_t cchunks = (cbytes + 7) / 8;
         const uint64_t abytes = 4 * ((d.numel + kNF4Block - 1) / kNF4Block);
         const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+        if ((local + 1) * kTileNF4 <= d.numel) {  // uniform: a whole tile, 32 whole blocks
+            const gu32x4_t* codes = reinterpret_cast<const gu32x4_t*>(d.data) + local * 64;
+            const u32x4_t v = __builtin_nontemporal_load(codes + lane);
+            // the tile's 128 absmax bytes as 16 chunks on lanes 0..15; every
+            // lane loads (lane mod 16), so that both loads issue before any mix
+            const MEZO_GLOBAL uint64_t* am = reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.aux) + local * 16;
+            const uint64_t f = __builtin_nontemporal_load(am + (lane & 15u));
+            const uint64_t p0 = 128 * local * kChunkPos + cpos_code;
+            sum += fmix64((uint64_t(v.x) | (uint64_t(v.y) << 32)) ^ p0 ^ tmix);
+            sum += fmix64((uint64_t(v.z) | (uint64_t(v.w) << 32)) ^ (p0 + kChunkPos) ^ tmix);
+            const uint64_t fm = fmix64(f ^ ((cchunks + 16 * local) * kChunkPos + cpos_abs) ^ tmix);
+            sum += lane < 16u ? fm : 0u;
+            continue;
+        }
         // codes: bytes [16u, 16u + 16) = chunks 2u, 2u + 1
         const uint64_t u = local * 64 + lane;
         if (16 * u < cbytes) {
