@@ -330,6 +330,14 @@ __device__ __forceinline__ void nf4_lds_init(NF4Lds& s)
     __syncthreads();
 }
 
+// Whether any lane of the wave misses elements (valid != 0xFF): a uniform
+// test, so that the masking it guards stays a branch that every other wave
+// skips instead of selects that every wave executes.
+__device__ __forceinline__ bool partial_wave(uint32_t valid)
+{
+    return __builtin_amdgcn_ballot_w64(valid != 0xFFu) != 0;
+}
+
 // Which of a lane's 8 elements e0 .. e0 + 7 exist (bit j for element e0 + j).
 __device__ __forceinline__ uint32_t nf4_valid(uint64_t e0, uint64_t numel)
 {
@@ -376,7 +384,7 @@ __device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, fl
 {
 #pragma unroll
     for (int j = 0; j < 8; ++j) w[j] = s.val[(packed >> (4 * j)) & 15u] * am;
-    if (valid != 0xFFu) {  // a tensor's last lanes only
+    if (partial_wave(valid)) {  // only the wave holding a tensor's last elements
 #pragma unroll
         for (int j = 0; j < 8; ++j)
             if (!((valid >> j) & 1u)) w[j] = 0.0f;
@@ -432,7 +440,7 @@ __device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, 
         if constexpr (kNext) w[j] = (up ? e.v_hi : e.v_lo) * m;
         p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
     }
-    packed = p & nf4_nibble_mask(valid);
+    packed = partial_wave(valid) ? p & nf4_nibble_mask(valid) : p;
     am = m;
 }
 
@@ -465,7 +473,7 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
             w[j] = w[j] + acc[j];
             acc[j] = 0.0f;
         }
-        if (valid != 0xFFu) {  // a tensor's last lanes only
+        if (partial_wave(valid)) {  // only the wave holding a tensor's last elements
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 if (!((valid >> j) & 1u)) w[j] = 0.0f;
