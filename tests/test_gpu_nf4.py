@@ -141,13 +141,16 @@ def compare_step(nf4, got, start, n, tid, apply, exact, what, blocks=None):
     return {"codes_differing": int(mism.size), "absmax_err": aerr}
 
 
-SET_SIZES = [1, 65, 4097, 70001, 64 * 300]
+# the last tiles: wave 0 partial (1, 65, 4097, 70001); waves 0 whole and 1
+# partial (64 * 300); waves 0-2 whole and a lane in the middle of wave 3
+# partial (2048 + 1536 + 8 * 40 + 3)
+SET_SIZES = [1, 65, 4097, 70001, 64 * 300, 2048 + 1536 + 8 * 40 + 3]
 
 
 @pytest.mark.parametrize("portable", [True, False])
 def test_perturb_triple_and_updates(mz, orc, nf4, portable):
     import torch
-    dev, ids = nf4_set(mz, SET_SIZES, seed=1, ids=[5, 0, 17, 3, 1 << 20])
+    dev, ids = nf4_set(mz, SET_SIZES, seed=1, ids=[5, 0, 17, 3, 1 << 20, 9])
     ps = mz.ParamSet(dev, ids, gaussian=mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST)
     eps = 1e-3
     s = (7, 2, 1)
