@@ -346,14 +346,16 @@ __device__ __forceinline__ uint32_t nf4_valid(uint64_t e0, uint64_t numel)
     return (1u << uint32_t(numel - e0)) - 1u;
 }
 
-// A lane's code dword and its block's absmax (zeros past the end).
+// A lane's code dword and its block's absmax (zeros past the end). kFull:
+// the lane's 8 elements are known to exist (a tile wholly inside its tensor).
+template <bool kFull = false>
 __device__ __forceinline__ void nf4_load(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
                                          uint32_t& packed, float& am)
 {
     packed = 0u;
     am = 0.0f;
-    if (e0 >= numel) return;
-    if (e0 + 8 <= numel) {
+    if (!kFull && e0 >= numel) return;
+    if (kFull || e0 + 8 <= numel) {
         packed = __builtin_nontemporal_load(reinterpret_cast<const MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
     } else {
         const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
@@ -364,11 +366,12 @@ __device__ __forceinline__ void nf4_load(uint64_t codes, uint64_t absmax, uint64
     am = reinterpret_cast<const gfloat_t*>(absmax)[e0 / kNF4Block];
 }
 
+template <bool kFull = false>
 __device__ __forceinline__ void nf4_store(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
                                           uint32_t packed, float am)
 {
-    if (e0 >= numel) return;
-    if (e0 + 8 <= numel) {
+    if (!kFull && e0 >= numel) return;
+    if (kFull || e0 + 8 <= numel) {
         __builtin_nontemporal_store(packed, reinterpret_cast<MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
     } else {
         MEZO_GLOBAL uint8_t* b = reinterpret_cast<MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
@@ -444,11 +447,13 @@ __device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, 
     am = m;
 }
 
-template <bool kInline, bool kPortable>
+// kFull: a tile wholly inside its tensor, where every lane's 8 elements exist
+// (no masks, no bounds).
+template <bool kInline, bool kPortable, bool kFull>
 __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& d, uint64_t e0, uint32_t packed,
                                          float am, const NF4Lds& s)
 {
-    const uint32_t valid = nf4_valid(e0, d.numel);
+    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, d.numel);
     float w[8];
     nf4_dequant(s, packed, am, valid, w);
     float acc[8];
@@ -480,7 +485,7 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
         }
     };
     if (a.n_rec == 0) {  // out of place with nothing to apply: a copy
-        nf4_store(d.data, d.aux, e0, d.numel, packed, am);
+        nf4_store<kFull>(d.data, d.aux, e0, d.numel, packed, am);
         return;
     }
     // every record list ends a step with its last record, which is peeled off
@@ -495,10 +500,14 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
     accumulate(a.n_rec - 1);
     step_end();
     nf4_requant<false>(s.bin, valid, w, packed, am);
-    nf4_store(d.data, d.aux, e0, d.numel, packed, am);
+    nf4_store<kFull>(d.data, d.aux, e0, d.numel, packed, am);
 }
 
-template <bool kInline, uint32_t kDtype, bool kPortable>
+// kShort (NF4 only): a call of at most two records, where the per-tile work
+// outweighs the record loop; whole tiles then take a copy of the path compiled
+// without bounds or masks. Long record lists keep a single copy of the loop
+// (a second one costs the loop more than the tiles gain).
+template <bool kInline, uint32_t kDtype, bool kPortable, bool kShort = false>
 __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
@@ -509,12 +518,19 @@ __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
         // out of place: read tensor ti of the source set (same layout), write d
         const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
         const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
-        const uint64_t e0 = (tile - d.tile_begin) * kTileNF4 + threadIdx.x * 8u;
+        const uint64_t local = tile - d.tile_begin;
+        const uint64_t e0 = local * kTileNF4 + threadIdx.x * 8u;
         uint32_t packed;
         float am;
-        nf4_load(codes, absmax, e0, d.numel, packed, am);
-        nf4_lds_init(lds);
-        tile_nf4<kInline, kPortable>(a, d, e0, packed, am, lds);
+        if (kShort && (local + 1) * kTileNF4 <= d.numel) {  // uniform: all but a tensor's last tile
+            nf4_load<true>(codes, absmax, e0, d.numel, packed, am);
+            nf4_lds_init(lds);
+            tile_nf4<kInline, kPortable, true>(a, d, e0, packed, am, lds);
+        } else {
+            nf4_load(codes, absmax, e0, d.numel, packed, am);
+            nf4_lds_init(lds);
+            tile_nf4<kInline, kPortable, false>(a, d, e0, packed, am, lds);
+        }
     } else {
         // out of place: read tensor ti of the source set (same layout), write d
         const uint64_t src = a.src_tensors ? a.src_tensors[ti].data : d.data;
@@ -891,6 +907,9 @@ hipError_t launch_dtype(const EngineArgs& args, uint32_t dtype, dim3 g, dim3 b, 
 {
     if (dtype == kF32) return launch1(engine_kernel<kInline, kF32, kPortable>, g, b, stream, args);
     if (dtype == kBF16) return launch1(engine_kernel<kInline, kBF16, kPortable>, g, b, stream, args);
+    if constexpr (kInline) {
+        if (args.n_rec <= 2) return launch1(engine_kernel<kInline, kNF4, kPortable, true>, g, b, stream, args);
+    }
     return launch1(engine_kernel<kInline, kNF4, kPortable>, g, b, stream, args);
 }
 }  // namespace
