@@ -549,28 +549,17 @@ __global__ __launch_bounds__(kThreads) void engine_kernel(EngineArgs a)
     }
 }
 
-// Standalone NF4 conversions (one tile of 2048 elements per workgroup).
-__global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
+// One lane's 8 elements of nf4_quantize_kernel; kFull: they all exist.
+template <bool kFull>
+__device__ __forceinline__ void nf4_quantize_tile(const NF4ConvArgs& a, const NF4Bin* bins, uint64_t e0)
 {
-    // one copy of the bin table per wave: a wave fills its own and reads it
-    // after its writes (one wave's LDS accesses complete in order), so the
-    // waves of a workgroup never wait for each other
-    __shared__ NF4Bin wave_bins[kThreads / 64][kNF4Bins];
-    NF4Bin* bins = wave_bins[threadIdx.x >> 6];
-    const uint32_t lane = threadIdx.x & 63u;
-    bins[lane] = kNF4Table.bin[lane];
-    bins[lane + 64] = kNF4Table.bin[lane + 64];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
-    const uint32_t valid = nf4_valid(e0, a.n);
+    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, a.n);
     float w[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) w[j] = 0.0f;
     if (a.dtype == kF32) {
         const gfloat_t* in = reinterpret_cast<const gfloat_t*>(a.values);
-        if (valid == 0xFFu) {
+        if (kFull || valid == 0xFFu) {
             const uint4 v0 = load_stream(a.values + e0 * 4);
             const uint4 v1 = load_stream(a.values + e0 * 4 + 16);
             const uint32_t u[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
@@ -583,7 +572,7 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
         }
     } else {
         const gu16_t* in = reinterpret_cast<const gu16_t*>(a.values);
-        if (valid == 0xFFu) {
+        if (kFull || valid == 0xFFu) {
             const uint4 v = load_stream(a.values + e0 * 2);
             const uint32_t u[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -600,7 +589,28 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
     uint32_t packed;
     float am;
     nf4_requant<false>(bins, valid, w, packed, am);
-    nf4_store(a.codes, a.absmax, e0, a.n, packed, am);
+    nf4_store<kFull>(a.codes, a.absmax, e0, a.n, packed, am);
+}
+
+// Standalone NF4 conversions (one tile of 2048 elements per workgroup).
+__global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
+{
+    // one copy of the bin table per wave: a wave fills its own and reads it
+    // after its writes (one wave's LDS accesses complete in order), so the
+    // waves of a workgroup never wait for each other
+    __shared__ NF4Bin wave_bins[kThreads / 64][kNF4Bins];
+    NF4Bin* bins = wave_bins[threadIdx.x >> 6];
+    const uint32_t lane = threadIdx.x & 63u;
+    bins[lane] = kNF4Table.bin[lane];
+    bins[lane + 64] = kNF4Table.bin[lane + 64];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
+    if ((uint64_t(blockIdx.x) + 1) * kTileNF4 <= a.n)  // uniform: every tile but the last
+        nf4_quantize_tile<true>(a, bins, e0);
+    else
+        nf4_quantize_tile<false>(a, bins, e0);
 }
 
 // The 16 values held by lanes 0..15 of every wave (lane l: value l mod 16).
@@ -626,19 +636,20 @@ __device__ __forceinline__ void nf4_dequant_lanes(uint32_t table, uint32_t packe
     }
 }
 
-__global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
+// One lane's 8 elements of nf4_dequantize_kernel; kFull: they all exist.
+template <bool kFull>
+__device__ __forceinline__ void nf4_dequantize_tile(const NF4ConvArgs& a, uint64_t e0)
 {
-    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
-    const uint32_t valid = nf4_valid(e0, a.n);
+    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, a.n);
     const uint32_t table = nf4_value_lanes();
     uint32_t packed;
     float am;
-    nf4_load(a.codes, a.absmax, e0, a.n, packed, am);
+    nf4_load<kFull>(a.codes, a.absmax, e0, a.n, packed, am);
     float w[8];
     nf4_dequant_lanes(table, packed, am, valid, w);
     if (a.dtype == kF32) {
         gfloat_t* out = reinterpret_cast<gfloat_t*>(a.values);
-        if (valid == 0xFFu) {
+        if (kFull || valid == 0xFFu) {
             store_stream(a.values + e0 * 4, make_uint4(__float_as_uint(w[0]), __float_as_uint(w[1]),
                                                        __float_as_uint(w[2]), __float_as_uint(w[3])));
             store_stream(a.values + e0 * 4 + 16, make_uint4(__float_as_uint(w[4]), __float_as_uint(w[5]),
@@ -650,7 +661,7 @@ __global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
         }
     } else {
         gu16_t* out = reinterpret_cast<gu16_t*>(a.values);
-        if (valid == 0xFFu) {
+        if (kFull || valid == 0xFFu) {
             store_stream(a.values + e0 * 2, make_uint4(pack_bf16(w[0], w[1]), pack_bf16(w[2], w[3]),
                                                        pack_bf16(w[4], w[5]), pack_bf16(w[6], w[7])));
         } else {
@@ -659,6 +670,15 @@ __global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
                 if ((valid >> j) & 1u) out[e0 + j] = to_bf16(w[j]);
         }
     }
+}
+
+__global__ __launch_bounds__(kThreads) void nf4_dequantize_kernel(NF4ConvArgs a)
+{
+    const uint64_t e0 = uint64_t(blockIdx.x) * kTileNF4 + threadIdx.x * 8u;
+    if ((uint64_t(blockIdx.x) + 1) * kTileNF4 <= a.n)  // uniform: every tile but the last
+        nf4_dequantize_tile<true>(a, e0);
+    else
+        nf4_dequantize_tile<false>(a, e0);
 }
 
 // Inspection: RNG words and Gaussians of a range of elements, one Philox
