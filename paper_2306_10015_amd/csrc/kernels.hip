@@ -330,9 +330,10 @@ __device__ __forceinline__ void nf4_lds_init(NF4Lds& s)
     __syncthreads();
 }
 
-// Whether any lane of the wave misses elements (valid != 0xFF): a uniform
-// test, so that the masking it guards stays a branch that every other wave
-// skips instead of selects that every wave executes.
+// Whether any lane of the wave misses elements (valid != 0xFF; only waves
+// that reach a tensor's end): a uniform test, so that the masking it guards
+// stays a branch that every other wave skips instead of selects that every
+// wave executes.
 __device__ __forceinline__ bool partial_wave(uint32_t valid)
 {
     return __builtin_amdgcn_ballot_w64(valid != 0xFFu) != 0;
@@ -387,7 +388,7 @@ __device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, fl
 {
 #pragma unroll
     for (int j = 0; j < 8; ++j) w[j] = s.val[(packed >> (4 * j)) & 15u] * am;
-    if (partial_wave(valid)) {  // only the wave holding a tensor's last elements
+    if (partial_wave(valid)) {  // only waves that reach a tensor's end
 #pragma unroll
         for (int j = 0; j < 8; ++j)
             if (!((valid >> j) & 1u)) w[j] = 0.0f;
@@ -478,7 +479,7 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
             w[j] = w[j] + acc[j];
             acc[j] = 0.0f;
         }
-        if (partial_wave(valid)) {  // only the wave holding a tensor's last elements
+        if (partial_wave(valid)) {  // only waves that reach a tensor's end
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 if (!((valid >> j) & 1u)) w[j] = 0.0f;
