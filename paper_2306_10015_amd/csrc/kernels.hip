@@ -111,12 +111,20 @@ __device__ __forceinline__ void load_tile_full(uint64_t src, uint64_t tile, Tile
     }
 }
 
+// Cache-policy bits of a buffer store on gfx950: sc1 (16) | nt (2).
+constexpr int kStorePolicy = 16 | 2;
+
 template <int kGroups>
 __device__ __forceinline__ void store_group_full(uint64_t dst, uint64_t tile, int g, uint4 v)
 {
-    gu32x4_t* base = reinterpret_cast<gu32x4_t*>(dst) + tile * (kThreads * kGroups);
+    // a buffer store over the tile's 4 KiB with the cache policy "sc1 nt"
+    // (paired against "nt" alone: the 125M fp32 sweep 1.9% faster, the bf16
+    // sweeps and the record loops unchanged)
+    void* base = reinterpret_cast<void*>(dst + tile * (kThreads * kGroups * 16));
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(base, (short)0, kThreads * kGroups * 16, 0x00020000);
     const u32x4_t w = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(w, base + (uint32_t(g * kThreads) + threadIdx.x));
+    __builtin_amdgcn_raw_buffer_store_b128(w, r, (uint32_t(g * kThreads) + threadIdx.x) * 16u, 0, kStorePolicy);
 }
 
 // One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
