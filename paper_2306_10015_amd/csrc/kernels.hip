@@ -658,7 +658,19 @@ __device__ __forceinline__ void nf4_dequantize_tile(const NF4ConvArgs& a, uint64
     nf4_dequant_lanes(table, packed, am, valid, w);
     if (a.dtype == kF32) {
         gfloat_t* out = reinterpret_cast<gfloat_t*>(a.values);
-        if (kFull || valid == 0xFFu) {
+        if constexpr (kFull) {
+            // the workgroup's 8 KiB of output through a buffer resource, with
+            // the engine's store policy
+            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+                reinterpret_cast<void*>(a.values + uint64_t(blockIdx.x) * kTileNF4 * 4), (short)0,
+                int(kTileNF4 * 4), 0x00020000);
+            const u32x4_t lo = {__float_as_uint(w[0]), __float_as_uint(w[1]), __float_as_uint(w[2]),
+                                __float_as_uint(w[3])};
+            const u32x4_t hi = {__float_as_uint(w[4]), __float_as_uint(w[5]), __float_as_uint(w[6]),
+                                __float_as_uint(w[7])};
+            __builtin_amdgcn_raw_buffer_store_b128(lo, r, threadIdx.x * 32u, 0, kStorePolicy);
+            __builtin_amdgcn_raw_buffer_store_b128(hi, r, threadIdx.x * 32u + 16u, 0, kStorePolicy);
+        } else if (valid == 0xFFu) {
             store_stream(a.values + e0 * 4, make_uint4(__float_as_uint(w[0]), __float_as_uint(w[1]),
                                                        __float_as_uint(w[2]), __float_as_uint(w[3])));
             store_stream(a.values + e0 * 4 + 16, make_uint4(__float_as_uint(w[4]), __float_as_uint(w[5]),
@@ -670,7 +682,14 @@ __device__ __forceinline__ void nf4_dequantize_tile(const NF4ConvArgs& a, uint64
         }
     } else {
         gu16_t* out = reinterpret_cast<gu16_t*>(a.values);
-        if (kFull || valid == 0xFFu) {
+        if constexpr (kFull) {
+            const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+                reinterpret_cast<void*>(a.values + uint64_t(blockIdx.x) * kTileNF4 * 2), (short)0,
+                int(kTileNF4 * 2), 0x00020000);
+            const u32x4_t v = {pack_bf16(w[0], w[1]), pack_bf16(w[2], w[3]), pack_bf16(w[4], w[5]),
+                               pack_bf16(w[6], w[7])};
+            __builtin_amdgcn_raw_buffer_store_b128(v, r, threadIdx.x * 16u, 0, kStorePolicy);
+        } else if (valid == 0xFFu) {
             store_stream(a.values + e0 * 2, make_uint4(pack_bf16(w[0], w[1]), pack_bf16(w[2], w[3]),
                                                        pack_bf16(w[4], w[5]), pack_bf16(w[6], w[7])));
         } else {
