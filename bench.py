@@ -1,27 +1,29 @@
 """Throughput of the seeded perturbation engine on one MI355X.
 
-One step is one pass of the whole hot path over a synthetic OPT-125m-shaped
-fp32 parameter set (123,581,952 elements in 123 tensors, N(0, 0.02)):
+One step is one pass of the whole hot path over a synthetic OPT-6.7B-shaped
+parameter set in bf16 storage (6,648,897,536 elements in 323 tensors,
+N(0, 0.02); fp32 arithmetic):
 
   1. PerturbParameters +eps, -2eps, +eps with this machine's seed
      (Algorithm 1, inner inference loop; eps = 1e-3);
-  2. quantize_projgrad of the K = 8 projected gradients of the iteration
+  2. quantize_projgrad of the K = 64 projected gradients of the iteration
      (Section 3, one byte each; linear code, scale 1/127);
-  3. update_multi: the fused apply loop over the K = 8 (machine, sample)
+  3. update_multi: the fused apply loop over the K = 64 (machine, sample)
      seeds (Algorithm 1; lr = 1e-6);
   4. replay: a late joiner's catch-up over a log of T = 4 earlier iterations
-     of K = 8 seeds each (Appendix B).
+     of K = 64 seeds each (Appendix B).
 
 Every parameter is read and written once per call; z is regenerated in
 registers. The metric is param-seed updates per second: elements x seeds
 applied, summed over the step's calls, divided by the time of the step.
 
-Prints ONE JSON line. Also reports, for the engine kernel (the only kernel of
-the step), the ALU roofline fraction against 256 CUs x 4 SIMDs x 16 lanes x
-2.4 GHz = 39.3e12 lane-instructions/s, each call timed alone (`ops`), and the
-CPU oracle timed on a bounded sample of the same step.
+Prints ONE JSON line with the engine kernel's ALU roofline (the step is
+RNG-bound: its ceiling is the VALU issue rate of the instructions that make z,
+below), each call timed alone (`ops`), the memory-bound perturb sweep of the
+OPT-125m-shaped fp32 set (`secondary`) and the CPU oracle timed on a bounded
+sample of the same step (`cpu_baseline`).
 
-    python bench.py [--gpus 1] [--steps 400] [--warmup 100] [--workload NAME]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload NAME]
                     [--gaussian fast|portable] [--no-ops] [--no-cpu-baseline]
 """
 from __future__ import annotations
@@ -39,11 +41,14 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-#: VALU issue capacity of one MI355X: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-#: = 39.3e12 lane-instructions per second (a wave64 VALU instruction occupies a
-#: 16-lane SIMD for 4 cycles when issued singly). It is the published
-#: 157.3 TFLOP/s fp32 vector peak / (2 flops per fma x 2 lanes per packed op).
-#: gfx950 can dual-issue some VALU instructions, so a kernel can exceed it.
+#: VALU issue ceiling of one MI355X for the engine's instruction stream:
+#: every non-transcendental VALU instruction of a wave64 occupies its 16-lane
+#: SIMD for 4 cycles, so 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12
+#: lane-instructions per second; transcendentals (log, sqrt, sin, cos) issue
+#: on a unit of their own beside them (their 2 per param-seed take 2 x 8
+#: cycles per wave on it, less than the 13.5 x 4 of the rest), so they add no
+#: time at the ceiling. The counters agree: the dual-issue share of the
+#: engine's VALU cycles (14-15%) is its transcendental share (8 of 62).
 CLOCK_GHZ = 2.4
 VALU_LANE_INSTR_PER_S = 256 * 4 * 16 * CLOCK_GHZ * 1e9
 HBM_PEAK_GBS = 8000.0
@@ -69,29 +74,34 @@ INNER_LOOP_MIX = {
     "v_cvt_f32_u32": 4, "v_fmamk_f32": 2, "v_mul_f32": 4, "v_log_f32": 2, "v_sqrt_f32": 2,
     "v_sin_f32": 2, "v_cos_f32": 2, "v_fmac_f32": 4,
 }
-#: lane-instructions per param-seed (= 62 / 4)
+TRANSCENDENTAL = ("v_log_f32", "v_sqrt_f32", "v_sin_f32", "v_cos_f32")
+#: lane-instructions per param-seed (= 62 / 4), and the non-transcendental
+#: ones that bound the issue rate (= 54 / 4)
 INSTR_PER_PARAM_SEED = sum(INNER_LOOP_MIX.values()) / 4.0
+NONTRANS_PER_PARAM_SEED = sum(v for k, v in INNER_LOOP_MIX.items() if k not in TRANSCENDENTAL) / 4.0
+#: the ceiling in param-seeds per second
+PARAM_SEED_PEAK = VALU_LANE_INSTR_PER_S / NONTRANS_PER_PARAM_SEED
 
-#: counter profile of the engine kernel on this workload (FETCH_SIZE /
-#: WRITE_SIZE per dispatch, calibrated against a plain copy); its traffic is
-#: reported only while the kernel sources it was taken on are unchanged.
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_{workload}_traffic.json")
-KERNEL_SOURCES = ["paper_2306_10015_amd/csrc/kernels.hip", "paper_2306_10015_amd/csrc/engine.hpp",
-                  "paper_2306_10015_amd/csrc/records.hpp", "paper_2306_10015_amd/csrc/nf4.hpp",
-                  "paper_2306_10015_amd/csrc/launch.hpp"]
+#: counter profile of the engine kernel on a workload (traffic per dispatch,
+#: VALU counters), quoted only while the kernel's sources are the ones it was
+#: taken on
+PROFILE = os.path.join(ROOT, "profiles", "engine_kernel_{workload}.json")
+ENGINE_UNIT = {"f32": "engine_dense.hip", "bf16": "engine_dense.hip", "nf4": "engine_nf4.hip"}
 
 T_REPLAY = 4
+SECONDARY_WORKLOAD = "opt125m"
 
 
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=400)
-    p.add_argument("--warmup", type=int, default=100)
-    p.add_argument("--workload", default="opt125m")
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="opt6.7b")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-ops", action="store_true",
-                   help="skip the per-operation measurements after the timed region (profiling runs)")
+                   help="skip the per-operation and secondary measurements after the timed region "
+                        "(profiling runs)")
     p.add_argument("--gaussian", choices=["fast", "portable"], default="fast",
                    help="how z is computed (portable: binary32 operations only, bit-identical "
                         "on any IEEE device)")
@@ -103,14 +113,11 @@ def parse():
                    help="rmw probe: 16-byte groups per lane (default 1, the engine's)")
     p.add_argument("--rmw-lanes", type=int, choices=[128, 256, 512], default=256,
                    help="rmw probe: lanes per workgroup (default 256, the engine's)")
-    p.add_argument("--cpu-seconds", type=float, default=12.0,
-                   help="target CPU work of the oracle baseline sample")
     return p.parse_args()
 
 
 def flat_views(torch, w, device):
     """One 256-byte-aligned allocation holding every tensor of the set."""
-    import math
     esz = 4 if w.dtype == "f32" else 2
     align = 256 // esz
     offs, total = [], 0
@@ -127,7 +134,6 @@ def flat_views(torch, w, device):
 def nf4_buffers(torch, mezo, synth, w, device):
     """4-bit storage of every tensor as views into one code buffer and one
     absmax buffer (each view 256-byte aligned)."""
-    import math
     offs, ctot, atot = [], 0, 0
     for _, shape in w.shapes:
         n = int(math.prod(shape))
@@ -151,11 +157,33 @@ def storage_bytes(w) -> float:
     return {"f32": 4.0, "bf16": 2.0, "nf4": 0.5 + 4.0 / 64}[w.dtype]
 
 
+def fill_dense(torch, synth, w, views, dev):
+    """theta0 ~ N(0, 0.02) of a dense set, resident in HBM."""
+    if w.numel <= 200_000_000:
+        # numpy PCG64 per tensor (the same theta0 the tests and the oracle use)
+        for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
+            h = synth.theta0_tensor(shape, w.dtype, i, 0)
+            if w.dtype == "f32":
+                v.copy_(torch.from_numpy(h))
+            else:
+                v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
+    else:
+        # billions of elements: the same law drawn in HBM by torch's seeded generator
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        for v in views:
+            tmp = torch.empty(v.numel(), dtype=torch.float32, device=dev)
+            tmp.normal_(0.0, 0.02, generator=g)
+            v.copy_(tmp)
+            del tmp
+
+
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: the engine has no multi-GPU path "
-              f"(--gpus {args.gpus} requested). Run with --gpus 1.", file=sys.stderr)
+        print(f"bench.py measures one GPU: the engine's path is the kernel on one GPU's share of the "
+              f"parameters, with no collectives (--gpus {args.gpus} requested). Run with --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -175,7 +203,6 @@ def main():
         codes, absmax, views_of = nf4_buffers(torch, mezo, synth, w, dev)
         views = views_of(codes, absmax)
         if N <= 200_000_000:
-            # numpy PCG64 per tensor (the same storage the tests start from)
             for i, v in enumerate(views):
                 p, a = synth.nf4_theta0_tensor(v.numel(), i, 0)
                 v.codes.copy_(torch.from_numpy(p))
@@ -193,23 +220,7 @@ def main():
             return mezo.ParamSet(views_of(c2, a2), gaussian=gauss), (c2, a2)
     else:
         flat, views, offs = flat_views(torch, w, dev)
-        if N <= 200_000_000:
-            # numpy PCG64 per tensor (the same theta0 the tests and the oracle use)
-            for i, (v, (_, shape)) in enumerate(zip(views, w.shapes)):
-                h = synth.theta0_tensor(shape, w.dtype, i, 0)
-                if w.dtype == "f32":
-                    v.copy_(torch.from_numpy(h))
-                else:
-                    v.copy_(torch.from_numpy(h.view(np.int16)).view(torch.bfloat16))
-        else:
-            # billions of elements: N(0, 0.02) drawn in HBM by torch's seeded generator
-            g = torch.Generator(device=dev)
-            g.manual_seed(0)
-            for v in views:
-                tmp = torch.empty(v.numel(), dtype=torch.float32, device=dev)
-                tmp.normal_(0.0, 0.02, generator=g)
-                v.copy_(tmp)
-                del tmp
+        fill_dense(torch, synth, w, views, dev)
 
         def make_backup():
             b = flat.clone()
@@ -252,6 +263,7 @@ def main():
     torch.cuda.synchronize()
 
     # ---- timed region: exactly `steps` steps ---------------------------------
+    # HIP events on the stream every kernel of the step is enqueued on
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -271,20 +283,56 @@ def main():
     # Engine kernel: every call of the step is one launch of it (per storage
     # type; the sets here have one). Its average launch duration is the timed
     # region's GPU time over its launches (the step enqueues nothing else on
-    # the stream); achieved ALU work = param-seeds x minimal lane-instructions
-    # per param-seed over that time.
+    # the stream but the record lists' 8 KiB copies); achieved = param-seeds x
+    # the non-transcendental lane-instructions per param-seed over that time.
     n_launch = len(calls)
     avg_launch_s = ms_per_step / n_launch / 1e3
     ps_per_launch = ps_per_step / n_launch
-    achieved = ps_per_launch * INSTR_PER_PARAM_SEED / avg_launch_s / 1e12
+    achieved = ps_per_launch * NONTRANS_PER_PARAM_SEED / avg_launch_s / 1e12
     peak = VALU_LANE_INSTR_PER_S / 1e12
-    # the step's launches bind differently (the sweeps HBM, the updates the
-    # VALU): its ideal time puts every launch at its own roofline, the larger
-    # of bytes / HBM peak and instructions / VALU peak
-    ideal_ms = 1e3 * sum(max(bytes_per_launch / (HBM_PEAK_GBS * 1e9),
-                             N * recs[c] * INSTR_PER_PARAM_SEED / VALU_LANE_INSTR_PER_S) for c in calls)
-    ops = None if args.no_ops else measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args,
-                                               recs, proj, seeds_t, log, bytes_per_launch, flat)
+    # the step's launches bind differently (a sweep can be memory-bound, the
+    # updates are VALU-bound): its ideal time puts every launch at its own
+    # roofline, the larger of bytes / HBM peak and param-seeds / ALU peak
+    ideal_ms = 1e3 * sum(max(bytes_per_launch / (HBM_PEAK_GBS * 1e9), N * recs[c] / PARAM_SEED_PEAK)
+                         for c in calls)
+    prof = engine_profile(w, args.gaussian)
+    roofline = {"bound": "alu", "achieved": achieved, "peak": peak,
+                "unit": "Tinstr/s", "frac": achieved / peak,
+                "traffic": prof["hbm_bytes_per_dispatch"] if prof and "hbm_bytes_per_dispatch" in prof else None,
+                "alg_bytes_per_launch": bytes_per_launch,
+                "kernel": f"engine_kernel<{w.dtype}> ("
+                          + ", ".join(f"{recs[c]} record{'s' if recs[c] > 1 else ''}" for c in calls)
+                          + " per launch)",
+                "peak_basis": "non-transcendental VALU issue: 256 CU x 4 SIMD x 16 lanes x 2.4 GHz; "
+                              "transcendentals co-issue on their own unit",
+                "instr_per_param_seed": NONTRANS_PER_PARAM_SEED,
+                "instr_per_param_seed_with_transcendentals": INSTR_PER_PARAM_SEED,
+                "param_seed_peak": PARAM_SEED_PEAK,
+                "param_seeds_per_launch": ps_per_launch,
+                "avg_launch_ms": avg_launch_s * 1e3,
+                "step_ideal_ms": ideal_ms,
+                "combined_frac": ideal_ms / ms_per_step}
+    if prof and "valu_by_records" in prof:
+        # counters of the same kernel sources: the largest record count is the
+        # update or replay, where z is nearly all the work
+        vr = prof["valu_by_records"]
+        kmax = max(vr, key=int)
+        roofline["counters"] = {
+            "profile": os.path.relpath(PROFILE.format(workload=w.name), ROOT),
+            "records": int(kmax),
+            "valu_busy_pct": vr[kmax]["busy_pct"],
+            "dual_issue_pct": vr[kmax]["dual_issue_pct"],
+            "valu_instr_per_param_seed": vr[kmax]["instr_per_param_seed"],
+            "nontrans_instr_per_param_seed": vr[kmax]["instr_per_param_seed"] - vr[kmax]["trans_per_param_seed"],
+            "by_records": {r: {"valu_busy_pct": round(v["busy_pct"], 1),
+                               "valu_instr_per_param_seed": round(v["instr_per_param_seed"], 3)}
+                           for r, v in vr.items()}}
+    ops = secondary = None
+    if not args.no_ops:
+        ops = measure_ops(torch, mezo, synth, w, ps, make_backup, stream, recs, proj, seeds_t, log,
+                          bytes_per_launch, flat)
+        if w.name != SECONDARY_WORKLOAD and args.gaussian == "fast":
+            secondary = measure_secondary(torch, mezo, synth, dev, stream)
 
     out = {
         "metric": "param-seed updates/sec (params x K per s)",
@@ -307,84 +355,46 @@ def main():
                    "storage": w.dtype,
                    "gaussian": args.gaussian,
                    "eps": eps, "lr": lr, "param_seeds_per_step": ps_per_step},
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": peak,
-                     "unit": "Tinstr/s", "frac": achieved / peak,
-                     "traffic": measured_traffic(w.name, args.gaussian),
-                     "alg_bytes_per_launch": bytes_per_launch,
-                     "kernel": f"engine_kernel<{'inline' if max(recs[c] for c in calls) <= 32 else 'staged'}"
-                               f" records, {w.dtype}>",
-                     "instr_per_param_seed": INSTR_PER_PARAM_SEED,
-                     "param_seeds_per_launch": ps_per_launch,
-                     "avg_launch_ms": avg_launch_s * 1e3,
-                     "step_ideal_ms": ideal_ms,
-                     "combined_frac": ideal_ms / ms_per_step},
+        "roofline": roofline,
         "wall_s_timed": wall,
     }
     if ops is not None:
         out["ops"] = ops
         if "perturb" in ops and "stream_rmw_no_rng" in ops:
-            # the memory-bound sweep against the same buffer's streaming ceiling
             out["roofline"]["sweep_frac_of_stream_ceiling"] = (ops["perturb"]["alg_GBps"]
                                                                / ops["stream_rmw_no_rng"]["alg_GBps"])
-        out["issue_cycles_isolated"] = {k: round(v, 3) for k, v in issue_costs().items()}
+    if secondary is not None:
+        out["secondary"] = secondary
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, recs, calls, log, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, recs, calls, log)
         out["gpu_over_cpu"] = value / out["cpu_baseline"]["value"]
     print(json.dumps(out))
 
 
-def issue_costs() -> dict:
-    """SIMD cycles per wave instruction of each instruction of the inner loop in
-    isolation, measured now on this device by libisa_probe.so (8 waves per
-    SIMD, 8 independent chains per lane): context for the instruction mix."""
-    import ctypes
-    from paper_2306_10015_amd import build as b
-    if not b.PROBE_LIB.exists():
-        raise RuntimeError(f"{b.PROBE_LIB} is not built")
-    L = ctypes.CDLL(str(b.PROBE_LIB))
-    L.isa_probe_count.restype = ctypes.c_int
-    L.isa_probe_name.restype = ctypes.c_char_p
-    L.isa_probe_name.argtypes = [ctypes.c_int]
-    L.isa_probe_run.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_double]
-    n = L.isa_probe_count()
-    out = (ctypes.c_double * n)()
-    rc = L.isa_probe_run(out, CLOCK_GHZ)
-    if rc != 0:
-        raise RuntimeError(f"isa_probe_run failed ({rc})")
-    return {L.isa_probe_name(i).decode(): float(out[i]) for i in range(n)}
-
-
-def kernel_source_hash() -> str:
-    import hashlib
-    h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()
-
-
-def measured_traffic(workload: str, gaussian: str = "fast"):
-    """HBM bytes per engine launch from the committed counter profile of this
-    workload, or None when there is none or the kernel sources changed since
-    it was taken."""
+def engine_profile(w, gaussian: str):
+    """The committed counter profile of the engine kernel on this workload,
+    or None when there is none or the kernel's sources changed since it was
+    taken."""
     if gaussian != "fast":
         return None
+    from paper_2306_10015_amd import profile_summary
     try:
-        with open(TRAFFIC_PROFILE.format(workload=workload)) as f:
+        with open(PROFILE.format(workload=w.name)) as f:
             prof = json.load(f)
     except (OSError, ValueError):
         return None
-    if prof.get("kernel_source_sha256") != kernel_source_hash():
+    unit = ENGINE_UNIT[w.dtype]
+    if prof.get("kernel_unit") != unit or prof.get("kernel_source_sha256") != profile_summary.source_hash(unit):
         return None
-    return prof["hbm_bytes_per_dispatch"]
+    return prof
 
 
-def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj, seeds_t, log,
-                bytes_per_launch, flat):
-    """Each operation alone, repeated back to back between two events on the
-    kernels' stream (after the timed region, not part of the step)."""
-    N, K, lr = w.numel, w.K, w.lr
-
+def timer(torch, stream):
+    """timed(fn): the average duration of one call of fn (enqueuing work on
+    stream), from batches of back-to-back calls between two events on the
+    stream: each batch lasts about OPS_LOOP_MS, so that short calls are timed
+    over many launches at the clock a long run settles at; the median of
+    OPS_BATCHES batches."""
     def loop(fn, reps):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
@@ -396,14 +406,20 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
         return a.elapsed_time(b) / reps
 
     def timed(fn):
-        # warm up, then batches of about OPS_LOOP_MS so that short calls are
-        # timed over many launches at the clock a long run settles at; the
-        # median batch's average launch
         fn()
         torch.cuda.synchronize()
         once = loop(fn, 1)
         reps = max(1, min(OPS_MAX_REPS, math.ceil(OPS_LOOP_MS / max(once, 1e-3))))
         return statistics.median(loop(fn, reps) for _ in range(OPS_BATCHES))
+    return timed
+
+
+def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, recs, proj, seeds_t, log,
+                bytes_per_launch, flat):
+    """Each operation alone, repeated back to back between two events on the
+    kernels' stream (after the timed region, not part of the step)."""
+    N, K, lr = w.numel, w.K, w.lr
+    timed = timer(torch, stream)
 
     def entry(records, ms, nbytes=bytes_per_launch):
         t_s = ms / 1e3
@@ -411,7 +427,7 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
              "hbm_frac": nbytes / t_s / 1e9 / HBM_PEAK_GBS}
         if records:
             e.update({"records": records, "param_seeds_per_s": N * records / t_s,
-                      "alu_frac": N * records * INSTR_PER_PARAM_SEED / t_s / VALU_LANE_INSTR_PER_S})
+                      "alu_frac": N * records / t_s / PARAM_SEED_PEAK})
         return e
 
     q0 = mezo.quantize_projgrad(proj[0])
@@ -471,13 +487,43 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, args, recs, proj
     return ops
 
 
+def measure_secondary(torch, mezo, synth, dev, stream):
+    """The memory-bound regime in the same run: the perturb sweep (one record)
+    of the OPT-125m-shaped fp32 set against 8 TB/s and against an in-place
+    streaming read-modify-write of the same buffer without RNG; its checksum
+    (a read-only stream)."""
+    w = synth.WORKLOADS[SECONDARY_WORKLOAD]
+    flat, views, _ = flat_views(torch, w, dev)
+    fill_dense(torch, synth, w, views, dev)
+    ps = mezo.ParamSet(views)
+    timed = timer(torch, stream)
+    nbytes = 2 * w.numel * storage_bytes(w)
+    ms = timed(lambda: ps.perturb((0, 0, 0), w.eps))
+    one, moved = rmw_pass(flat, stream)
+    ms_rmw = timed(one)
+    ck = torch.empty(1, dtype=torch.int64, device="cuda")
+    ms_ck = timed(lambda: ps.checksum_into(ck))
+    ps.close()
+    gbps = nbytes / (ms / 1e3) / 1e9
+    rmw_gbps = moved / (ms_rmw / 1e3) / 1e9
+    ck_gbps = nbytes / 2 / (ms_ck / 1e3) / 1e9
+    return {"workload": f"{w.name}: {w.numel} f32 params in {w.n_tensors} tensors",
+            "perturb_sweep": {"ms": round(ms, 4), "alg_GBps": gbps, "hbm_frac": gbps / HBM_PEAK_GBS,
+                              "frac_of_stream_ceiling": gbps / rmw_gbps},
+            "stream_rmw_no_rng": {"ms": round(ms_rmw, 4), "alg_GBps": rmw_gbps,
+                                  "hbm_frac": rmw_gbps / HBM_PEAK_GBS},
+            "checksum": {"ms": round(ms_ck, 4), "alg_GBps": ck_gbps, "hbm_frac": ck_gbps / HBM_PEAK_GBS}}
+
+
 def rmw_pass(flat, stream, groups: int = 1, lanes: int = 256):
-    """A callable enqueuing one pass of libisa_probe.so's stream_rmw over the
-    parameter buffer on stream: read and written in place, an xor with 0 per
-    word (every bit kept), the engine's tile shape by default and non-temporal
-    16-byte accesses; and the bytes it moves."""
+    """A callable enqueuing one pass of libstream_probe.so's stream_rmw over
+    the parameter buffer on stream: read and written in place, an xor with 0
+    per word (every bit kept), the engine's tile shape by default and
+    non-temporal 16-byte accesses; and the bytes it moves."""
     import ctypes
     from paper_2306_10015_amd import build as b
+    if not b.PROBE_LIB.exists():
+        raise RuntimeError(f"{b.PROBE_LIB} is not built")
     L = ctypes.CDLL(str(b.PROBE_LIB))
     L.stream_rmw.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int, ctypes.c_int,
                              ctypes.c_void_p]
@@ -538,62 +584,89 @@ def copy_probe(torch, flat, args):
                       "hbm_frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 
 
-def cpu_baseline(w, recs, calls, log, target_s):
-    """The oracle, as it stands, on a bounded element sample of the same step:
-    elements 0 .. n-1 of one tensor (tensor_id 0, the workload's value
-    distribution), n sized to about `target_s` of CPU time."""
+def host_cores():
+    """The host cores this process may use, and how many of them the oracle
+    runs on: all of them, unless OMP_NUM_THREADS (the GPU machine's share of
+    its host for one GPU, set by its environment) says fewer."""
+    nproc = os.cpu_count() or 1
+    affinity = sorted(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else list(range(nproc))
+    threads = len(affinity)
+    omp = os.environ.get("OMP_NUM_THREADS", "")
+    if omp.isdigit() and int(omp) > 0:
+        threads = min(threads, int(omp))
+    return threads, {"nproc": nproc, "affinity": len(affinity),
+                     "affinity_cpus": f"{affinity[0]}-{affinity[-1]}" if affinity else "",
+                     "omp_num_threads": omp or None}
+
+
+def sample_step(w, recs, calls, log, idx, tids, vals, rounds: int = 1):
+    """The oracle through the bench's step on sampled elements: each tensor's
+    values at its indices, in place; returns the seconds it took."""
     import oracle
     from paper_2306_10015_amd import synth
-    n_threads = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    n_threads = min(n_threads, 16)
-    oracle.set_threads(n_threads)
     seeds = synth.seeds(w.machines, w.samples_per_machine, step=0)
     q = synth.grads_int8(w.K, "uniform", seed=1)
+    t0 = time.perf_counter()
+    for _ in range(rounds):
+        for tid, ix, th in zip(tids, idx, vals):
+            if w.T == 0:
+                oracle.perturb(th, tid, (0, 0, 0), w.eps, idx=ix)
+                oracle.perturb(th, tid, (0, 0, 0), -2 * w.eps, idx=ix)
+                oracle.perturb(th, tid, (0, 0, 0), w.eps, idx=ix)
+                oracle.update(th, tid, seeds, q, w.lr, idx=ix)
+            oracle.replay(th, tid, log, idx=ix)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(w, recs, calls, log):
+    """The oracle, as it stands, on a bounded sample of the same step: the
+    first and last `edge` elements of every tensor plus random 4-aligned
+    blocks (PCG64 seed 2), with N(0, 0.02) values in the workload's storage;
+    on every host core the process may use, then on one thread (a smaller
+    sample)."""
+    import oracle
+    from paper_2306_10015_amd import synth
+    if w.dtype == synth.NF4:
+        raise SystemExit("the CPU baseline covers the fp32/bf16 workloads (use --no-cpu-baseline)")
+    threads, cores = host_cores()
     seeds_per_elem = sum(recs[c] for c in calls)
 
-    def run(n):
-        if w.dtype == synth.NF4:
-            from oracle import nf4
-            p, a = synth.nf4_theta0_tensor(n, 0, 0)
-            c = nf4.unpack(p, n)
-            t0 = time.perf_counter()
-            if w.T == 0:
-                c, a = nf4.perturb(c, a, 0, (0, 0, 0), w.eps)
-                c, a = nf4.perturb(c, a, 0, (0, 0, 0), -2 * w.eps)
-                c, a = nf4.perturb(c, a, 0, (0, 0, 0), w.eps)
-                c, a = nf4.update(c, a, 0, seeds, q, w.lr)
-            nf4.replay(c, a, 0, log)
-            return time.perf_counter() - t0
-        th = synth.theta0_tensor((n,), w.dtype, 0, 0)
-        t0 = time.perf_counter()
-        if w.T == 0:
-            oracle.perturb(th, 0, (0, 0, 0), w.eps)
-            oracle.perturb(th, 0, (0, 0, 0), -2 * w.eps)
-            oracle.perturb(th, 0, (0, 0, 0), w.eps)
-            oracle.update(th, 0, seeds, q, w.lr)
-        oracle.replay(th, 0, log)
-        return time.perf_counter() - t0
+    def make(edge, blocks):
+        rng = np.random.Generator(np.random.PCG64(2))
+        idx, vals = [], []
+        for tid, (_, shape) in enumerate(w.shapes):
+            ix = synth.sample_indices(int(np.prod(shape)), rng, edge=edge, blocks=blocks)
+            x = rng.standard_normal(size=ix.size, dtype=np.float32) * np.float32(0.02)
+            idx.append(ix)
+            vals.append(x if w.dtype == synth.F32 else synth.bf16_bits_truncated(x))
+        return idx, list(range(w.n_tensors)), vals
 
-    def sized(seconds):
-        n = 1 << 10
-        dt = run(n)
-        while dt < 0.5 and n < w.numel:
-            n *= 4
-            dt = run(n)
-        n_full = int(min(max(n * seconds / max(dt, 1e-6), n), w.numel))
-        return n_full, run(n_full)
-
-    n_full, dt = sized(target_s)
-    out = {"value": n_full * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": n_threads,
-           "kind": "oracle",
-           "sample": f"elements 0..{n_full - 1} of one tensor (id 0) through the same step "
-                     f"({seeds_per_elem} param-seeds per element), {dt:.1f} s"}
-    # the same oracle on one thread (a shorter sample), for the per-core rate
+    # all cores: first/last 4096 elements of every tensor + 2^16 blocks over
+    # the set (spread in proportion to the tensors' sizes)
+    blocks = [max(1, round(65536 * int(np.prod(s)) / w.numel)) for _, s in w.shapes]
+    oracle.set_threads(threads)
+    rng = np.random.Generator(np.random.PCG64(2))
+    idx, vals = [], []
+    for tid, ((_, shape), nb) in enumerate(zip(w.shapes, blocks)):
+        ix = synth.sample_indices(int(np.prod(shape)), rng, edge=4096, blocks=nb)
+        x = rng.standard_normal(size=ix.size, dtype=np.float32) * np.float32(0.02)
+        idx.append(ix)
+        vals.append(x if w.dtype == synth.F32 else synth.bf16_bits_truncated(x))
+    n_el = sum(ix.size for ix in idx)
+    dt = sample_step(w, recs, calls, log, idx, list(range(w.n_tensors)), vals)
+    out = {"value": n_el * seeds_per_elem / dt, "unit": "param-seeds/s", "cores": threads,
+           "kind": "oracle", "host": cores,
+           "sample": f"{n_el} elements: the first and last 4096 of each of the {w.n_tensors} tensors and "
+                     f"{sum(blocks)} random 4-aligned blocks, through the same step ({seeds_per_elem} "
+                     f"param-seeds per element), {dt:.1f} s on {threads} threads"}
+    # one thread, on the first and last 256 elements of every tensor
     oracle.set_threads(1)
-    n1, dt1 = sized(max(1.0, target_s / 4))
-    oracle.set_threads(n_threads)
+    idx1, tids1, vals1 = make(256, 0)
+    n1 = sum(ix.size for ix in idx1)
+    dt1 = sample_step(w, recs, calls, log, idx1, tids1, vals1)
+    oracle.set_threads(threads)
     out["value_1_thread"] = n1 * seeds_per_elem / dt1
-    out["sample_1_thread"] = f"elements 0..{n1 - 1} of one tensor (id 0), {dt1:.1f} s"
+    out["sample_1_thread"] = f"{n1} elements (first and last 256 of every tensor), {dt1:.1f} s"
     return out
 
 

@@ -18,7 +18,7 @@ PKG = Path(__file__).resolve().parent
 CSRC = PKG / "csrc"
 ROOT = PKG.parent
 LIB = PKG / "libmezo.so"
-PROBE_LIB = PKG / "libisa_probe.so"
+PROBE_LIB = PKG / "libstream_probe.so"
 BUILD_DIR = ROOT / "_build"
 
 ARCH = "gfx950"
@@ -49,22 +49,29 @@ def _run(cmd):
         sys.stderr.write(err + "\n")
 
 
+#: The kernel translation units of libmezo, one object each.
+KERNEL_UNITS = ["engine_dense.hip", "engine_nf4.hip", "nf4_convert.hip", "checksum.hip", "inspect.hip"]
+
+
 def build(verbose: bool = False) -> Path:
-    """Compile kernels.hip and api.cpp and link libmezo.so next to this file."""
+    """Compile the kernel units and api.cpp and link libmezo.so next to this
+    file; compile the streaming probe the benchmark measures against into
+    libstream_probe.so."""
     BUILD_DIR.mkdir(exist_ok=True)
     cc = hipcc()
-    k_obj = BUILD_DIR / "kernels.o"
-    i_obj = BUILD_DIR / "inspect.o"
+    objs = []
+    for unit in KERNEL_UNITS:
+        obj = BUILD_DIR / (Path(unit).stem + ".o")
+        _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / unit), "-o", str(obj)])
+        objs.append(str(obj))
     a_obj = BUILD_DIR / "api.o"
-    _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / "kernels.hip"), "-o", str(k_obj)])
-    _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / "inspect.hip"), "-o", str(i_obj)])
     _run([cc, *COMMON, "-c", str(CSRC / "api.cpp"), "-o", str(a_obj)])
     tmp = LIB.with_suffix(".so.tmp")
-    _run([cc, "-shared", "-fPIC", *DEVICE, str(k_obj), str(i_obj), str(a_obj), "-o", str(tmp)])
+    _run([cc, "-shared", "-fPIC", *DEVICE, *objs, str(a_obj), "-o", str(tmp)])
     os.replace(tmp, LIB)
-    # the benchmark's issue-rate probe (measurement only, not part of libmezo)
+    # the benchmark's streaming ceiling probe (measurement only, not part of libmezo)
     ptmp = PROBE_LIB.with_suffix(".so.tmp")
-    _run([cc, *COMMON, *DEVICE, "-shared", str(CSRC / "isa_probe.hip"), "-o", str(ptmp)])
+    _run([cc, *COMMON, *DEVICE, "-shared", str(CSRC / "stream_probe.hip"), "-o", str(ptmp)])
     os.replace(ptmp, PROBE_LIB)
     if verbose:
         print(f"built {LIB} and {PROBE_LIB.name}")

@@ -17,8 +17,10 @@
 #include <vector>
 
 #include "../../include/mezo.h"
+#include "checksum_launch.hpp"
+#include "engine_launch.hpp"
 #include "inspect.hpp"
-#include "launch.hpp"
+#include "nf4_launch.hpp"
 #include "records.hpp"
 
 namespace {
@@ -375,7 +377,8 @@ int launch_records(mezo_paramset* ps, RecSpan recs, bool portable, hipStream_t s
         args.src_tensors = src ? src->d_table[dt] : nullptr;
         args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
         args.total_tiles = ps->total_tiles[dt];
-        e = mezo::launch_engine(args, dt, portable, stream);
+        e = dt == mezo::kNF4 ? mezo::launch_engine_nf4(args, portable, stream)
+                             : mezo::launch_engine_dense(args, dt, portable, stream);
     }
     // The slot is reused only after this event: recorded whenever its copy
     // was enqueued, also when a launch failed.

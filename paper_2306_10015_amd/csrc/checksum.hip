@@ -1,0 +1,259 @@
+// checksum.hip — the 64-bit checksum of theta (ChecksumMatch, Algorithm 1):
+// a read-only stream over the same tiles as the engine; every lane sums the
+// mixes of its 8-byte chunks, a workgroup reduces across lanes and waves and
+// adds its sum to the output with one 64-bit atomic. Sums mod 2^64 commute, so
+// the grid shape and the order of the atomics do not change the result.
+#include <atomic>
+
+#include "checksum_launch.hpp"
+#include "nf4.hpp"
+#include "stream_io.hpp"
+#include "tiles.hpp"
+
+namespace mezo {
+
+__device__ __forceinline__ uint64_t fmix64(uint64_t x)
+{
+    x ^= x >> 33;
+    x *= kFmixA;
+    x ^= x >> 33;
+    x *= kFmixB;
+    x ^= x >> 33;
+    return x;
+}
+
+// Reduce every lane's sum across the workgroup and add it to *out with one
+// 64-bit atomic (all lanes of the workgroup must call it).
+__device__ __forceinline__ void add_workgroup_sum(uint64_t sum, unsigned long long* out)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+    __shared__ uint64_t part[kThreads / 64];
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t s = 0;
+#pragma unroll
+        for (int i = 0; i < kThreads / 64; ++i) s += part[i];
+        atomicAdd(out, static_cast<unsigned long long>(s));
+    }
+}
+
+// One lane's share of a tile that lies wholly inside its tensor (every tile
+// but a tensor's last): no bounds, the tile's scalar base plus a 32-bit lane
+// offset, and chunk numbers as a uniform part plus the lane's constant one.
+template <int kGroups>
+__device__ __forceinline__ uint64_t checksum_full_tile(uint64_t data, uint64_t local, uint64_t cpos_tile,
+                                                       uint64_t tmix, const uint64_t (&cpos_lane)[kGroups])
+{
+    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(data) + local * (kThreads * kGroups);
+    uint64_t sum = 0;
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        const u32x4_t v = __builtin_nontemporal_load(base + (uint32_t(g * kThreads) + threadIdx.x));
+        const uint64_t p0 = cpos_tile + cpos_lane[g];  // (its first chunk's number) * kChunkPos
+        const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+        const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+        sum += fmix64(lo ^ p0 ^ tmix);
+        sum += fmix64(hi ^ (p0 + kChunkPos) ^ tmix);
+    }
+    return sum;
+}
+
+template <uint32_t kDtype>
+__global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
+{
+    constexpr int kGroups = Layout<kDtype>::kGroups;
+    constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
+    constexpr uint64_t kEsz = 16 / kPer;
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kGroups * kPer;
+    // chunk number of a lane's group g within its tile, times kChunkPos
+    uint64_t cpos_lane[kGroups];
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) {
+        cpos_lane[g] = 2 * (uint64_t(g) * kThreads + threadIdx.x) * kChunkPos;
+        // opaque from here on: otherwise the compiler folds uniform + lane
+        // constant back into one per-lane 64-bit multiply in every tile
+        asm("" : "+v"(cpos_lane[g]));
+    }
+    uint64_t sum = 0;
+    for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
+        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+        const uint64_t local = tile - d.tile_begin;
+        const uint64_t nbytes = d.numel * kEsz;
+        const uint64_t nchunks = (nbytes + 7) / 8;
+        const uint64_t cbase = d.first * kEsz / 8;  // chunk number of the shard's first byte
+        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+        if ((local + 1) * kTileElems <= d.numel) {  // uniform
+            const uint64_t cpos_tile = (cbase + 2 * local * (kThreads * kGroups)) * kChunkPos;
+            sum += checksum_full_tile<kGroups>(d.data, local, cpos_tile, tmix, cpos_lane);
+            continue;
+        }
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const uint64_t grp = group_index<kGroups>(local, g);
+            const uint64_t c0 = grp * 2;  // the group's first chunk within the shard
+            if (c0 >= nchunks) continue;
+            uint4 v;
+            if ((grp + 1) * kPer <= d.numel) {
+                v = load_stream(d.data + grp * 16);
+            } else {
+                // tail: read the elements that exist, zero the rest
+                uint32_t w[4] = {0u, 0u, 0u, 0u};
+                if constexpr (kDtype == kF32) {
+                    const MEZO_GLOBAL uint32_t* in = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.data);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (grp * 4 + j < d.numel) w[j] = in[grp * 4 + j];
+                } else {
+                    const gu16_t* in = reinterpret_cast<const gu16_t*>(d.data);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (grp * 8 + j < d.numel) w[j >> 1] |= uint32_t(in[grp * 8 + j]) << (16 * (j & 1));
+                }
+                v = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+            const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+            const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+            sum += fmix64(lo ^ ((cbase + c0) * kChunkPos) ^ tmix);
+            if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((cbase + c0 + 1) * kChunkPos) ^ tmix);
+        }
+    }
+    add_workgroup_sum(sum, a.out);
+}
+
+// NF4 tensors: the code bytes zero-padded to whole chunks, then the absmax
+// values, chunk numbers continuing. One wave per tile of 2048 elements: every
+// lane reads 16 code bytes (two chunks) and lanes 0..7 also 16 bytes of the
+// tile's 128 absmax bytes.
+__global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
+{
+    constexpr uint32_t kWaves = kThreads / 64;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63u;
+    // position terms of a lane's chunks within a tile, computed once (opaque
+    // to the compiler, as in checksum_kernel): code chunks 2 lane, 2 lane + 1;
+    // absmax chunk lane (lanes 0..15)
+    uint64_t cpos_code = 2 * uint64_t(lane) * kChunkPos;
+    uint64_t cpos_abs = uint64_t(lane & 15u) * kChunkPos;
+    asm("" : "+v"(cpos_code));
+    asm("" : "+v"(cpos_abs));
+    uint64_t sum = 0;
+    for (uint64_t tile = uint64_t(blockIdx.x) * kWaves + wave; tile < a.total_tiles;
+         tile += uint64_t(gridDim.x) * kWaves) {
+        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
+        const uint64_t local = tile - d.tile_begin;
+        const uint64_t cbytes = (d.numel + 1) / 2;
+        const uint64_t cchunks = (cbytes + 7) / 8;
+        const uint64_t abytes = 4 * ((d.numel + kNF4Block - 1) / kNF4Block);
+        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+        if ((local + 1) * kTileNF4 <= d.numel) {  // uniform: a whole tile, 32 whole blocks
+            const gu32x4_t* codes = reinterpret_cast<const gu32x4_t*>(d.data) + local * 64;
+            const u32x4_t v = __builtin_nontemporal_load(codes + lane);
+            // the tile's 128 absmax bytes as 16 chunks on lanes 0..15; every
+            // lane loads (lane mod 16), so that both loads issue before any mix
+            const MEZO_GLOBAL uint64_t* am = reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.aux) + local * 16;
+            const uint64_t f = __builtin_nontemporal_load(am + (lane & 15u));
+            const uint64_t p0 = 128 * local * kChunkPos + cpos_code;
+            sum += fmix64((uint64_t(v.x) | (uint64_t(v.y) << 32)) ^ p0 ^ tmix);
+            sum += fmix64((uint64_t(v.z) | (uint64_t(v.w) << 32)) ^ (p0 + kChunkPos) ^ tmix);
+            const uint64_t fm = fmix64(f ^ ((cchunks + 16 * local) * kChunkPos + cpos_abs) ^ tmix);
+            sum += lane < 16u ? fm : 0u;
+            continue;
+        }
+        // codes: bytes [16u, 16u + 16) = chunks 2u, 2u + 1
+        const uint64_t u = local * 64 + lane;
+        if (16 * u < cbytes) {
+            uint64_t lo = 0, hi = 0;
+            if (16 * u + 16 <= cbytes) {
+                const uint4 v = load_stream(d.data + 16 * u);
+                lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+                hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+            } else {
+                const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(d.data);
+                for (uint64_t k = 16 * u; k < cbytes; ++k) {
+                    const uint64_t byte = uint64_t(b[k]);
+                    const uint64_t off = k - 16 * u;
+                    if (off < 8)
+                        lo |= byte << (8 * off);
+                    else
+                        hi |= byte << (8 * (off - 8));
+                }
+            }
+            sum += fmix64(lo ^ (2 * u * kChunkPos) ^ tmix);
+            if (16 * u + 8 < cbytes) sum += fmix64(hi ^ ((2 * u + 1) * kChunkPos) ^ tmix);
+        }
+        // absmax: bytes [ab, ab + 16) = absmax chunks k0, k0 + 1
+        const uint64_t ab = local * (kTileNF4 / kNF4Block * 4) + 16 * uint64_t(lane);
+        if (lane < kTileNF4 / kNF4Block * 4 / 16 && ab < abytes) {
+            const uint64_t k0 = ab / 8;
+            uint32_t f[4] = {0u, 0u, 0u, 0u};
+            if (ab + 16 <= abytes) {
+                const uint4 v = load_stream(d.aux + ab);
+                f[0] = v.x;
+                f[1] = v.y;
+                f[2] = v.z;
+                f[3] = v.w;
+            } else {
+                const MEZO_GLOBAL uint32_t* am = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.aux);
+                for (uint64_t k = ab; k < abytes; k += 4) f[(k - ab) / 4] = am[k / 4];
+            }
+            sum += fmix64((uint64_t(f[0]) | (uint64_t(f[1]) << 32)) ^ ((cchunks + k0) * kChunkPos) ^ tmix);
+            if (ab + 8 < abytes)
+                sum += fmix64((uint64_t(f[2]) | (uint64_t(f[3]) << 32)) ^ ((cchunks + k0 + 1) * kChunkPos) ^ tmix);
+        }
+    }
+    add_workgroup_sum(sum, a.out);
+}
+
+__global__ void zero_u64_kernel(unsigned long long* out)
+{
+    if (threadIdx.x == 0 && blockIdx.x == 0) *out = 0ull;
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];  // compute units per device, 0 = not yet asked
+
+template <class Arg>
+hipError_t launch1(void (*kernel)(Arg), dim3 g, dim3 b, hipStream_t stream, Arg arg)
+{
+    void* params[] = {&arg};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kernel), g, b, params, 0, stream);
+}
+}  // namespace
+
+hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n_tables,
+                           unsigned long long* out, int device, hipStream_t stream)
+{
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidValue;
+    int cus = g_cus[device].load(std::memory_order_relaxed);
+    if (cus == 0) {
+        hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+        if (e != hipSuccess) return e;
+        g_cus[device].store(cus, std::memory_order_relaxed);
+    }
+    hipError_t e = launch1(zero_u64_kernel, dim3(1), dim3(64), stream, out);
+    if (e != hipSuccess) return e;
+    for (int i = 0; i < n_tables; ++i) {
+        if (tables[i].total_tiles == 0) continue;
+        // as many workgroups as fill the device (8 per CU), each striding over
+        // tiles (NF4: four tiles at a time, one per wave)
+        const uint64_t per_wg = dtypes[i] == kNF4 ? kThreads / 64 : 1;
+        const uint64_t need = (tables[i].total_tiles + per_wg - 1) / per_wg;
+        const uint64_t cap = uint64_t(cus) * 8;
+        const uint64_t grid = need < cap ? need : cap;
+        const dim3 g{uint32_t(grid)};
+        const dim3 b{uint32_t(kThreads)};
+        if (dtypes[i] == kF32)
+            e = launch1(checksum_kernel<kF32>, g, b, stream, tables[i]);
+        else if (dtypes[i] == kBF16)
+            e = launch1(checksum_kernel<kBF16>, g, b, stream, tables[i]);
+        else
+            e = launch1(checksum_nf4_kernel, g, b, stream, tables[i]);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+}  // namespace mezo

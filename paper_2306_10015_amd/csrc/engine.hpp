@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "engine_launch.hpp"
 #include "records.hpp"
 
 namespace mezo {
@@ -276,6 +277,17 @@ __device__ __forceinline__ void accumulate4(float c, uint32_t w0, uint32_t w1, u
         box_muller_pair_acc(w0, w1, c, a0, a1);
         box_muller_pair_acc(w2, w3, c, a2, a3);
     }
+}
+
+// Record r of a launch: from the kernel arguments (kInline) or the staged
+// device buffer. Either way a wave-uniform address: the words go to SGPRs.
+template <bool kInline>
+__device__ __forceinline__ const SeedRec& rec_at(const EngineArgs& a, uint32_t r)
+{
+    if constexpr (kInline)
+        return a.inl[r];
+    else
+        return a.ext[r];
 }
 
 // ---- storage conversions ---------------------------------------------------

@@ -1,0 +1,122 @@
+// engine_nf4.hip — the engine kernel on 4-bit NF4 storage (gfx950): the
+// same record loop as on fp32/bf16 storage, with the block dequantized once
+// before the first record and quantized again at every step end (Section 3:
+// the weights are dequantized before the noise is added and quantized again
+// afterwards).
+#include "engine.hpp"
+#include "engine_launch.hpp"
+#include "nf4_ops.hpp"
+
+namespace mezo {
+
+// kFull: a tile wholly inside its tensor, where every lane's 8 elements exist
+// (no masks, no bounds).
+template <bool kInline, bool kPortable, bool kFull>
+__device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& d, uint64_t e0, uint32_t packed,
+                                         float am, const NF4Lds& s)
+{
+    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, d.numel);
+    float w[8];
+    nf4_dequant(s, packed, am, valid, w);
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
+    const uint64_t blk = (d.first + e0) >> 2;  // block of the logical tensor
+    const BlockPre pre0 = block_pre(uint32_t(blk));
+    const BlockPre pre1 = block_pre(uint32_t(blk + 1));
+    const auto accumulate = [&](uint32_t r) {
+        const SeedRec& rec = rec_at<kInline>(a, r);
+        const SeedUniform u = seed_uniform(rec, d.tensor_id);
+        const float c = rec.coef;
+        uint32_t w0, w1, w2, w3;
+        philox_words(u, pre0, w0, w1, w2, w3);
+        accumulate4<kPortable>(c, w0, w1, w2, w3, acc[0], acc[1], acc[2], acc[3]);
+        philox_words(u, pre1, w0, w1, w2, w3);
+        accumulate4<kPortable>(c, w0, w1, w2, w3, acc[4], acc[5], acc[6], acc[7]);
+    };
+    const auto step_end = [&]() {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            w[j] = w[j] + acc[j];
+            acc[j] = 0.0f;
+        }
+        if (partial_wave(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (!((valid >> j) & 1u)) w[j] = 0.0f;
+        }
+    };
+    if (a.n_rec == 0) {  // out of place with nothing to apply: a copy
+        nf4_store<kFull>(d.data, d.aux, e0, d.numel, packed, am);
+        return;
+    }
+    // every record list ends a step with its last record, which is peeled off
+    // the loop: its quantization needs no values for a next step
+    for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
+        accumulate(r);
+        if (rec_at<kInline>(a, r).last) {
+            step_end();
+            nf4_requant<true>(s.bin, valid, w, packed, am);
+        }
+    }
+    accumulate(a.n_rec - 1);
+    step_end();
+    nf4_requant<false>(s.bin, valid, w, packed, am);
+    nf4_store<kFull>(d.data, d.aux, e0, d.numel, packed, am);
+}
+
+// kShort: a call of at most two records, where the per-tile work outweighs
+// the record loop; whole tiles then take a copy of the path compiled without
+// bounds or masks. Long record lists keep a single copy of the loop (a second
+// one costs the loop more than the tiles gain).
+template <bool kInline, bool kPortable, bool kShort>
+__global__ __launch_bounds__(kThreads) void engine_nf4_kernel(EngineArgs a)
+{
+    const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
+    const uint32_t ti = a.tile_tensor[tile];
+    const TensorDesc d = a.tensors[ti];
+    __shared__ NF4Lds lds;
+    // out of place: read tensor ti of the source set (same layout), write d
+    const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
+    const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
+    const uint64_t local = tile - d.tile_begin;
+    const uint64_t e0 = local * kTileNF4 + threadIdx.x * 8u;
+    uint32_t packed;
+    float am;
+    if (kShort && (local + 1) * kTileNF4 <= d.numel) {  // uniform: all but a tensor's last tile
+        nf4_load<true>(codes, absmax, e0, d.numel, packed, am);
+        nf4_lds_init(lds);
+        tile_nf4<kInline, kPortable, true>(a, d, e0, packed, am, lds);
+    } else {
+        nf4_load(codes, absmax, e0, d.numel, packed, am);
+        nf4_lds_init(lds);
+        tile_nf4<kInline, kPortable, false>(a, d, e0, packed, am, lds);
+    }
+}
+
+namespace {
+hipError_t launch1(void (*kernel)(EngineArgs), dim3 g, dim3 b, hipStream_t stream, EngineArgs arg)
+{
+    void* params[] = {&arg};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kernel), g, b, params, 0, stream);
+}
+
+template <bool kPortable>
+hipError_t launch_variant(const EngineArgs& args, dim3 g, dim3 b, hipStream_t stream)
+{
+    if (args.n_rec > kInlineRecs) return launch1(engine_nf4_kernel<false, kPortable, false>, g, b, stream, args);
+    if (args.n_rec <= 2) return launch1(engine_nf4_kernel<true, kPortable, true>, g, b, stream, args);
+    return launch1(engine_nf4_kernel<true, kPortable, false>, g, b, stream, args);
+}
+}  // namespace
+
+hipError_t launch_engine_nf4(const EngineArgs& args, bool portable, hipStream_t stream)
+{
+    if (args.total_tiles == 0) return hipSuccess;
+    if (args.total_tiles > uint64_t(0x7FFFFFFF)) return hipErrorInvalidValue;
+    const dim3 g{uint32_t(args.total_tiles)};
+    const dim3 b{uint32_t(kThreads)};
+    return portable ? launch_variant<true>(args, g, b, stream) : launch_variant<false>(args, g, b, stream);
+}
+
+}  // namespace mezo

@@ -1,0 +1,147 @@
+// nf4_ops.hpp — device helpers of the 4-bit storage (the 4-bit forward-only
+// variant of Section 3), shared by the NF4 engine kernel and the standalone
+// conversions.
+//
+// A lane owns 8 consecutive elements (one dword of codes); the 8 lanes
+// tid & ~7 .. tid | 7 own one 64-element block and share its absmax. Codes
+// become values through a 16-entry table and values become codes through the
+// 128-bin table of nf4.hpp.
+#pragma once
+
+#include "engine.hpp"
+#include "nf4.hpp"
+#include "stream_io.hpp"
+
+namespace mezo {
+
+struct NF4Lds {
+    NF4Bin bin[kNF4Bins];
+    float val[kNF4Codes];
+};
+
+__device__ __forceinline__ void nf4_lds_init(NF4Lds& s)
+{
+    if (threadIdx.x < kNF4Bins) s.bin[threadIdx.x] = kNF4Table.bin[threadIdx.x];
+    if (threadIdx.x < kNF4Codes) s.val[threadIdx.x] = kNF4Values[threadIdx.x];
+    __syncthreads();
+}
+
+// Whether any lane of the wave misses elements (valid != 0xFF; only waves
+// that reach a tensor's end): a uniform test, so that the masking it guards
+// stays a branch that every other wave skips instead of selects that every
+// wave executes.
+__device__ __forceinline__ bool partial_wave(uint32_t valid)
+{
+    return __builtin_amdgcn_ballot_w64(valid != 0xFFu) != 0;
+}
+
+// Which of a lane's 8 elements e0 .. e0 + 7 exist (bit j for element e0 + j).
+__device__ __forceinline__ uint32_t nf4_valid(uint64_t e0, uint64_t numel)
+{
+    if (e0 >= numel) return 0u;
+    if (e0 + 8 <= numel) return 0xFFu;
+    return (1u << uint32_t(numel - e0)) - 1u;
+}
+
+// A lane's code dword and its block's absmax (zeros past the end). kFull:
+// the lane's 8 elements are known to exist (a tile wholly inside its tensor).
+template <bool kFull = false>
+__device__ __forceinline__ void nf4_load(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
+                                         uint32_t& packed, float& am)
+{
+    packed = 0u;
+    am = 0.0f;
+    if (!kFull && e0 >= numel) return;
+    if (kFull || e0 + 8 <= numel) {
+        packed = __builtin_nontemporal_load(reinterpret_cast<const MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
+    } else {
+        const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k)
+            if (e0 + 2 * k < numel) packed |= uint32_t(b[k]) << (8 * k);
+    }
+    am = reinterpret_cast<const gfloat_t*>(absmax)[e0 / kNF4Block];
+}
+
+template <bool kFull = false>
+__device__ __forceinline__ void nf4_store(uint64_t codes, uint64_t absmax, uint64_t e0, uint64_t numel,
+                                          uint32_t packed, float am)
+{
+    if (!kFull && e0 >= numel) return;
+    if (kFull || e0 + 8 <= numel) {
+        __builtin_nontemporal_store(packed, reinterpret_cast<MEZO_GLOBAL uint32_t*>(codes + e0 / 2));
+    } else {
+        MEZO_GLOBAL uint8_t* b = reinterpret_cast<MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
+#pragma unroll
+        for (uint32_t k = 0; k < 4; ++k)
+            if (e0 + 2 * k < numel) b[k] = uint8_t(packed >> (8 * k));
+    }
+    if ((threadIdx.x & 7u) == 0u) reinterpret_cast<gfloat_t*>(absmax)[e0 / kNF4Block] = am;
+}
+
+__device__ __forceinline__ void nf4_dequant(const NF4Lds& s, uint32_t packed, float am, uint32_t valid,
+                                            float (&w)[8])
+{
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = s.val[(packed >> (4 * j)) & 15u] * am;
+    if (partial_wave(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
+}
+
+// max over the 8 lanes of a block (lanes 8i .. 8i + 7) of a value >= 0:
+// swap neighbours, then pairs within each quad, then the two quads of each
+// half-row (DPP quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror).
+// Non-negative floats order like their bit patterns, so the maximum is taken
+// on the integers.
+__device__ __forceinline__ float max8(float m)
+{
+    uint32_t u = __float_as_uint(m);
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0xB1, 0xF, 0xF, false)));
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0x4E, 0xF, 0xF, false)));
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0x141, 0xF, 0xF, false)));
+    return __uint_as_float(u);
+}
+
+// Nibbles of the packed codes that hold existing elements.
+__device__ __forceinline__ uint32_t nf4_nibble_mask(uint32_t valid)
+{
+    const uint32_t k = __builtin_popcount(valid);  // valid is a run of low bits
+    return k >= 8 ? 0xFFFFFFFFu : (1u << (4 * k)) - 1u;
+}
+
+// Quantize a block held by 8 lanes (w = 0 for elements that do not exist):
+// a = max |w| over the block, r = 1 / a (correctly rounded; 0 for a = 0),
+// code = nearest NF4 value to fl32(w * r), ties to the lower code. Returns the
+// packed codes (0 for missing elements) and the new absmax; with kNext it also
+// replaces w by the dequantized values fl32(v * a) the next step starts from
+// (0 stays 0: x = 0 lies in a bin without a midpoint whose lower value is 0).
+// Every lane of the wave must call it (the block maximum is exchanged across
+// lanes).
+template <bool kNext>
+__device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, float (&w)[8], uint32_t& packed,
+                                            float& am)
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
+    m = max8(m);
+    const float r = m > 0.0f ? 1.0f / m : 0.0f;
+    uint32_t p = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float x = w[j] * r;
+        int b = static_cast<int>(__builtin_fmaf(x, 64.0f, 64.0f));
+        b = b < 0 ? 0 : (b > kNF4Bins - 1 ? kNF4Bins - 1 : b);
+        const NF4Bin e = bins[b];
+        const bool up = x > e.mid;
+        if constexpr (kNext) w[j] = (up ? e.v_hi : e.v_lo) * m;
+        p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
+    }
+    packed = partial_wave(valid) ? p & nf4_nibble_mask(valid) : p;
+    am = m;
+}
+
+}  // namespace mezo

@@ -1,5 +1,5 @@
 // records.hpp — structures and constants shared by the host code (api.cpp)
-// and the kernels (kernels.hip): the seed record, the tensor table entry, the
+// and the kernels (*.hip): the seed record, the tensor table entry, the
 // work decomposition and the Philox4x32-10 constants.
 #pragma once
 
