@@ -73,9 +73,43 @@ def test_full_size_perturb_and_update(mz, orc, name):
     torch.cuda.empty_cache()
 
 
+def test_full_size_bf16_update_that_moves_the_weights_6p7b(mz, orc):
+    """The 6.7B bf16 set, K = 64, at lr = 1e-3: a step large enough that
+    nearly every bf16 weight rounds to a new value (at lr = 1e-6 most round
+    back to where they were), so the update's rounding itself is compared
+    with the oracle's on sampled elements, to the bf16 bar."""
+    import torch
+    w = synth.WORKLOADS["opt6.7b"]
+    tensors = theta_on_device(w, seed=3, device_rng=True)
+    ps = mz.ParamSet(tensors)
+    idx = sample_all(w, edge=512, blocks=32, seed=4)
+    seeds = synth.workload_seeds(w, step=7)
+    q = workload_q(w, step=7)
+    lr = 1e-3
+    before = gather(torch, tensors, idx)
+    ps.update_multi(seeds, q, lr)
+    torch.cuda.synchronize()
+    after = gather(torch, tensors, idx)
+    changed = total = n_cancel = 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        ref = orc.update(b.copy(), tid, seeds, q, lr, idx=ix)
+        s = assert_theta_close(a, ref, f"opt6.7b update lr=1e-3 tensor {tid}", inp=b)
+        n_cancel += s.get("cancelled_gt1ulp", 0)
+        changed += int(np.sum(ref != b))
+        total += b.size
+    print(f"opt6.7b K=64 lr=1e-3: {changed} of {total} sampled weights changed; "
+          f"cancellations beyond 1 ulp: {n_cancel}")
+    assert changed / total > 0.5
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
+
+
 def test_full_size_replay_1p3b(mz, orc):
     """T = 200 logged steps of K = 32 seeds (4 machines x 8 samples) on the
-    1.3B bf16 set, against the oracle's step-by-step replay."""
+    1.3B bf16 set, against the oracle's step-by-step replay, at the
+    workloads' lr = 1e-6: most steps round back to the weights they started
+    from, but over 200 steps more than a tenth of the weights change."""
     import torch
     w = synth.WORKLOADS["replay1.3b"]
     tensors = theta_on_device(w, seed=0, device_rng=True)
@@ -104,9 +138,44 @@ def test_full_size_replay_1p3b(mz, orc):
             i = synth.bf16_bits_to_fp32(b[far]).astype(np.float64)
             assert np.all(np.abs(g - r) <= bf16_ulp_of(np.maximum(np.abs(i), np.abs(r)))), \
                 f"tensor {tid}: replay off by more than an operand-scale ulp"
-    print(f"replay T={w.T} K={w.K}: sampled {hist.sum()} elements, {changed} changed by the "
+    print(f"replay T={w.T} K={w.K} lr={w.lr}: sampled {hist.sum()} elements, {changed} changed by the "
           f"oracle's replay; ulp distance histogram {hist.tolist()}")
     assert hist[0] / hist.sum() > 0.999
+    assert changed / hist.sum() > 0.1
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
+
+
+def test_full_size_replay_1p3b_portable_large_steps(mz, orc):
+    """The same replay with the portable Gaussian (binary32 operations only,
+    bit-identical to the oracle's) at lr = 1e-4, where nearly every step moves
+    nearly every weight: 200 roundings to bf16 per element, compared bit for
+    bit with the oracle's replay on sampled elements. (With the fast Gaussian
+    a rounding that flips once carries its one-ulp difference along, and a
+    weight that flipped in a larger binade and came back into a smaller one
+    then differs by two ulps of the smaller: only a bit-exact z rules out flips.)"""
+    import torch
+    w = synth.WORKLOADS["replay1.3b"]
+    tensors = theta_on_device(w, seed=6, device_rng=True)
+    ps = mz.ParamSet(tensors, gaussian=mz.GAUSS_PORTABLE)
+    idx = sample_all(w, edge=32, blocks=8, seed=8)
+    before = gather(torch, tensors, idx)
+    lr = 1e-4
+    steps = [(synth.seeds(w.machines, w.samples_per_machine, step=t),
+              synth.grads_int8(w.K, "uniform", seed=700 + t), lr) for t in range(w.T)]
+    ps.replay(steps)
+    torch.cuda.synchronize()
+    after = gather(torch, tensors, idx)
+    changed = total = 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        ref = orc.replay(b.copy(), tid, steps, idx=ix, portable=True)
+        assert np.array_equal(a, ref), f"tensor {tid}: portable replay differs from the oracle's"
+        changed += int(np.sum(ref != b))
+        total += b.size
+    print(f"portable replay T={w.T} K={w.K} lr={lr}: {changed} of {total} sampled weights changed, "
+          f"all bit-identical to the oracle")
+    assert changed / total > 0.5
     ps.close()
     del tensors
     torch.cuda.empty_cache()
