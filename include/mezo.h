@@ -279,6 +279,28 @@ MEZO_API int mezo_update_multi(mezo_paramset_t ps, const mezo_seed_t* seeds, con
 MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T,
                 const mezo_codec_t* codec, void* stream);
 
+/* mezo_replay for callers that cannot allocate memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation. It makes no
+ * device, pinned-host or heap allocation and creates no HIP event: the records
+ * (32 B each) go into a file-scope device array of 65536 records (2 MiB) that
+ * every GPU the library runs on holds until the process ends, written by small
+ * kernels that carry them in their arguments (or, for at most 32 records, into
+ * the engine's arguments directly), and the engine reads them from there.
+ * Same arguments, checks, arithmetic and result as mezo_replay, bit for bit.
+ * Limits and conditions:
+ *   - at most 65536 records (non-zero terms) in one call, else MEZO_ERANGE
+ *     before anything is enqueued (split a longer log at step ends over
+ *     several calls on one stream);
+ *   - ps must already have device tables on the current device, which its
+ *     first call of any other engine entry point creates (else MEZO_EINVAL);
+ *   - the array is shared by every call on a GPU and keeps the last call's
+ *     records (nothing in it needs clearing: a call writes every record it
+ *     reads): two calls whose work may overlap on one GPU — on different
+ *     streams without an ordering between them — race; calls on one stream,
+ *     or ordered by events, do not. */
+MEZO_API int mezo_replay_noalloc(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T,
+                                 const mezo_codec_t* codec, void* stream);
+
 /* Out of place (the weight restore of Algorithm 1 fused into the sweep; it
  * also removes the perturb/restore drift Section 2 mentions): read every
  * tensor of src, write the corresponding tensor of dst, in one pass.

@@ -50,7 +50,8 @@ def _run(cmd):
 
 
 #: The kernel translation units of libmezo, one object each.
-KERNEL_UNITS = ["engine_dense.hip", "engine_nf4.hip", "nf4_convert.hip", "checksum.hip", "inspect.hip"]
+KERNEL_UNITS = ["engine_dense.hip", "engine_nf4.hip", "nf4_convert.hip", "checksum.hip", "inspect.hip",
+                "noalloc.hip"]
 
 
 def build(verbose: bool = False) -> Path:

@@ -21,6 +21,7 @@
 #include "engine_launch.hpp"
 #include "inspect.hpp"
 #include "nf4_launch.hpp"
+#include "noalloc_launch.hpp"
 #include "records.hpp"
 
 namespace {
@@ -136,10 +137,9 @@ mezo::SeedRec make_rec(const mezo_seed_t& s, float coef, bool last, bool fold)
     return r;
 }
 
-// Checks one step of the apply loop and appends its records (zero weights
-// dropped; the step's last kept record is flagged to round to storage).
-int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t* codec,
-                float lr, bool fold, std::vector<mezo::SeedRec>& out)
+// Checks one step of the apply loop: the codec, lr, every code against the
+// codec's range and the seeds strictly ascending (machine-timestamp order).
+int check_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t* codec, float lr)
 {
     if (!codec) return MEZO_EINVAL;
     if (!codec_valid(codec) || !std::isfinite(lr)) return MEZO_ERANGE;
@@ -150,13 +150,46 @@ int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mez
         if (q[k] > qmax || q[k] < -qmax) return MEZO_ERANGE;  // -128 included
     for (uint32_t k = 1; k < K; ++k)
         if (!seed_less(seeds[k - 1], seeds[k])) return MEZO_EORDER;
-    const size_t first = out.size();
-    for (uint32_t k = 0; k < K; ++k) {
-        // weight of perturbation k in the apply loop: -grad * lr (Algorithm 1)
-        const float c = static_cast<float>(-double(lr) * double(decode(q[k], *codec)));
-        if (c != 0.0f) out.push_back(make_rec(seeds[k], c, false, fold));
+    return MEZO_OK;
+}
+
+// Weight of perturbation k in the apply loop: -grad * lr (Algorithm 1).
+float step_coef(int8_t q, const mezo_codec_t& codec, float lr)
+{
+    return static_cast<float>(-double(lr) * double(decode(q, codec)));
+}
+
+// Calls emit(record) for the records of a checked step in order: zero
+// weights dropped, the step's last kept record flagged to round to storage.
+// Returns how many it emitted.
+template <class Emit>
+uint32_t emit_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t& codec, float lr,
+                   bool fold, Emit&& emit)
+{
+    uint32_t last = K;
+    for (uint32_t k = K; k-- > 0;) {
+        if (step_coef(q[k], codec, lr) != 0.0f) {
+            last = k;
+            break;
+        }
     }
-    if (out.size() > first) out.back().last = 1u;
+    uint32_t n = 0;
+    for (uint32_t k = 0; last < K && k <= last; ++k) {
+        const float c = step_coef(q[k], codec, lr);
+        if (c == 0.0f) continue;
+        emit(make_rec(seeds[k], c, k == last, fold));
+        ++n;
+    }
+    return n;
+}
+
+// Checks one step of the apply loop and appends its records.
+int append_step(const mezo_seed_t* seeds, const int8_t* q, uint32_t K, const mezo_codec_t* codec,
+                float lr, bool fold, std::vector<mezo::SeedRec>& out)
+{
+    const int rc = check_step(seeds, q, K, codec, lr);
+    if (rc || K == 0) return rc;
+    emit_step(seeds, q, K, *codec, lr, fold, [&](const mezo::SeedRec& r) { out.push_back(r); });
     return MEZO_OK;
 }
 
@@ -180,14 +213,16 @@ struct mezo_paramset {
     // latest launch on that stream: destroy waits for all of them before it
     // frees the tables (work on an earlier stream may still be running). At
     // most kUses streams are tracked; a further stream takes over the entry
-    // used longest ago, after waiting on the host for that entry's event.
+    // used longest ago, after waiting on the host for that entry's event. The
+    // events are made with the device tables, at the first call, so that no
+    // later call creates one.
     struct Use {
-        hipStream_t stream;
-        hipEvent_t done;
-        uint64_t seq;  // when the entry was last recorded
+        hipStream_t stream = nullptr;
+        hipEvent_t done = nullptr;
+        uint64_t seq = 0;  // when the entry was last recorded; 0: not yet used
     };
     static constexpr size_t kUses = 16;
-    std::vector<Use> uses;
+    Use uses[kUses];
     uint64_t use_seq = 0;
 
     // Staging of record lists too long for the kernel arguments: a ring of
@@ -240,12 +275,18 @@ int ensure_device(mezo_paramset* ps)
             e = hipMemcpy(ps->d_tile_tensor[dt], owner.data(), owner.size() * sizeof(uint32_t),
                           hipMemcpyHostToDevice);
     }
+    for (size_t i = 0; i < mezo_paramset::kUses && e == hipSuccess; ++i)
+        e = hipEventCreateWithFlags(&ps->uses[i].done, hipEventDisableTiming);
     if (e != hipSuccess) {
         for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
             if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
             ps->d_table[dt] = nullptr;
             ps->d_tile_tensor[dt] = nullptr;
+        }
+        for (auto& u : ps->uses) {
+            if (u.done) (void)hipEventDestroy(u.done);
+            u.done = nullptr;
         }
         return hip_fail(e, "paramset device table");
     }
@@ -272,25 +313,19 @@ int refuse_first_use_in_capture(const mezo_paramset* ps)
     return MEZO_EINVAL;
 }
 
-// Record that ps's tables are read by work enqueued so far on stream.
+// Record that ps's tables are read by work enqueued so far on stream (after
+// ensure_device: the events exist; nothing is created here).
 int mark_use(mezo_paramset* ps, hipStream_t stream)
 {
     mezo_paramset::Use* use = nullptr;
     for (auto& u : ps->uses)
-        if (u.stream == stream) use = &u;
-    if (!use && ps->uses.size() >= mezo_paramset::kUses) {
-        use = &*std::min_element(ps->uses.begin(), ps->uses.end(),
-                                 [](const mezo_paramset::Use& a, const mezo_paramset::Use& b) {
-                                     return a.seq < b.seq;
-                                 });
-        MEZO_HIP(hipEventSynchronize(use->done));
-        use->stream = stream;
-    }
+        if (u.seq && u.stream == stream) use = &u;
     if (!use) {
-        hipEvent_t ev = nullptr;
-        MEZO_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
-        ps->uses.push_back({stream, ev, 0});
-        use = &ps->uses.back();
+        // an entry not used yet (seq 0), else the one used longest ago
+        use = std::min_element(std::begin(ps->uses), std::end(ps->uses),
+                               [](const mezo_paramset::Use& a, const mezo_paramset::Use& b) { return a.seq < b.seq; });
+        if (use->seq) MEZO_HIP(hipEventSynchronize(use->done));
+        use->stream = stream;
     }
     use->seq = ++ps->use_seq;
     MEZO_HIP(hipEventRecord(use->done, stream));
@@ -308,6 +343,25 @@ struct RecSpan {
     size_t size;
     bool empty() const { return size == 0; }
 };
+
+// One engine launch per storage type of ps with the records args carries
+// (src: read that set, of the same layout, and write ps).
+hipError_t launch_tables(const mezo_paramset* ps, mezo::EngineArgs& args, bool portable, hipStream_t stream,
+                         const mezo_paramset* src)
+{
+    hipError_t e = hipSuccess;
+    for (uint32_t dt = 0; dt < mezo::kStorageTypes && e == hipSuccess; ++dt) {
+        if (ps->table[dt].empty()) continue;
+        args.tensors = ps->d_table[dt];
+        args.tile_tensor = ps->d_tile_tensor[dt];
+        args.src_tensors = src ? src->d_table[dt] : nullptr;
+        args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
+        args.total_tiles = ps->total_tiles[dt];
+        e = dt == mezo::kNF4 ? mezo::launch_engine_nf4(args, portable, stream)
+                             : mezo::launch_engine_dense(args, dt, portable, stream);
+    }
+    return e;
+}
 
 // Enqueue the engine over every storage type of ps, with the Gaussian the
 // records were made for. With src (same layout), read src and write ps; that
@@ -369,17 +423,7 @@ int launch_records(mezo_paramset* ps, RecSpan recs, bool portable, hipStream_t s
                                 hipMemcpyHostToDevice, stream));
         args.ext = slot->dev;
     }
-    hipError_t e = hipSuccess;
-    for (uint32_t dt = 0; dt < mezo::kStorageTypes && e == hipSuccess; ++dt) {
-        if (ps->table[dt].empty()) continue;
-        args.tensors = ps->d_table[dt];
-        args.tile_tensor = ps->d_tile_tensor[dt];
-        args.src_tensors = src ? src->d_table[dt] : nullptr;
-        args.n_tensors = static_cast<uint32_t>(ps->table[dt].size());
-        args.total_tiles = ps->total_tiles[dt];
-        e = dt == mezo::kNF4 ? mezo::launch_engine_nf4(args, portable, stream)
-                             : mezo::launch_engine_dense(args, dt, portable, stream);
-    }
+    hipError_t e = launch_tables(ps, args, portable, stream, src);
     // The slot is reused only after this event: recorded whenever its copy
     // was enqueued, also when a launch failed.
     if (slot) {
@@ -523,7 +567,8 @@ void mezo_paramset_destroy(mezo_paramset_t ps)
         } catch (...) {
         }
         for (auto& u : ps->uses) {
-            (void)hipEventSynchronize(u.done);
+            if (!u.done) continue;
+            if (u.seq) (void)hipEventSynchronize(u.done);
             (void)hipEventDestroy(u.done);
         }
         for (auto& s : ps->slots) {
@@ -675,6 +720,82 @@ int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const 
             end = e;
         }
         return launch_records(ps, RecSpan{recs.data() + start, end - start}, portable, st);
+    });
+}
+
+int mezo_replay_noalloc(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t T, const mezo_codec_t* codec,
+                        void* stream)
+{
+    // Nothing below allocates: records are built in a fixed array on the
+    // stack and reach the device through the file-scope staging array
+    // (noalloc.hip), or the kernel arguments for at most 32 records.
+    return guarded("mezo_replay_noalloc", [&]() -> int {
+        if (!ps || !codec) return MEZO_EINVAL;
+        if (!codec_valid(codec)) return MEZO_ERANGE;
+        if (T == 0) return MEZO_OK;
+        if (!steps) return MEZO_EINVAL;
+        uint64_t total = 0;  // records kept (non-zero weights)
+        for (uint32_t t = 0; t < T; ++t) {
+            const int rc = check_step(steps[t].seeds, steps[t].q, steps[t].K, codec, steps[t].lr);
+            if (rc) return rc;
+            for (uint32_t k = 0; k < steps[t].K; ++k) total += step_coef(steps[t].q[k], *codec, steps[t].lr) != 0.0f;
+        }
+        if (total == 0) return MEZO_OK;
+        if (total > mezo::kNoAllocRecords) {
+            set_error("mezo_replay_noalloc", "more than 65536 records (non-zero terms) in one call");
+            return MEZO_ERANGE;
+        }
+        const bool portable = portable_of(ps);
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        std::lock_guard<std::mutex> lock(ps->mu);
+        int dev = -1;
+        MEZO_HIP(hipGetDevice(&dev));
+        if (ps->device < 0) {
+            set_error("mezo_replay_noalloc",
+                      "the paramset has no device tables yet: its first call must be one that may allocate them");
+            return MEZO_EINVAL;
+        }
+        if (ps->device != dev) {
+            set_error("paramset used on a device other than the one it was first used on");
+            return MEZO_EINVAL;
+        }
+        bool capture = false;
+        int rc = capturing(st, capture);
+        if (rc) return rc;
+        mezo::EngineArgs args;
+        std::memset(&args, 0, sizeof(args));
+        args.n_rec = static_cast<uint32_t>(total);
+        if (total <= mezo::kInlineRecs) {
+            uint32_t i = 0;
+            for (uint32_t t = 0; t < T; ++t)
+                if (steps[t].K)
+                    emit_step(steps[t].seeds, steps[t].q, steps[t].K, *codec, steps[t].lr, !portable,
+                              [&](const mezo::SeedRec& r) { args.inl[i++] = r; });
+        } else {
+            mezo::SeedRec* scratch = nullptr;
+            MEZO_HIP(mezo::noalloc_scratch(&scratch));
+            mezo::SeedRec chunk[mezo::kStageRecs];
+            uint32_t n = 0, offset = 0;
+            hipError_t e = hipSuccess;
+            const auto flush = [&]() {
+                if (n && e == hipSuccess) e = mezo::launch_stage(scratch, offset, chunk, n, st);
+                offset += n;
+                n = 0;
+            };
+            for (uint32_t t = 0; t < T; ++t)
+                if (steps[t].K)
+                    emit_step(steps[t].seeds, steps[t].q, steps[t].K, *codec, steps[t].lr, !portable,
+                              [&](const mezo::SeedRec& r) {
+                                  chunk[n++] = r;
+                                  if (n == mezo::kStageRecs) flush();
+                              });
+            flush();
+            if (e != hipSuccess) return hip_fail(e, "record staging");
+            args.ext = scratch;
+        }
+        const hipError_t e = launch_tables(ps, args, portable, st, nullptr);
+        if (e != hipSuccess) return hip_fail(e, "engine launch");
+        return capture ? MEZO_OK : mark_use(ps, st);
     });
 }
 

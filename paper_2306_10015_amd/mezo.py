@@ -62,7 +62,8 @@ class Step(ctypes.Structure):
 #: Every symbol include/mezo.h declares.
 EXPORTS = ("mezo_paramset_create", "mezo_paramset_destroy", "mezo_paramset_numel",
            "mezo_paramset_set_gaussian",
-           "mezo_perturb", "mezo_perturb_multi", "mezo_update_multi", "mezo_replay", "mezo_perturb_from",
+           "mezo_perturb", "mezo_perturb_multi", "mezo_update_multi", "mezo_replay", "mezo_replay_noalloc",
+           "mezo_perturb_from",
            "mezo_update_multi_from", "mezo_checksum", "quantize_projgrad",
            "mezo_dequantize", "mezo_nf4_quantize", "mezo_nf4_dequantize", "mezo_debug_generate", "mezo_debug_box_muller",
            "mezo_strerror", "mezo_last_error", "mezo_version")
@@ -95,6 +96,8 @@ def _load() -> ctypes.CDLL:
     L.mezo_update_multi.restype = i32
     L.mezo_replay.argtypes = [vp, ctypes.POINTER(Step), u32, ctypes.POINTER(Codec), vp]
     L.mezo_replay.restype = i32
+    L.mezo_replay_noalloc.argtypes = [vp, ctypes.POINTER(Step), u32, ctypes.POINTER(Codec), vp]
+    L.mezo_replay_noalloc.restype = i32
     L.mezo_perturb_from.argtypes = [vp, vp, Seed, f32, vp]
     L.mezo_perturb_from.restype = i32
     L.mezo_update_multi_from.argtypes = [vp, vp, vp, vp, u32, ctypes.POINTER(Codec), f32, vp]
@@ -394,6 +397,15 @@ class ParamSet:
 
     def replay(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
         """Late-joiner catch-up: steps = [(seeds, q, lr), ...] in order."""
+        self._replay(lib.mezo_replay, "mezo_replay", steps, codec_, stream)
+
+    def replay_noalloc(self, steps, codec_: Codec = DEFAULT_CODEC, stream=None) -> None:
+        """replay through mezo_replay_noalloc, the entry point that allocates
+        nothing (at most 65536 records; the set must have had a call of
+        another engine entry point first)."""
+        self._replay(lib.mezo_replay_noalloc, "mezo_replay_noalloc", steps, codec_, stream)
+
+    def _replay(self, fn, what, steps, codec_, stream) -> None:
         keep = []
         arr = (Step * max(1, len(steps)))()
         for i, (s, q, lr) in enumerate(steps):
@@ -404,8 +416,7 @@ class ParamSet:
             keep.append((sa, qa))
             arr[i] = Step(sa.ctypes.data, qa.ctypes.data, sa.size, float(lr))
         with self._on_device():
-            _check(lib.mezo_replay(self._h, arr, len(steps), ctypes.byref(codec_),
-                                   _stream_ptr(stream)), "mezo_replay")
+            _check(fn(self._h, arr, len(steps), ctypes.byref(codec_), _stream_ptr(stream)), what)
 
 
 def step_lr(eta: float, n_grads: int, sqrt_scaling: bool = False) -> float:

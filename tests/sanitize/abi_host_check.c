@@ -31,6 +31,8 @@ unsigned long double_generate_launches(void);
 unsigned long double_event_syncs(void);
 unsigned long double_events_live(void);
 size_t double_device_allocations(void);
+unsigned long double_allocation_calls(void);
+unsigned long double_stage_launches(void);
 uint32_t double_last_records(float* coef, uint32_t* last, uint32_t* machine, uint32_t max);
 int double_last_out_of_place(void);
 
@@ -323,6 +325,90 @@ static void check_staging_and_replay(void)
     free(q);
 }
 
+static float g_coef2[MAXREC];
+static uint32_t g_last2[MAXREC], g_mach2[MAXREC];
+
+/* mezo_replay_noalloc: the records mezo_replay would launch, through the
+ * staging array, with no allocation and no event created */
+static void check_replay_noalloc(void)
+{
+    mezo_paramset_t ps, fresh;
+    mezo_codec_t c = {MEZO_CODEC_LINEAR, 1.0f / 127.0f, 0.0f};
+    mezo_seed_t* s = seeds_n(70000, 0);
+    int8_t* q = codes_n(70000, 5);  /* every 5th code zero: dropped */
+    mezo_step_t st[3];
+    unsigned long allocs, stages, launches;
+    uint32_t n, n2, i;
+    CHECK(create1(T(0x100000, 3000, 0, MEZO_BF16, 0, 0), &ps) == MEZO_OK);
+    CHECK(create1(T(0x200000, 300, 1, MEZO_F32, 0, 0), &fresh) == MEZO_OK);
+    for (i = 0; i < 3; ++i) {
+        st[i].seeds = s;
+        st[i].q = q;
+        st[i].K = 400 + 37 * i;
+        st[i].lr = 1e-3f;
+    }
+    /* no device tables yet: refused (creating them would allocate) */
+    CHECK(mezo_replay_noalloc(fresh, st, 3, &c, NULL) == MEZO_EINVAL);
+    CHECK(strlen(mezo_last_error()) > 0);
+    CHECK(mezo_replay_noalloc(NULL, st, 3, &c, NULL) == MEZO_EINVAL);
+    CHECK(mezo_replay_noalloc(ps, st, 3, NULL, NULL) == MEZO_EINVAL);
+    CHECK(mezo_replay_noalloc(ps, st, 0, &c, NULL) == MEZO_OK);
+    CHECK(mezo_replay(ps, st, 3, &c, NULL) == MEZO_OK);  /* creates the tables */
+    n = double_last_records(g_coef, g_last, g_mach, MAXREC);
+    allocs = double_allocation_calls();
+    stages = double_stage_launches();
+    launches = double_engine_launches(MEZO_BF16);
+    for (i = 0; i < 20; ++i)  /* 20 streams: more than the tracked ones */
+        CHECK(mezo_replay_noalloc(ps, st, 3, &c, (void*)(uintptr_t)(0x1000 * (i + 1))) == MEZO_OK);
+    n2 = double_last_records(g_coef2, g_last2, g_mach2, MAXREC);
+    CHECK(double_allocation_calls() == allocs);
+    CHECK(double_engine_launches(MEZO_BF16) == launches + 20);
+    CHECK(double_stage_launches() == stages + 20 * ((n + 31) / 32));
+    CHECK(n2 == n && memcmp(g_coef, g_coef2, n * sizeof(float)) == 0 &&
+          memcmp(g_last, g_last2, n * sizeof(uint32_t)) == 0 && memcmp(g_mach, g_mach2, n * sizeof(uint32_t)) == 0);
+    /* a second, smaller call: only its own records are read */
+    st[0].K = 40;
+    CHECK(mezo_replay(ps, st, 1, &c, NULL) == MEZO_OK);
+    n = double_last_records(g_coef, g_last, g_mach, MAXREC);
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_OK);
+    n2 = double_last_records(g_coef2, g_last2, g_mach2, MAXREC);
+    CHECK(n == 32 && n2 == n && memcmp(g_coef, g_coef2, n * sizeof(float)) == 0);
+    /* at most 32 records travel in the engine's arguments: no staging */
+    stages = double_stage_launches();
+    st[0].K = 20;
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_OK);
+    CHECK(double_stage_launches() == stages);
+    /* argument checks as for mezo_replay, before anything is enqueued */
+    q[3] = -128;
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_ERANGE);
+    q[3] = 4;
+    st[0].lr = NAN;
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_ERANGE);
+    st[0].lr = 1e-3f;
+    s[7] = S(3, 0, 0);
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_EORDER);
+    s[7] = S(7, 0, 0);
+    /* more records than the staging array holds: refused; exactly 65536 fits */
+    for (i = 0; i < 70000; ++i) q[i] = 1;
+    st[0].K = 65537;
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_ERANGE);
+    st[0].K = 65536;
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_OK);
+    CHECK(double_last_records(g_coef, g_last, g_mach, MAXREC) == 65536 && g_last[65535] == 1 && g_last[65534] == 0);
+    /* graph capture: every step is a kernel launch, so it may be captured */
+    double_set_capturing(1);
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_OK);
+    double_set_capturing(0);
+    /* the device its tables live on */
+    double_set_device(2);
+    CHECK(mezo_replay_noalloc(ps, st, 1, &c, NULL) == MEZO_EINVAL);
+    double_set_device(0);
+    mezo_paramset_destroy(fresh);
+    mezo_paramset_destroy(ps);
+    free(s);
+    free(q);
+}
+
 static void check_streams_devices_capture(void)
 {
     mezo_paramset_t ps, fresh;
@@ -485,6 +571,7 @@ int main(void)
     check_perturb_calls();
     check_staging_and_replay();
     check_streams_devices_capture();
+    check_replay_noalloc();
     check_from_mixed_checksum_nf4();
     check_inspection_and_messages();
     check_threads();

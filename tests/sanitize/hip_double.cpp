@@ -24,6 +24,7 @@
 #include "engine_launch.hpp"
 #include "inspect.hpp"
 #include "nf4_launch.hpp"
+#include "noalloc_launch.hpp"
 #include "records.hpp"
 
 namespace {
@@ -34,7 +35,6 @@ std::map<uintptr_t, size_t> g_host;  // live pinned host allocations
 int g_device = 0;
 int g_capturing = 0;
 long g_fail_malloc_in = -1;          // fail the n-th hipMalloc from now (0 = the next)
-uint64_t g_next_symbol_device = 0;
 
 struct Stats {
     unsigned long launches[3];       // engine launches per storage type
@@ -44,7 +44,12 @@ struct Stats {
     unsigned long event_syncs;
     unsigned long events_live;
     unsigned long h2d_bytes;
+    unsigned long allocations;       // hipMalloc + hipHostMalloc + hipEventCreateWithFlags calls
+    unsigned long stage_launches;
 } g_stats;
+
+// the file-scope staging array of the entry point that allocates nothing
+mezo::SeedRec g_scratch[mezo::kNoAllocRecords];
 
 std::vector<mezo::SeedRec> g_last_recs;
 uint32_t g_last_dtype = 0;
@@ -117,6 +122,7 @@ hipError_t hipMalloc(void** p, size_t bytes)
         return hipErrorOutOfMemory;
     }
     if (g_fail_malloc_in > 0) --g_fail_malloc_in;
+    ++g_stats.allocations;
     *p = std::malloc(bytes ? bytes : 1);
     if (!*p) return hipErrorOutOfMemory;
     g_dev[reinterpret_cast<uintptr_t>(*p)] = bytes;
@@ -135,6 +141,7 @@ hipError_t hipFree(void* p)
 hipError_t hipHostMalloc(void** p, size_t bytes, unsigned int)
 {
     std::lock_guard<std::mutex> lock(g_mu);
+    ++g_stats.allocations;
     *p = std::malloc(bytes ? bytes : 1);
     if (!*p) return hipErrorOutOfMemory;
     g_host[reinterpret_cast<uintptr_t>(*p)] = bytes;
@@ -183,6 +190,7 @@ hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned)
     *e = reinterpret_cast<hipEvent_t>(ev);
     std::lock_guard<std::mutex> lock(g_mu);
     ++g_stats.events_live;
+    ++g_stats.allocations;
     return hipSuccess;
 }
 
@@ -211,16 +219,6 @@ hipError_t hipEventDestroy(hipEvent_t e)
     delete ev;
     std::lock_guard<std::mutex> lock(g_mu);
     --g_stats.events_live;
-    return hipSuccess;
-}
-
-hipError_t hipGetSymbolAddress(void** p, const void* symbol)
-{
-    // the "device copy" of a file-scope device array: its host-side address
-    // stands in for it, one per device
-    std::lock_guard<std::mutex> lock(g_mu);
-    *p = const_cast<void*>(symbol);
-    ++g_next_symbol_device;
     return hipSuccess;
 }
 
@@ -287,6 +285,25 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
     return hipSuccess;
 }
 
+hipError_t noalloc_scratch(SeedRec** out)
+{
+    std::lock_guard<std::mutex> lock(g_mu);
+    // registered as device memory so that the engine launch may read it
+    g_dev[reinterpret_cast<uintptr_t>(g_scratch)] = sizeof(g_scratch);
+    *out = g_scratch;
+    return hipSuccess;
+}
+
+hipError_t launch_stage(SeedRec* dst, uint32_t offset, const SeedRec* recs, uint32_t n, hipStream_t)
+{
+    if (dst != g_scratch) fail("staging outside the staging array");
+    if (n == 0 || n > kStageRecs || offset > kNoAllocRecords - n) fail("staging past the staging array");
+    std::lock_guard<std::mutex> lock(g_mu);
+    std::memcpy(dst + offset, recs, n * sizeof(SeedRec));
+    ++g_stats.stage_launches;
+    return hipSuccess;
+}
+
 hipError_t launch_nf4(const NF4ConvArgs& a, bool, hipStream_t)
 {
     if (a.n == 0 || (a.dtype != kF32 && a.dtype != kBF16)) fail("bad NF4 conversion");
@@ -327,7 +344,12 @@ unsigned long double_nf4_launches(void) { return g_stats.nf4_launches; }
 unsigned long double_generate_launches(void) { return g_stats.generate_launches; }
 unsigned long double_event_syncs(void) { return g_stats.event_syncs; }
 unsigned long double_events_live(void) { return g_stats.events_live; }
-size_t double_device_allocations(void) { return g_dev.size() + g_host.size(); }
+size_t double_device_allocations(void)
+{
+    return g_dev.size() + g_host.size() - g_dev.count(reinterpret_cast<uintptr_t>(g_scratch));
+}
+unsigned long double_allocation_calls(void) { return g_stats.allocations; }
+unsigned long double_stage_launches(void) { return g_stats.stage_launches; }
 
 // The records of the last engine launch: their count, and for each its
 // coefficient, step-end flag and low machine word (arrays of at least max).
