@@ -65,11 +65,118 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
     nf4_store<kFull>(d.data, d.aux, e0, d.numel, packed, am);
 }
 
-// kShort: a call of at most two records, where the per-tile work outweighs
-// the record loop; whole tiles then take a copy of the path compiled without
-// bounds or masks. Long record lists keep a single copy of the loop (a second
-// one costs the loop more than the tiles gain).
-template <bool kInline, bool kPortable, bool kShort>
+// The noise of record r for a lane's 8 elements: acc = c z (kSet, a step's
+// first record, which saves zeroing the accumulators: the result can differ
+// from fma(c, z, +0) only in the sign of a zero, which no code depends on, +0
+// and -0 sharing the zero code's bin) or acc += c z.
+template <bool kPortable, bool kSet>
+__device__ __forceinline__ void short_record(const SeedRec& rec, uint32_t tensor_id, BlockPre pre0, BlockPre pre1,
+                                             float (&acc)[8])
+{
+    const SeedUniform u = seed_uniform(rec, tensor_id);
+    const float c = rec.coef;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        uint32_t w0, w1, w2, w3;
+        philox_words(u, h ? pre1 : pre0, w0, w1, w2, w3);
+        float* a4 = acc + 4 * h;
+        if constexpr (!kSet) {
+            accumulate4<kPortable>(c, w0, w1, w2, w3, a4[0], a4[1], a4[2], a4[3]);
+        } else if constexpr (kPortable) {
+            const Z4 z = gauss4_portable(w0, w1, w2, w3);
+            a4[0] = c * z.z0;
+            a4[1] = c * z.z1;
+            a4[2] = c * z.z2;
+            a4[3] = c * z.z3;
+        } else {
+            // box_muller_pair_acc with acc = 0: c r once per pair, then c r cos, c r sin
+            constexpr float kTwoM24 = 0x1p-24f;
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                const uint32_t wa = p ? w2 : w0, wb = p ? w3 : w1;
+                const float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
+                const float u2 = float(wb >> 8) * kTwoM24;
+                const float cr = c * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1));
+                a4[2 * p] = cr * __builtin_amdgcn_cosf(u2);
+                a4[2 * p + 1] = cr * __builtin_amdgcn_sinf(u2);
+            }
+        }
+    }
+}
+
+// A lane's 8 elements through a call of one or two records (inline):
+// dequantize through the pair table, the records (a step's first one
+// assigning the accumulators), and at each step end add and quantize on the
+// round-to-nearest table. kFull: the 8 elements all exist (no masks).
+template <bool kPortable, bool kFull>
+__device__ __forceinline__ void short_records(const EngineArgs& a, const TensorDesc& d, uint64_t e0,
+                                              const NF4ShortLds& s, uint32_t& packed, float& am)
+{
+    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, d.numel);
+    float w[8];
+    nf4_dequant_pairs(s, packed, am, valid, w);
+    const uint64_t blk = (d.first + e0) >> 2;  // block of the logical tensor
+    const BlockPre pre0 = block_pre(uint32_t(blk));
+    const BlockPre pre1 = block_pre(uint32_t(blk + 1));
+    float acc[8];
+    const auto step_end = [&]() {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = w[j] + acc[j];
+        if (!kFull && partial_wave(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (!((valid >> j) & 1u)) w[j] = 0.0f;
+        }
+    };
+    short_record<kPortable, true>(a.inl[0], d.tensor_id, pre0, pre1, acc);
+    if (a.n_rec == 2) {
+        if (a.inl[0].last) {
+            step_end();
+            nf4_requant_round<true>(s.bin, valid, w, packed, am);
+            short_record<kPortable, true>(a.inl[1], d.tensor_id, pre0, pre1, acc);
+        } else {
+            short_record<kPortable, false>(a.inl[1], d.tensor_id, pre0, pre1, acc);
+        }
+    }
+    step_end();
+    nf4_requant_round<false>(s.bin, valid, w, packed, am);
+}
+
+// A call of at most two records (inline): a perturbation, or a restore fused
+// with the next perturbation, where the per-tile work around the noise weighs
+// most; whole tiles take a path compiled without bounds or masks. With no
+// records (out of place with nothing to apply) a tile is copied. Compiled for
+// 8 waves per SIMD (at most 64 VGPRs), the occupancy of the other kernels.
+template <bool kPortable>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void engine_nf4_short_kernel(EngineArgs a)
+{
+    const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
+    const uint32_t ti = a.tile_tensor[tile];
+    const TensorDesc d = a.tensors[ti];
+    __shared__ NF4ShortLds lds;
+    // out of place: read tensor ti of the source set (same layout), write d
+    const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
+    const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
+    const uint64_t local = tile - d.tile_begin;
+    const uint64_t e0 = local * kTileNF4 + threadIdx.x * 8u;
+    uint32_t packed;
+    float am;
+    if ((local + 1) * kTileNF4 <= d.numel) {  // uniform: all but a tensor's last tile
+        nf4_load<true>(codes, absmax, e0, d.numel, packed, am);
+        nf4_short_lds_init(lds);
+        if (a.n_rec) short_records<kPortable, true>(a, d, e0, lds, packed, am);
+        nf4_store<true>(d.data, d.aux, e0, d.numel, packed, am);
+    } else {
+        nf4_load(codes, absmax, e0, d.numel, packed, am);
+        nf4_short_lds_init(lds);
+        if (a.n_rec) short_records<kPortable, false>(a, d, e0, lds, packed, am);
+        nf4_store(d.data, d.aux, e0, d.numel, packed, am);
+    }
+}
+
+// Record lists of more than two records: one loop over the records (tile_nf4).
+template <bool kInline, bool kPortable>
 __global__ __launch_bounds__(kThreads) void engine_nf4_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
@@ -83,15 +190,9 @@ __global__ __launch_bounds__(kThreads) void engine_nf4_kernel(EngineArgs a)
     const uint64_t e0 = local * kTileNF4 + threadIdx.x * 8u;
     uint32_t packed;
     float am;
-    if (kShort && (local + 1) * kTileNF4 <= d.numel) {  // uniform: all but a tensor's last tile
-        nf4_load<true>(codes, absmax, e0, d.numel, packed, am);
-        nf4_lds_init(lds);
-        tile_nf4<kInline, kPortable, true>(a, d, e0, packed, am, lds);
-    } else {
-        nf4_load(codes, absmax, e0, d.numel, packed, am);
-        nf4_lds_init(lds);
-        tile_nf4<kInline, kPortable, false>(a, d, e0, packed, am, lds);
-    }
+    nf4_load(codes, absmax, e0, d.numel, packed, am);
+    nf4_lds_init(lds);
+    tile_nf4<kInline, kPortable, false>(a, d, e0, packed, am, lds);
 }
 
 namespace {
@@ -104,9 +205,9 @@ hipError_t launch1(void (*kernel)(EngineArgs), dim3 g, dim3 b, hipStream_t strea
 template <bool kPortable>
 hipError_t launch_variant(const EngineArgs& args, dim3 g, dim3 b, hipStream_t stream)
 {
-    if (args.n_rec > kInlineRecs) return launch1(engine_nf4_kernel<false, kPortable, false>, g, b, stream, args);
-    if (args.n_rec <= 2) return launch1(engine_nf4_kernel<true, kPortable, true>, g, b, stream, args);
-    return launch1(engine_nf4_kernel<true, kPortable, false>, g, b, stream, args);
+    if (args.n_rec > kInlineRecs) return launch1(engine_nf4_kernel<false, kPortable>, g, b, stream, args);
+    if (args.n_rec <= 2) return launch1(engine_nf4_short_kernel<kPortable>, g, b, stream, args);
+    return launch1(engine_nf4_kernel<true, kPortable>, g, b, stream, args);
 }
 }  // namespace
 

@@ -5,7 +5,10 @@
 // A lane owns 8 consecutive elements (one dword of codes); the 8 lanes
 // tid & ~7 .. tid | 7 own one 64-element block and share its absmax. Codes
 // become values through a 16-entry table and values become codes through the
-// 128-bin table of nf4.hpp.
+// 128-bin table of nf4.hpp. Calls of one or two records (where the per-element
+// work around the noise weighs most) take the short path at the end of this
+// file: a table of byte -> the values of its two codes, the 129-bin
+// round-to-nearest table, and a shorter reciprocal.
 #pragma once
 
 #include "engine.hpp"
@@ -139,6 +142,130 @@ __device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, 
         const bool up = x > e.mid;
         if constexpr (kNext) w[j] = (up ? e.v_hi : e.v_lo) * m;
         p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
+    }
+    packed = partial_wave(valid) ? p & nf4_nibble_mask(valid) : p;
+    am = m;
+}
+
+// ---- the short path: calls of one or two records ---------------------------
+
+struct NF4ShortLds {
+    NF4Bin bin[kNF4RoundBins];
+    float2 pair[kNF4Pairs];  // byte b -> (value of code b & 15, value of code b >> 4)
+};
+static_assert(kThreads == kNF4Pairs && kThreads >= kNF4RoundBins, "one table entry per lane");
+
+__device__ __forceinline__ void nf4_short_lds_init(NF4ShortLds& s)
+{
+    const uint32_t t = threadIdx.x;
+    s.pair[t] = make_float2(kNF4Values[t & 15u], kNF4Values[t >> 4]);
+    if (t < uint32_t(kNF4RoundBins)) s.bin[t] = kNF4RoundTable.bin[t];
+    __syncthreads();
+}
+
+// Byte k of packed times 8, the LDS byte offset of its entry in the pair
+// table: one shift with sub-dword (SDWA) selection of the byte.
+template <int k>
+__device__ __forceinline__ uint32_t byte_x8(uint32_t packed)
+{
+    uint32_t off;
+    if constexpr (k == 0)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+            : "=v"(off) : "v"(packed));
+    else if constexpr (k == 1)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+            : "=v"(off) : "v"(packed));
+    else if constexpr (k == 2)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+            : "=v"(off) : "v"(packed));
+    else
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+            : "=v"(off) : "v"(packed));
+    return off;
+}
+
+template <int k>
+__device__ __forceinline__ float2 nf4_pair(const NF4ShortLds& s, uint32_t packed)
+{
+    return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(s.pair) + byte_x8<k>(packed));
+}
+
+// nf4_dequant through the pair table: each code byte fetches the values of
+// its two codes at once.
+__device__ __forceinline__ void nf4_dequant_pairs(const NF4ShortLds& s, uint32_t packed, float am, uint32_t valid,
+                                                  float (&w)[8])
+{
+    const float2 p0 = nf4_pair<0>(s, packed);
+    const float2 p1 = nf4_pair<1>(s, packed);
+    const float2 p2 = nf4_pair<2>(s, packed);
+    const float2 p3 = nf4_pair<3>(s, packed);
+    w[0] = p0.x * am;
+    w[1] = p0.y * am;
+    w[2] = p1.x * am;
+    w[3] = p1.y * am;
+    w[4] = p2.x * am;
+    w[5] = p2.y * am;
+    w[6] = p3.x * am;
+    w[7] = p3.y * am;
+    if (partial_wave(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
+}
+
+// Block maxima whose reciprocal takes the short sequence: [2^-64, 2^64].
+constexpr uint32_t kRecipLo = 0x1F800000u;  // 2^-64
+constexpr uint32_t kRecipHi = 0x5F800000u;  // 2^64
+
+// nf4_requant on the round-to-nearest table. When every lane's block maximum
+// a lies in [2^-64, 2^64] (the usual case), r = 1 / a comes from the
+// correctly rounded division sequence without its operand scaling and
+// special-value fix-up (which act only outside that range), every |x| <= 1 +
+// 2^-23, and the bin's table offset is read off t = fl32(64 x + magic)
+// directly. Otherwise (a = 0, tiny or huge blocks; x may be infinite or NaN)
+// the wave takes the general division and clamps the bin to the table, a NaN
+// x (0 * inf) taking the lowest bin like the comparisons it fails. Same
+// result as nf4_requant either way.
+template <bool kNext>
+__device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t valid, float (&w)[8],
+                                                  uint32_t& packed, float& am)
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
+    m = max8(m);
+    const bool usual = __float_as_uint(m) - kRecipLo <= kRecipHi - kRecipLo;
+    const char* base = reinterpret_cast<const char*>(bins);
+    uint32_t p = 0u;
+    const auto code = [&](int j, float x, uint32_t off) {
+        if constexpr (kNext) {
+            const NF4Bin e = *reinterpret_cast<const NF4Bin*>(base + off);
+            const bool up = x > e.mid;
+            w[j] = (up ? e.v_hi : e.v_lo) * m;
+            p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
+        } else {
+            const float2 e = *reinterpret_cast<const float2*>(base + off);  // mid, lo
+            p |= (__float_as_uint(e.y) + (x > e.x ? 1u : 0u)) << (4 * j);
+        }
+    };
+    if (__builtin_amdgcn_ballot_w64(!usual) == 0) {  // uniform
+        const float r = div_rn_normal(1.0f, m);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float x = w[j] * r;
+            const uint32_t t = __float_as_uint(__builtin_fmaf(x, 64.0f, kNF4BinMagic));
+            code(j, x, (t << 4) - (kNF4BinBase << 4));  // 16 (t - base) = 16 b
+        }
+    } else {
+        const float r = m > 0.0f ? 1.0f / m : 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float x = w[j] * r;
+            const float xs = x == x ? x : -2.0f;
+            const int k = int(__float_as_uint(__builtin_fmaf(xs, 64.0f, kNF4BinMagic))) - int(kNF4BinBase);
+            code(j, x, uint32_t(k < 0 ? 0 : (k > kNF4RoundBins - 1 ? kNF4RoundBins - 1 : k)) << 4);
+        }
     }
     packed = partial_wave(valid) ? p & nf4_nibble_mask(valid) : p;
     am = m;

@@ -49,8 +49,9 @@ constexpr int kGroupsBF16 = 1;
 constexpr uint64_t kTileF32 = uint64_t(kThreads) * kGroupsF32 * 4;
 constexpr uint64_t kTileBF16 = uint64_t(kThreads) * kGroupsBF16 * 8;
 // NF4: each lane owns 8 consecutive elements (4 code bytes, two Philox
-// blocks); 8 lanes make one 64-element block.
+// blocks); 8 lanes make one block of kNF4Block elements sharing one absmax.
 constexpr uint64_t kTileNF4 = uint64_t(kThreads) * 8;
+constexpr int kNF4Block = 64;
 
 // Records that travel inside the kernel arguments (above this they are staged
 // in device memory).

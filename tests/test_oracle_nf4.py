@@ -6,6 +6,7 @@ quantizer against a brute-force nearest-value search, the storage round trip
 and error bound, the nibble order, and the relations of perturb, update and
 replay on NF4 storage to the exact perturbation and to each other."""
 import math
+import os
 from pathlib import Path
 
 import numpy as np
@@ -247,3 +248,26 @@ def test_checksum_image(orc, nf4):
     b.view(np.uint32)[1] ^= 1
     assert nf4.checksum_tensor(p, b, 9) != base
     assert nf4.checksum_tensor(p, a, 8) != base
+
+
+def test_kernel_bin_table_is_the_nearest_value_rule(nf4, tmp_path):
+    """The kernels' NF4 quantizer looks codes up in a bin table of
+    csrc/nf4.hpp: the floor table (long record lists, conversions) or the
+    round-to-nearest table, its bin read off one fma (short lists' fast path)
+    or clamped (their general path). Replayed on the host over every float x
+    with |x| <= 1 + 2^-22 and over infinities, NaN and out-of-range values,
+    each code equals the number of the oracle's midpoints strictly below x."""
+    import shutil
+    import subprocess
+    if shutil.which("g++") is None:
+        pytest.skip("needs g++")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    exe = tmp_path / "nf4_table_check"
+    subprocess.run(["g++", "-std=c++17", "-O2", "-ffp-contract=off", "-march=x86-64-v3",
+                    "-I" + os.path.join(root, "paper_2306_10015_amd", "csrc"),
+                    os.path.join(root, "tests", "nf4_table_check.cpp"), "-o", str(exe)], check=True)
+    mids = " ".join(f"{int(u):08x}" for u in nf4.midpoints().astype(np.float32).view(np.uint32))
+    r = subprocess.run([str(exe)], input=mids, capture_output=True, text=True, timeout=600)
+    print(r.stdout)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert " 0 mismatches" in r.stdout
