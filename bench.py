@@ -105,10 +105,12 @@ def parse():
     p.add_argument("--gaussian", choices=["fast", "portable"], default="fast",
                    help="how z is computed (portable: binary32 operations only, bit-identical "
                         "on any IEEE device)")
-    p.add_argument("--probe", choices=["copy", "rmw"], default=None,
+    p.add_argument("--probe", choices=["copy", "rmw", "checksum", "nf4-dequantize", "nf4-quantize"],
+                   default=None,
                    help="copy: time a plain device copy of the parameter buffer instead; rmw: an in-place "
                         "streaming read-modify-write of it with the engine's access pattern (the sweep's "
-                        "memory ceiling)")
+                        "memory ceiling); checksum: the set's checksum alone; nf4-dequantize / "
+                        "nf4-quantize: an NF4 set's largest tensor converted to bf16 and back")
     p.add_argument("--rmw-groups", type=int, choices=[1, 2], default=None,
                    help="rmw probe: 16-byte groups per lane (default 1, the engine's)")
     p.add_argument("--rmw-lanes", type=int, choices=[128, 256, 512], default=256,
@@ -232,6 +234,9 @@ def main():
         rmw_probe(torch, flat, args)
         return
     ps = mezo.ParamSet(views, gaussian=gauss)
+    if args.probe is not None:
+        kernel_probe(torch, mezo, synth, w, ps, args)
+        return
     eps, lr = w.eps, w.lr
 
     total_steps = args.warmup + args.steps
@@ -322,6 +327,8 @@ def main():
             "records": int(kmax),
             "valu_busy_pct": vr[kmax]["busy_pct"],
             "dual_issue_pct": vr[kmax]["dual_issue_pct"],
+            "main_pipe_busy_pct": vr[kmax].get("main_pipe_busy_pct"),
+            "clock_ghz": vr[kmax].get("clock_ghz"),
             "valu_instr_per_param_seed": vr[kmax]["instr_per_param_seed"],
             "nontrans_instr_per_param_seed": vr[kmax]["instr_per_param_seed"] - vr[kmax]["trans_per_param_seed"],
             "by_records": {r: {"valu_busy_pct": round(v["busy_pct"], 1),
@@ -582,6 +589,48 @@ def copy_probe(torch, flat, args):
     print(json.dumps({"probe": "copy", "bytes_per_copy": nbytes, "ms": ms,
                       "GBps": nbytes / (ms / 1e3) / 1e9,
                       "hbm_frac": nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
+
+
+def kernel_probe(torch, mezo, synth, w, ps, args):
+    """One of the set's standalone kernels alone, `steps` launches back to back
+    after `warmup` (for kernel traces and counters): the checksum of the whole
+    set (a read-only stream), or the conversions of an NF4 set's largest
+    tensor (the embedding) to bf16 and back."""
+    stream = torch.cuda.current_stream()
+    if args.probe == "checksum":
+        ck = torch.empty(1, dtype=torch.int64, device="cuda")
+        moved = w.numel * storage_bytes(w)
+
+        def one():
+            ps.checksum_into(ck, stream=stream)
+    else:
+        if w.dtype != synth.NF4:
+            raise SystemExit(f"--probe {args.probe} needs an NF4 workload")
+        big = max(ps.tensors, key=lambda t: t.numel())
+        n = big.numel()
+        vals = mezo.nf4_dequantize(big, dtype=torch.bfloat16, stream=stream)
+        spare = mezo.NF4Tensor.empty(n, big.device)
+        moved = (n + 1) // 2 + 4 * ((n + synth.NF4_BLOCK - 1) // synth.NF4_BLOCK) + 2 * n
+        if args.probe == "nf4-dequantize":
+            def one():
+                mezo.nf4_dequantize(big, out=vals, stream=stream)
+        else:
+            def one():
+                mezo.nf4_quantize(vals, out=spare, stream=stream)
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(args.steps):
+        one()
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    print(json.dumps({"probe": args.probe, "workload": w.name, "bytes_per_call": moved, "ms": ms,
+                      "GBps": moved / (ms / 1e3) / 1e9,
+                      "hbm_frac": moved / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 
 
 def host_cores():

@@ -6,7 +6,6 @@
 #include <atomic>
 
 #include "checksum_launch.hpp"
-#include "nf4.hpp"
 #include "stream_io.hpp"
 #include "tiles.hpp"
 
@@ -39,85 +38,150 @@ __device__ __forceinline__ void add_workgroup_sum(uint64_t sum, unsigned long lo
     }
 }
 
-// One lane's share of a tile that lies wholly inside its tensor (every tile
-// but a tensor's last): no bounds, the tile's scalar base plus a 32-bit lane
-// offset, and chunk numbers as a uniform part plus the lane's constant one.
-template <int kGroups>
-__device__ __forceinline__ uint64_t checksum_full_tile(uint64_t data, uint64_t local, uint64_t cpos_tile,
-                                                       uint64_t tmix, const uint64_t (&cpos_lane)[kGroups])
+// A lane's 16 bytes of a tile that lies wholly inside its tensor: the
+// tile's base plus a 32-bit lane offset, no bounds.
+__device__ __forceinline__ u32x4_t load_whole_tile(uint64_t data, uint64_t local)
 {
-    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(data) + local * (kThreads * kGroups);
-    uint64_t sum = 0;
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-        const u32x4_t v = __builtin_nontemporal_load(base + (uint32_t(g * kThreads) + threadIdx.x));
-        const uint64_t p0 = cpos_tile + cpos_lane[g];  // (its first chunk's number) * kChunkPos
-        const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
-        const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
-        sum += fmix64(lo ^ p0 ^ tmix);
-        sum += fmix64(hi ^ (p0 + kChunkPos) ^ tmix);
-    }
-    return sum;
+    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(data) + local * kThreads;
+    return __builtin_nontemporal_load(base + threadIdx.x);
 }
 
+// The mixes of a lane's two chunks of a whole tile: chunk numbers as the
+// tile's uniform part plus the lane's constant part.
+__device__ __forceinline__ uint64_t mix_whole_tile(u32x4_t v, uint64_t cpos_tile, uint64_t tmix, uint64_t cpos_lane)
+{
+    const uint64_t p0 = cpos_tile + cpos_lane;  // (its first chunk's number) * kChunkPos
+    const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+    const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+    return fmix64(lo ^ p0 ^ tmix) + fmix64(hi ^ (p0 + kChunkPos) ^ tmix);
+}
+
+// A lane's share of a tensor's last tile, which the tensor's end may cut:
+// only the elements that exist, the last chunk zero-padded.
+template <uint32_t kDtype>
+__device__ __forceinline__ uint64_t mix_last_tile(const TensorDesc& d, uint64_t local)
+{
+    constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
+    constexpr uint64_t kEsz = 16 / kPer;
+    const uint64_t nchunks = (d.numel * kEsz + 7) / 8;
+    const uint64_t cbase = d.first * kEsz / 8;  // chunk number of the shard's first byte
+    const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
+    const uint64_t grp = group_index<1>(local, 0);
+    const uint64_t c0 = grp * 2;  // the group's first chunk within the shard
+    if (c0 >= nchunks) return 0;
+    uint4 v;
+    if ((grp + 1) * kPer <= d.numel) {
+        v = load_stream(d.data + grp * 16);
+    } else {
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        if constexpr (kDtype == kF32) {
+            const MEZO_GLOBAL uint32_t* in = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.data);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (grp * 4 + j < d.numel) w[j] = in[grp * 4 + j];
+        } else {
+            const gu16_t* in = reinterpret_cast<const gu16_t*>(d.data);
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (grp * 8 + j < d.numel) w[j >> 1] |= uint32_t(in[grp * 8 + j]) << (16 * (j & 1));
+        }
+        v = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+    const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+    const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+    uint64_t s = fmix64(lo ^ ((cbase + c0) * kChunkPos) ^ tmix);
+    if (c0 + 1 < nchunks) s += fmix64(hi ^ ((cbase + c0 + 1) * kChunkPos) ^ tmix);
+    return s;
+}
+
+// The tensor a run of tiles is in: its descriptor's fields in scalar
+// registers, moved forward tensor by tensor (the tensors of a table lie in
+// tile order, each right after the one before).
+template <uint64_t kTileElems>
+struct RunCursor {
+    const TensorDesc* tensors;
+    uint32_t ti;
+    uint64_t data, numel, first, begin, end;  // end: one past the tensor's last tile
+    uint32_t id;
+
+    __device__ __forceinline__ void load(uint32_t i)
+    {
+        ti = i;
+        data = tensors[i].data;
+        numel = tensors[i].numel;
+        first = tensors[i].first;
+        begin = tensors[i].tile_begin;
+        id = tensors[i].tensor_id;
+        end = begin + (numel + kTileElems - 1) / kTileElems;
+    }
+    __device__ __forceinline__ void seek(uint64_t tile)
+    {
+        while (tile >= end) load(ti + 1);
+    }
+};
+
+// fp32/bf16 tensors. Workgroup b takes the run of consecutive tiles
+// [T b / G, T (b + 1) / G) of the table's T tiles (G workgroups): the
+// descriptor changes only where the run crosses into the next tensor (no
+// per-tile map lookup). Tiles go in pairs where both lie wholly inside one
+// tensor: both loads are issued before either is mixed, two 16-byte loads in
+// flight per lane (four tiles in flight were slower on the large sets).
 template <uint32_t kDtype>
 __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
 {
-    constexpr int kGroups = Layout<kDtype>::kGroups;
+    static_assert(Layout<kDtype>::kGroups == 1, "one 16-byte group per lane");
     constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
     constexpr uint64_t kEsz = 16 / kPer;
-    constexpr uint64_t kTileElems = uint64_t(kThreads) * kGroups * kPer;
-    // chunk number of a lane's group g within its tile, times kChunkPos
-    uint64_t cpos_lane[kGroups];
-#pragma unroll
-    for (int g = 0; g < kGroups; ++g) {
-        cpos_lane[g] = 2 * (uint64_t(g) * kThreads + threadIdx.x) * kChunkPos;
-        // opaque from here on: otherwise the compiler folds uniform + lane
-        // constant back into one per-lane 64-bit multiply in every tile
-        asm("" : "+v"(cpos_lane[g]));
-    }
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kPer;
+    constexpr uint64_t kPair = 2;
+    // chunk number of the lane's first chunk within its tile, times kChunkPos;
+    // opaque from here on: otherwise the compiler folds uniform + lane
+    // constant back into one per-lane 64-bit multiply in every tile
+    uint64_t cpos_lane = 2 * uint64_t(threadIdx.x) * kChunkPos;
+    asm("" : "+v"(cpos_lane));
+    const uint64_t T = a.total_tiles;
+    const uint64_t t0 = T * blockIdx.x / gridDim.x;
+    const uint64_t t_end = T * (blockIdx.x + 1) / gridDim.x;
     uint64_t sum = 0;
-    for (uint64_t tile = blockIdx.x; tile < a.total_tiles; tile += gridDim.x) {
-        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
-        const uint64_t local = tile - d.tile_begin;
-        const uint64_t nbytes = d.numel * kEsz;
-        const uint64_t nchunks = (nbytes + 7) / 8;
-        const uint64_t cbase = d.first * kEsz / 8;  // chunk number of the shard's first byte
-        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
-        if ((local + 1) * kTileElems <= d.numel) {  // uniform
-            const uint64_t cpos_tile = (cbase + 2 * local * (kThreads * kGroups)) * kChunkPos;
-            sum += checksum_full_tile<kGroups>(d.data, local, cpos_tile, tmix, cpos_lane);
-            continue;
-        }
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-            const uint64_t grp = group_index<kGroups>(local, g);
-            const uint64_t c0 = grp * 2;  // the group's first chunk within the shard
-            if (c0 >= nchunks) continue;
-            uint4 v;
-            if ((grp + 1) * kPer <= d.numel) {
-                v = load_stream(d.data + grp * 16);
+    if (t0 < t_end) {
+        RunCursor<kTileElems> c;
+        c.tensors = a.tensors;
+        c.load(a.tile_tensor[t0]);
+        // the chunk-position term of tile `local` of the cursor's tensor
+        const auto cpos_of = [&](uint64_t local) { return (c.first * kEsz / 8 + 2 * local * kThreads) * kChunkPos; };
+        const auto one_tile = [&](uint64_t tile) {
+            c.seek(tile);
+            const uint64_t local = tile - c.begin;
+            if ((local + 1) * kTileElems <= c.numel) {  // uniform: all but a tensor's last tile
+                const u32x4_t v = load_whole_tile(c.data, local);
+                sum += mix_whole_tile(v, cpos_of(local), uint64_t(c.id) * kChunkTensor, cpos_lane);
             } else {
-                // tail: read the elements that exist, zero the rest
-                uint32_t w[4] = {0u, 0u, 0u, 0u};
-                if constexpr (kDtype == kF32) {
-                    const MEZO_GLOBAL uint32_t* in = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.data);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        if (grp * 4 + j < d.numel) w[j] = in[grp * 4 + j];
-                } else {
-                    const gu16_t* in = reinterpret_cast<const gu16_t*>(d.data);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        if (grp * 8 + j < d.numel) w[j >> 1] |= uint32_t(in[grp * 8 + j]) << (16 * (j & 1));
-                }
-                v = make_uint4(w[0], w[1], w[2], w[3]);
+                TensorDesc d;
+                d.data = c.data;
+                d.numel = c.numel;
+                d.first = c.first;
+                d.tensor_id = c.id;
+                sum += mix_last_tile<kDtype>(d, local);
             }
-            const uint64_t lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
-            const uint64_t hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
-            sum += fmix64(lo ^ ((cbase + c0) * kChunkPos) ^ tmix);
-            if (c0 + 1 < nchunks) sum += fmix64(hi ^ ((cbase + c0 + 1) * kChunkPos) ^ tmix);
+        };
+        uint64_t t = t0;
+        for (; t + kPair <= t_end; t += kPair) {
+            c.seek(t);
+            const uint64_t local = t - c.begin;
+            if ((local + kPair) * kTileElems <= c.numel) {  // uniform: both tiles whole, one tensor
+                u32x4_t v[kPair];
+#pragma unroll
+                for (uint64_t j = 0; j < kPair; ++j) v[j] = load_whole_tile(c.data, local + j);
+                const uint64_t cpos = cpos_of(local);
+                const uint64_t tmix = uint64_t(c.id) * kChunkTensor;
+#pragma unroll
+                for (uint64_t j = 0; j < kPair; ++j)
+                    sum += mix_whole_tile(v[j], cpos + j * (2 * kThreads * kChunkPos), tmix, cpos_lane);
+            } else {
+                for (uint64_t j = 0; j < kPair; ++j) one_tile(t + j);
+            }
         }
+        if (t < t_end) one_tile(t);
     }
     add_workgroup_sum(sum, a.out);
 }

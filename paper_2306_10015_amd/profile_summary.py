@@ -13,7 +13,13 @@ listed at the top of every summary).
 FETCH_SIZE and WRITE_SIZE are scaled by what the same counters read for a
 plain device copy of known size (--copy-*), per dispatch. VALU busy follows
 rocprofv3's derived metric, 100 * SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE
-cycles, with GRBM_GUI_ACTIVE summed over the 8 XCDs in the CSV. Instruction
+cycles, with GRBM_GUI_ACTIVE summed over the 8 XCDs in the CSV; it counts a
+cycle in which a second VALU instruction issued beside the first (a
+transcendental on its own unit) twice, so it exceeds 100 where instructions
+co-issue: the main pipe's busy share is that figure times (1 - the
+SQ_ACTIVE_INST_VALU2 share). GRBM_GUI_ACTIVE per XCD over the dispatch's
+duration is the clock it ran at (exact for long dispatches; the counted run's
+durations of short ones include collection overhead). Instruction
 counts are per lane: SQ_INSTS_VALU counts wave instructions, times 64 lanes,
 over the elements (x records for the engine) of the dispatch; transcendental
 ones (SQ_INSTS_VALU_TRANS_F32) are given apart, since they issue on a unit of
@@ -192,9 +198,9 @@ def main():
         per = "param-seed" if recs else "element"
         lines += ["## VALU (rocprofv3 --pmc SQ_ACTIVE_INST_VALU SQ_INSTS_VALU SQ_ACTIVE_INST_VALU2 "
                   "SQ_INSTS_VALU_TRANS_F32 ... GRBM_GUI_ACTIVE)", "",
-                  f"| dispatch | records | ns | VALU busy % | dual-issue share % | VALU instr per {per} | "
-                  f"of them transcendental | non-transcendental |",
-                  "|---|---|---|---|---|---|---|---|"]
+                  f"| dispatch | records | ns | GHz | VALU busy % | dual-issue share % | main pipe busy % | "
+                  f"VALU instr per {per} | of them transcendental | non-transcendental |",
+                  "|---|---|---|---|---|---|---|---|---|---|"]
         rows = []
         for i, (k, e) in enumerate(v.items()):
             cyc = e["GRBM_GUI_ACTIVE"] / XCDS
@@ -204,16 +210,19 @@ def main():
             units = a.elements * (r if recs else 1)
             ips = e["SQ_INSTS_VALU"] * 64 / units
             tps = e.get("SQ_INSTS_VALU_TRANS_F32", 0.0) * 64 / units
-            rows.append((r, busy, dual, ips, tps))
-            lines.append(f"| {k} | {r if recs else '-'} | {e['ns']} | {busy:.1f} | {dual:.1f} | {ips:.3f} | "
-                         f"{tps:.3f} | {ips - tps:.3f} |")
+            ghz = cyc / e["ns"]
+            rows.append((r, busy, dual, ips, tps, ghz))
+            lines.append(f"| {k} | {r if recs else '-'} | {e['ns']} | {ghz:.2f} | {busy:.1f} | {dual:.1f} | "
+                         f"{busy * (1 - dual / 100):.1f} | {ips:.3f} | {tps:.3f} | {ips - tps:.3f} |")
         lines.append("")
         by = collections.defaultdict(list)
-        for r, busy, dual, ips, tps in rows:
-            by[r].append((busy, dual, ips, tps))
+        for r, busy, dual, ips, tps, ghz in rows:
+            by[r].append((busy, dual, ips, tps, ghz))
         summary["valu_by_records"] = {
             str(r): {"busy_pct": sum(x[0] for x in vals) / len(vals),
                      "dual_issue_pct": sum(x[1] for x in vals) / len(vals),
+                     "main_pipe_busy_pct": sum(x[0] * (1 - x[1] / 100) for x in vals) / len(vals),
+                     "clock_ghz": sum(x[4] for x in vals) / len(vals),
                      f"instr_per_{per.replace('-', '_')}": sum(x[2] for x in vals) / len(vals),
                      f"trans_per_{per.replace('-', '_')}": sum(x[3] for x in vals) / len(vals)}
             for r, vals in by.items()}
