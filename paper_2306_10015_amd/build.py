@@ -9,6 +9,7 @@ portable Gaussian relies on them), and packed fp32 instructions disabled.
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -38,15 +39,41 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def _run(cmd):
+def _run(cmd) -> list[str]:
+    """Run a compiler command; returns its kernel resource remarks."""
     r = subprocess.run(cmd, capture_output=True, text=True)
     # hipcc's host pass reports the device-only feature flag as unknown: harmless
     noise = "'-packed-fp32-ops' is not a recognized feature"
-    err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
+    lines = [l for l in r.stderr.splitlines() if noise not in l]
+    remarks = [l for l in lines if RESOURCE_REMARK in l]
+    # the remarks' source excerpts ("  42 | {", "     | ^") go with them
+    err = "\n".join(l for l in lines if RESOURCE_REMARK not in l and not _EXCERPT.match(l))
     if r.returncode != 0:
         raise RuntimeError(f"command failed: {' '.join(cmd)}\n{err}")
     if err.strip():
         sys.stderr.write(err + "\n")
+    return remarks
+
+
+RESOURCE_REMARK = "-Rpass-analysis=kernel-resource-usage"
+_EXCERPT = re.compile(r"^\s*\d*\s*\|")
+_REMARK_FIELD = re.compile(r"remark:\s+([A-Za-z ]+?)(?: \[[^]]*\])?:\s+(\S+)")
+
+
+def kernel_resources(remarks: list[str]) -> list[dict]:
+    """One entry per kernel from the compiler's resource-usage remarks: its
+    name, VGPRs, scratch bytes per lane and occupancy (waves per SIMD)."""
+    out: list[dict] = []
+    for line in remarks:
+        m = _REMARK_FIELD.search(line)
+        if not m:
+            continue
+        key, val = m.group(1).strip(), m.group(2)
+        if key == "Function Name":
+            out.append({"kernel": val})
+        elif out and key in ("VGPRs", "ScratchSize", "Occupancy"):
+            out[-1][key] = int(val)
+    return out
 
 
 #: The kernel translation units of libmezo, one object each.
@@ -61,10 +88,22 @@ def build(verbose: bool = False) -> Path:
     BUILD_DIR.mkdir(exist_ok=True)
     cc = hipcc()
     objs = []
+    table = []
     for unit in KERNEL_UNITS:
         obj = BUILD_DIR / (Path(unit).stem + ".o")
-        _run([cc, *COMMON, *DEVICE, "-c", str(CSRC / unit), "-o", str(obj)])
+        remarks = _run([cc, *COMMON, *DEVICE, RESOURCE_REMARK, "-c", str(CSRC / unit), "-o", str(obj)])
+        table += [dict(unit=unit, **k) for k in kernel_resources(remarks)]
         objs.append(str(obj))
+    # every kernel keeps its values in registers: a spill to per-lane scratch
+    # memory is a build error
+    with open(BUILD_DIR / "kernel_resources.txt", "w") as f:
+        for k in table:
+            f.write(f"{k['unit']} {k['kernel']} vgprs={k.get('VGPRs')} scratch={k.get('ScratchSize')} "
+                    f"waves_per_simd={k.get('Occupancy')}\n")
+    spills = [k for k in table if k.get("ScratchSize", 0) > 0]
+    if not table or spills:
+        raise RuntimeError("kernels using scratch memory: "
+                           + (", ".join(k["kernel"] for k in spills) if table else "(no resource remarks)"))
     a_obj = BUILD_DIR / "api.o"
     _run([cc, *COMMON, "-c", str(CSRC / "api.cpp"), "-o", str(a_obj)])
     tmp = LIB.with_suffix(".so.tmp")

@@ -148,7 +148,7 @@ __device__ __forceinline__ void short_records(const EngineArgs& a, const TensorD
 // records (out of place with nothing to apply) a tile is copied. Compiled for
 // 8 waves per SIMD (at most 64 VGPRs), the occupancy of the other kernels.
 template <bool kPortable>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8, 8)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kPortable ? 1 : 8, 8)))
 void engine_nf4_short_kernel(EngineArgs a)
 {
     const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table

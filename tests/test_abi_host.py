@@ -366,3 +366,35 @@ def test_header_is_plain_c_and_cpp(tmp_path, compiler, std):
     r = subprocess.run([compiler, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
                         "-I", os.path.join(ROOT, "include"), str(src)], capture_output=True, text=True)
     assert r.returncode == 0, r.stderr
+
+
+def test_kernel_resource_remarks_parse():
+    """The build reads VGPRs, scratch and occupancy per kernel from the
+    compiler's resource-usage remarks (the spill check rests on it)."""
+    from paper_2306_10015_amd import build as b
+    tag = " [-Rpass-analysis=kernel-resource-usage]"
+    remarks = [f"x.hip:1:1: remark: Function Name: _Z1kv{tag}",
+               f"x.hip:1:1: remark:     VGPRs: 40{tag}",
+               f"x.hip:1:1: remark:     ScratchSize [bytes/lane]: 8{tag}",
+               f"x.hip:1:1: remark:     Occupancy [waves/SIMD]: 8{tag}",
+               f"x.hip:1:1: remark: Function Name: _Z1jv{tag}",
+               f"x.hip:1:1: remark:     VGPRs: 12{tag}",
+               f"x.hip:1:1: remark:     ScratchSize [bytes/lane]: 0{tag}"]
+    assert b.kernel_resources(remarks) == [
+        {"kernel": "_Z1kv", "VGPRs": 40, "ScratchSize": 8, "Occupancy": 8},
+        {"kernel": "_Z1jv", "VGPRs": 12, "ScratchSize": 0}]
+
+
+def test_no_kernel_spills_to_scratch():
+    """Every kernel of the last build keeps its values in registers (the
+    build records each kernel's resources and refuses a spill)."""
+    from paper_2306_10015_amd import build as b
+    path = b.BUILD_DIR / "kernel_resources.txt"
+    if not path.exists():
+        pytest.skip("no in-tree build record (run python -m paper_2306_10015_amd.build)")
+    rows = [l.split() for l in path.read_text().splitlines() if l.strip()]
+    assert {r[0] for r in rows} == set(b.KERNEL_UNITS)
+    for r in rows:
+        fields = dict(kv.split("=") for kv in r[2:])
+        assert fields["scratch"] == "0", r
+        assert int(fields["vgprs"]) <= 128, r
