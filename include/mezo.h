@@ -293,6 +293,8 @@ MEZO_API int mezo_replay(mezo_paramset_t ps, const mezo_step_t* steps, uint32_t 
  *     several calls on one stream);
  *   - ps must already have device tables on the current device, which its
  *     first call of any other engine entry point creates (else MEZO_EINVAL);
+ *     that set-up also finds the array's address on the device, so this call
+ *     makes only kernel launches and may be captured into a HIP graph;
  *   - the array is shared by every call on a GPU and keeps the last call's
  *     records (nothing in it needs clearing: a call writes every record it
  *     reads): two calls whose work may overlap on one GPU — on different

@@ -277,6 +277,11 @@ int ensure_device(mezo_paramset* ps)
     }
     for (size_t i = 0; i < mezo_paramset::kUses && e == hipSuccess; ++i)
         e = hipEventCreateWithFlags(&ps->uses[i].done, hipEventDisableTiming);
+    // the device address of mezo_replay_noalloc's staging array, resolved at
+    // set-up (once per device, cached), so that entry point makes no such
+    // query itself, also not under graph capture
+    mezo::SeedRec* staging = nullptr;
+    if (e == hipSuccess) e = mezo::noalloc_scratch(&staging);
     if (e != hipSuccess) {
         for (int dt = 0; dt < mezo_paramset::kTypes; ++dt) {
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);

@@ -121,3 +121,39 @@ def test_short_lists_and_limits(mz):
         assert np.array_equal(x, y)
     ps_a.close()
     ps_b.close()
+
+
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
+def test_graph_capture_of_a_long_replay(mz):
+    """A replay of 256 records (past what the kernel arguments carry) captured
+    into a HIP graph through mezo_replay_noalloc: the staging launches and the
+    engine launch are recorded, nothing is allocated, and each of three
+    replays, with eager work and synchronisations in between (one of them an
+    eager no-alloc call over the same staging array), applies the log again,
+    bit-identical to mezo_replay on a twin set."""
+    import torch
+    sizes = [(70001, "f32"), (4099, "bf16"), (64 * 9 + 5, "nf4")]
+    a = mixed_set(mz, sizes, seed=4)
+    b = clone(mz, a)
+    ps_a, ps_b = mz.ParamSet(a), mz.ParamSet(b)
+    ps_a.perturb((9, 0, 0), 1e-3)   # the first call creates the device tables
+    ps_b.perturb((9, 0, 0), 1e-3)
+    steps = log(4, 16, 4, 1e-3, seed=21)   # 4 x 64 = 256 records
+    other = mz.ParamSet(mixed_set(mz, [(3000, "bf16")], seed=5))
+    other.perturb((9, 0, 0), 1e-3)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ps_a.replay_noalloc(steps)
+    torch.cuda.synchronize()
+    for i in range(3):
+        g.replay()
+        ps_b.replay(steps)
+        torch.cuda.synchronize()
+        torch.randn(4096, device="cuda").sum().item()   # eager work between replays
+        other.replay_noalloc(log(2, 8, 4, 1e-3, seed=60 + i))   # rewrites the staging array
+        torch.cuda.synchronize()
+        for x, y in zip(bits(mz, a), bits(mz, b)):
+            assert np.array_equal(x, y), f"graph replay {i}"
+    for p in (ps_a, ps_b, other):
+        p.close()
