@@ -111,6 +111,8 @@ def parse():
                         "streaming read-modify-write of it with the engine's access pattern (the sweep's "
                         "memory ceiling); checksum: the set's checksum alone; nf4-dequantize / "
                         "nf4-quantize: an NF4 set's largest tensor converted to bf16 and back")
+    p.add_argument("--conv-dtype", choices=["bf16", "f32"], default="bf16",
+                   help="nf4-dequantize / nf4-quantize probes: the dense side's type")
     p.add_argument("--rmw-groups", type=int, choices=[1, 2], default=None,
                    help="rmw probe: 16-byte groups per lane (default 1, the engine's)")
     p.add_argument("--rmw-lanes", type=int, choices=[128, 256, 512], default=256,
@@ -595,7 +597,7 @@ def kernel_probe(torch, mezo, synth, w, ps, args):
     """One of the set's standalone kernels alone, `steps` launches back to back
     after `warmup` (for kernel traces and counters): the checksum of the whole
     set (a read-only stream), or the conversions of an NF4 set's largest
-    tensor (the embedding) to bf16 and back."""
+    tensor (the embedding) to bf16 (or fp32: --conv-dtype) and back."""
     stream = torch.cuda.current_stream()
     if args.probe == "checksum":
         ck = torch.empty(1, dtype=torch.int64, device="cuda")
@@ -608,9 +610,10 @@ def kernel_probe(torch, mezo, synth, w, ps, args):
             raise SystemExit(f"--probe {args.probe} needs an NF4 workload")
         big = max(ps.tensors, key=lambda t: t.numel())
         n = big.numel()
-        vals = mezo.nf4_dequantize(big, dtype=torch.bfloat16, stream=stream)
+        dense = torch.float32 if args.conv_dtype == "f32" else torch.bfloat16
+        vals = mezo.nf4_dequantize(big, dtype=dense, stream=stream)
         spare = mezo.NF4Tensor.empty(n, big.device)
-        moved = (n + 1) // 2 + 4 * ((n + synth.NF4_BLOCK - 1) // synth.NF4_BLOCK) + 2 * n
+        moved = (n + 1) // 2 + 4 * ((n + synth.NF4_BLOCK - 1) // synth.NF4_BLOCK) + vals.element_size() * n
         if args.probe == "nf4-dequantize":
             def one():
                 mezo.nf4_dequantize(big, out=vals, stream=stream)
@@ -628,7 +631,9 @@ def kernel_probe(torch, mezo, synth, w, ps, args):
     b.record(stream)
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / args.steps
-    print(json.dumps({"probe": args.probe, "workload": w.name, "bytes_per_call": moved, "ms": ms,
+    print(json.dumps({"probe": args.probe, "workload": w.name,
+                      **({} if args.probe == "checksum" else {"dense_dtype": args.conv_dtype}),
+                      "bytes_per_call": moved, "ms": ms,
                       "GBps": moved / (ms / 1e3) / 1e9,
                       "hbm_frac": moved / (ms / 1e3) / 1e9 / HBM_PEAK_GBS}))
 

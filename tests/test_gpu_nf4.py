@@ -18,7 +18,7 @@ from paper_2306_10015_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-SIZES = [1, 7, 64, 65, 2048, 4097, 70001]
+SIZES = [1, 7, 64, 65, 2048, 4097, 8192, 8 * 2048 * 3 + 5, 70001]
 
 
 @pytest.fixture(scope="module")
