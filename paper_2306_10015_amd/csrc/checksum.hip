@@ -101,13 +101,14 @@ template <uint64_t kTileElems>
 struct RunCursor {
     const TensorDesc* tensors;
     uint32_t ti;
-    uint64_t data, numel, first, begin, end;  // end: one past the tensor's last tile
+    uint64_t data, aux, numel, first, begin, end;  // end: one past the tensor's last tile
     uint32_t id;
 
     __device__ __forceinline__ void load(uint32_t i)
     {
         ti = i;
         data = tensors[i].data;
+        aux = tensors[i].aux;
         numel = tensors[i].numel;
         first = tensors[i].first;
         begin = tensors[i].tile_begin;
@@ -186,14 +187,69 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
     add_workgroup_sum(sum, a.out);
 }
 
+// A wave's share of an NF4 tensor's last tile, which the tensor's end may cut:
+// the code chunks and absmax chunks that exist, the last of each zero-padded.
+__device__ __forceinline__ uint64_t mix_nf4_last_tile(uint64_t data, uint64_t aux, uint64_t numel, uint64_t tmix,
+                                                      uint64_t local, uint32_t lane)
+{
+    const uint64_t cbytes = (numel + 1) / 2;
+    const uint64_t cchunks = (cbytes + 7) / 8;
+    const uint64_t abytes = 4 * ((numel + kNF4Block - 1) / kNF4Block);
+    uint64_t sum = 0;
+    // codes: bytes [16u, 16u + 16) = chunks 2u, 2u + 1
+    const uint64_t u = local * 64 + lane;
+    if (16 * u < cbytes) {
+        uint64_t lo = 0, hi = 0;
+        if (16 * u + 16 <= cbytes) {
+            const uint4 v = load_stream(data + 16 * u);
+            lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
+            hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+        } else {
+            const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(data);
+            for (uint64_t k = 16 * u; k < cbytes; ++k) {
+                const uint64_t byte = uint64_t(b[k]);
+                const uint64_t off = k - 16 * u;
+                if (off < 8)
+                    lo |= byte << (8 * off);
+                else
+                    hi |= byte << (8 * (off - 8));
+            }
+        }
+        sum += fmix64(lo ^ (2 * u * kChunkPos) ^ tmix);
+        if (16 * u + 8 < cbytes) sum += fmix64(hi ^ ((2 * u + 1) * kChunkPos) ^ tmix);
+    }
+    // absmax: bytes [ab, ab + 16) = absmax chunks k0, k0 + 1
+    const uint64_t ab = local * (kTileNF4 / kNF4Block * 4) + 16 * uint64_t(lane);
+    if (lane < kTileNF4 / kNF4Block * 4 / 16 && ab < abytes) {
+        const uint64_t k0 = ab / 8;
+        uint32_t f[4] = {0u, 0u, 0u, 0u};
+        if (ab + 16 <= abytes) {
+            const uint4 v = load_stream(aux + ab);
+            f[0] = v.x;
+            f[1] = v.y;
+            f[2] = v.z;
+            f[3] = v.w;
+        } else {
+            const MEZO_GLOBAL uint32_t* am = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(aux);
+            for (uint64_t k = ab; k < abytes; k += 4) f[(k - ab) / 4] = am[k / 4];
+        }
+        sum += fmix64((uint64_t(f[0]) | (uint64_t(f[1]) << 32)) ^ ((cchunks + k0) * kChunkPos) ^ tmix);
+        if (ab + 8 < abytes)
+            sum += fmix64((uint64_t(f[2]) | (uint64_t(f[3]) << 32)) ^ ((cchunks + k0 + 1) * kChunkPos) ^ tmix);
+    }
+    return sum;
+}
+
 // NF4 tensors: the code bytes zero-padded to whole chunks, then the absmax
-// values, chunk numbers continuing. One wave per tile of 2048 elements: every
-// lane reads 16 code bytes (two chunks) and lanes 0..7 also 16 bytes of the
-// tile's 128 absmax bytes.
+// values, chunk numbers continuing. A tile of 2048 elements is one wave's:
+// every lane reads 16 code bytes (two chunks) and lanes 0..15 a chunk of the
+// tile's 128 absmax bytes. Wave w of W takes the run of consecutive tiles
+// [T w / W, T (w + 1) / W), with its tensor's descriptor moved forward only
+// where the run crosses into the next tensor, two whole tiles at a time.
 __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
 {
     constexpr uint32_t kWaves = kThreads / 64;
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    constexpr uint64_t kPair = 2;
     const uint32_t lane = threadIdx.x & 63u;
     // position terms of a lane's chunks within a tile, computed once (opaque
     // to the compiler, as in checksum_kernel): code chunks 2 lane, 2 lane + 1;
@@ -202,70 +258,66 @@ __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
     uint64_t cpos_abs = uint64_t(lane & 15u) * kChunkPos;
     asm("" : "+v"(cpos_code));
     asm("" : "+v"(cpos_abs));
+    const uint64_t W = uint64_t(gridDim.x) * kWaves;
+    const uint64_t gw = uint64_t(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint64_t T = a.total_tiles;
+    const uint64_t t0 = T * gw / W;
+    const uint64_t t_end = T * (gw + 1) / W;
     uint64_t sum = 0;
-    for (uint64_t tile = uint64_t(blockIdx.x) * kWaves + wave; tile < a.total_tiles;
-         tile += uint64_t(gridDim.x) * kWaves) {
-        const TensorDesc d = a.tensors[a.tile_tensor[tile]];
-        const uint64_t local = tile - d.tile_begin;
-        const uint64_t cbytes = (d.numel + 1) / 2;
-        const uint64_t cchunks = (cbytes + 7) / 8;
-        const uint64_t abytes = 4 * ((d.numel + kNF4Block - 1) / kNF4Block);
-        const uint64_t tmix = uint64_t(d.tensor_id) * kChunkTensor;
-        if ((local + 1) * kTileNF4 <= d.numel) {  // uniform: a whole tile, 32 whole blocks
-            const gu32x4_t* codes = reinterpret_cast<const gu32x4_t*>(d.data) + local * 64;
-            const u32x4_t v = __builtin_nontemporal_load(codes + lane);
-            // the tile's 128 absmax bytes as 16 chunks on lanes 0..15; every
-            // lane loads (lane mod 16), so that both loads issue before any mix
-            const MEZO_GLOBAL uint64_t* am = reinterpret_cast<const MEZO_GLOBAL uint64_t*>(d.aux) + local * 16;
-            const uint64_t f = __builtin_nontemporal_load(am + (lane & 15u));
+    if (t0 < t_end) {
+        RunCursor<kTileNF4> c;
+        c.tensors = a.tensors;
+        c.load(a.tile_tensor[t0]);
+        // the mixes of whole tile `local` of the cursor's tensor from its
+        // lane's code chunk v and absmax chunk f
+        const auto mix_whole = [&](u32x4_t v, uint64_t f, uint64_t local) {
+            const uint64_t tmix = uint64_t(c.id) * kChunkTensor;
+            const uint64_t cchunks = ((c.numel + 1) / 2 + 7) / 8;
             const uint64_t p0 = 128 * local * kChunkPos + cpos_code;
-            sum += fmix64((uint64_t(v.x) | (uint64_t(v.y) << 32)) ^ p0 ^ tmix);
-            sum += fmix64((uint64_t(v.z) | (uint64_t(v.w) << 32)) ^ (p0 + kChunkPos) ^ tmix);
+            uint64_t s = fmix64((uint64_t(v.x) | (uint64_t(v.y) << 32)) ^ p0 ^ tmix);
+            s += fmix64((uint64_t(v.z) | (uint64_t(v.w) << 32)) ^ (p0 + kChunkPos) ^ tmix);
             const uint64_t fm = fmix64(f ^ ((cchunks + 16 * local) * kChunkPos + cpos_abs) ^ tmix);
-            sum += lane < 16u ? fm : 0u;
-            continue;
-        }
-        // codes: bytes [16u, 16u + 16) = chunks 2u, 2u + 1
-        const uint64_t u = local * 64 + lane;
-        if (16 * u < cbytes) {
-            uint64_t lo = 0, hi = 0;
-            if (16 * u + 16 <= cbytes) {
-                const uint4 v = load_stream(d.data + 16 * u);
-                lo = uint64_t(v.x) | (uint64_t(v.y) << 32);
-                hi = uint64_t(v.z) | (uint64_t(v.w) << 32);
+            return s + (lane < 16u ? fm : 0u);
+        };
+        // every lane loads absmax chunk (lane mod 16), so that both loads of a
+        // tile issue before any mix
+        const auto load_codes = [&](uint64_t local) {
+            return __builtin_nontemporal_load(reinterpret_cast<const gu32x4_t*>(c.data) + local * 64 + lane);
+        };
+        const auto load_absmax = [&](uint64_t local) {
+            return __builtin_nontemporal_load(reinterpret_cast<const MEZO_GLOBAL uint64_t*>(c.aux) + local * 16 +
+                                              (lane & 15u));
+        };
+        const auto one_tile = [&](uint64_t tile) {
+            c.seek(tile);
+            const uint64_t local = tile - c.begin;
+            if ((local + 1) * kTileNF4 <= c.numel) {  // uniform: a whole tile, 32 whole blocks
+                const u32x4_t v = load_codes(local);
+                const uint64_t f = load_absmax(local);
+                sum += mix_whole(v, f, local);
             } else {
-                const MEZO_GLOBAL uint8_t* b = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(d.data);
-                for (uint64_t k = 16 * u; k < cbytes; ++k) {
-                    const uint64_t byte = uint64_t(b[k]);
-                    const uint64_t off = k - 16 * u;
-                    if (off < 8)
-                        lo |= byte << (8 * off);
-                    else
-                        hi |= byte << (8 * (off - 8));
+                sum += mix_nf4_last_tile(c.data, c.aux, c.numel, uint64_t(c.id) * kChunkTensor, local, lane);
+            }
+        };
+        uint64_t t = t0;
+        for (; t + kPair <= t_end; t += kPair) {
+            c.seek(t);
+            const uint64_t local = t - c.begin;
+            if ((local + kPair) * kTileNF4 <= c.numel) {  // uniform: both tiles whole, one tensor
+                u32x4_t v[kPair];
+                uint64_t f[kPair];
+#pragma unroll
+                for (uint64_t j = 0; j < kPair; ++j) {
+                    v[j] = load_codes(local + j);
+                    f[j] = load_absmax(local + j);
                 }
-            }
-            sum += fmix64(lo ^ (2 * u * kChunkPos) ^ tmix);
-            if (16 * u + 8 < cbytes) sum += fmix64(hi ^ ((2 * u + 1) * kChunkPos) ^ tmix);
-        }
-        // absmax: bytes [ab, ab + 16) = absmax chunks k0, k0 + 1
-        const uint64_t ab = local * (kTileNF4 / kNF4Block * 4) + 16 * uint64_t(lane);
-        if (lane < kTileNF4 / kNF4Block * 4 / 16 && ab < abytes) {
-            const uint64_t k0 = ab / 8;
-            uint32_t f[4] = {0u, 0u, 0u, 0u};
-            if (ab + 16 <= abytes) {
-                const uint4 v = load_stream(d.aux + ab);
-                f[0] = v.x;
-                f[1] = v.y;
-                f[2] = v.z;
-                f[3] = v.w;
+#pragma unroll
+                for (uint64_t j = 0; j < kPair; ++j) sum += mix_whole(v[j], f[j], local + j);
             } else {
-                const MEZO_GLOBAL uint32_t* am = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(d.aux);
-                for (uint64_t k = ab; k < abytes; k += 4) f[(k - ab) / 4] = am[k / 4];
+                for (uint64_t j = 0; j < kPair; ++j) one_tile(t + j);
             }
-            sum += fmix64((uint64_t(f[0]) | (uint64_t(f[1]) << 32)) ^ ((cchunks + k0) * kChunkPos) ^ tmix);
-            if (ab + 8 < abytes)
-                sum += fmix64((uint64_t(f[2]) | (uint64_t(f[3]) << 32)) ^ ((cchunks + k0 + 1) * kChunkPos) ^ tmix);
         }
+        if (t < t_end) one_tile(t);
     }
     add_workgroup_sum(sum, a.out);
 }
@@ -301,8 +353,8 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
     if (e != hipSuccess) return e;
     for (int i = 0; i < n_tables; ++i) {
         if (tables[i].total_tiles == 0) continue;
-        // as many workgroups as fill the device (8 per CU), each striding over
-        // tiles (NF4: four tiles at a time, one per wave)
+        // as many workgroups as fill the device (8 per CU), each taking a run
+        // of consecutive tiles (NF4: each of its waves a run of its own)
         const uint64_t per_wg = dtypes[i] == kNF4 ? kThreads / 64 : 1;
         const uint64_t need = (tables[i].total_tiles + per_wg - 1) / per_wg;
         const uint64_t cap = uint64_t(cus) * 8;
