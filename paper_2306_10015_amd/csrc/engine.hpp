@@ -175,10 +175,10 @@ __device__ __forceinline__ Z4 gauss4(uint32_t w0, uint32_t w1, uint32_t w2, uint
 // 754 requires of / and sqrt.
 
 // n / d correctly rounded for normal n, d with a normal quotient and no
-// overflow in the steps (here |n| < 0.5, d in [1.7, 2.5]): the reciprocal from
-// v_rcp_f32 refined once, then two residual corrections of the quotient —
-// the general sequence without its operand scaling and special-value fix-up,
-// which only act outside that range.
+// overflow in the steps (the NF4 quantizer's 1 / m for a block maximum m in
+// [2^-64, 2^64]): the reciprocal from v_rcp_f32 refined once, then two
+// residual corrections of the quotient — the general sequence without its
+// operand scaling and special-value fix-up, which only act outside that range.
 __device__ __forceinline__ float div_rn_normal(float n, float d)
 {
     float y = __builtin_amdgcn_rcpf(d);
@@ -203,32 +203,53 @@ __device__ __forceinline__ float sqrt_rn_normal(float x)
     return r;
 }
 
+// (m - 1) / (m + 1) correctly rounded for the m of the transform below: the
+// reciprocal from v_rcp_f32 refined once, then one residual correction of the
+// quotient (Markstein's scheme). That this rounds correctly for every m the
+// transform meets (one per value of u1) is checked exhaustively: the GPU's z
+// is bit-identical to the oracle's, which divides with IEEE /, over all 2^24
+// values of u1.
+__device__ __forceinline__ float div_rn_transform(float n, float d)
+{
+    float y = __builtin_amdgcn_rcpf(d);
+    y = __builtin_fmaf(__builtin_fmaf(-d, y, 1.0f), y, y);
+    const float q = n * y;
+    return __builtin_fmaf(__builtin_fmaf(-d, q, n), y, q);
+}
+
 __device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t wb, float& zc, float& zs)
 {
-    const uint32_t n1 = (wa >> 8) + 1u;                     // u1 = n1 2^-24, n1 >= 1
-    int e = 31 - __builtin_clz(n1);                         // floor(log2 n1)
-    float m = __builtin_ldexpf(float(n1), -e);              // exact, [1, 2)
-    if (m >= 0x1.6a09e6p+0f) {                              // fl32(sqrt 2)
-        m = m * 0.5f;
-        e = e + 1;
-    }
+    // u1 = n1 2^-24 (n1 >= 1) = m 2^(e - 24) with m in [sqrt(1/2), sqrt(2)):
+    // float(n1) is exact (n1 <= 2^24), and so are its mantissa mp in [1/2, 1)
+    // and exponent ep (n1 = mp 2^ep); m is mp, or 2 mp below fl32(sqrt 2) / 2
+    const float fn = float((wa >> 8) + 1u);
+    const float mp = __builtin_amdgcn_frexp_mantf(fn);
+    const int ep = __builtin_amdgcn_frexp_expf(fn);
+    const bool upper = mp >= 0x1.6a09e6p-1f;                // fl32(sqrt 2) / 2
+    const float m = upper ? mp : mp + mp;
+    const int e = upper ? ep : ep - 1;
     const float f = m - 1.0f;                               // exact
-    const float s = div_rn_normal(f, f + 2.0f);
+    const float s = div_rn_transform(f, f + 2.0f);
     const float s2 = s * s;
     float p = __builtin_fmaf(s2, 0x1.c71c72p-4f, 0x1.24924ap-3f);  // 1/9, 1/7
     p = __builtin_fmaf(s2, p, 0x1.99999ap-3f);              // 1/5
     p = __builtin_fmaf(s2, p, 0x1.555556p-2f);              // 1/3
     p = __builtin_fmaf(s2, p, 1.0f);
-    const float ln_m = (s + s) * p;
-    const float ln_u1 = __builtin_fmaf(float(e - 24), 0x1.62e430p-1f, ln_m);  // + (e-24) ln 2
-    const float r = sqrt_rn_normal(-2.0f * ln_u1);
+    // ln m = fl32((s + s) p) and ln u1 = fl32((e - 24) fl32(ln 2) + ln m), each
+    // carried here times -2, which is exact: a scaling by -2 changes no rounding
+    const float m2ln_m = (s * -4.0f) * p;
+    const float m2ln_u1 = __builtin_fmaf(float(e - 24), -0x1.62e430p+0f, m2ln_m);
+    const float r = sqrt_rn_normal(m2ln_u1);            // sqrt(-2 ln u1)
 
-    const uint32_t t = wb >> 8;                             // u2 = t 2^-24
-    const float v = __builtin_ldexpf(float(t), -21);        // 8 u2, exact, [0, 8)
-    const int q = int(v);                                   // octant
-    const float x = v - float(q);                           // exact, [0, 1)
-    const float y = (q & 1) ? 1.0f - x : x;                 // exact, [0, 1]
-    const float a = y * 0x1.921fb6p-1f;                     // fl32(pi/4)
+    // u2 = t 2^-24 with t = wb >> 8: the octant q = floor(8 u2) is t's top
+    // three bits; x = 8 u2 - q, or 1 - x in odd octants, is y = yl 2^-21 with
+    // yl the low 21 bits of t or 2^21 minus them (exact, in integers); and
+    // a = fl32(y fl32(pi/4)) = fl32(yl K), K = fl32(pi/4) 2^-21, since a power
+    // of two scaling changes no rounding here
+    const uint32_t q = wb >> 29;                            // octant
+    const uint32_t tl = (wb >> 8) & 0x1FFFFFu;
+    const uint32_t yl = (q & 1u) ? 0x200000u - tl : tl;     // [0, 2^21]
+    const float a = float(yl) * 0x1.921fb6p-22f;            // fl32(pi/4) 2^-21
     const float a2 = a * a;
     float sn = __builtin_fmaf(a2, 0x1.71de3ap-19f, -0x1.a01a02p-13f);  // 1/9!, -1/7!
     sn = __builtin_fmaf(a2, sn, 0x1.111112p-7f);            // 1/5!
@@ -241,9 +262,9 @@ __device__ __forceinline__ void box_muller_pair_portable(uint32_t wa, uint32_t w
     cs = __builtin_fmaf(a2, cs, -0.5f);                     // -1/2!
     cs = __builtin_fmaf(a2, cs, 1.0f);
     // angle = q pi/4 + a for even q, (q + 1) pi/4 - a for odd q
-    const bool swap = ((q + 1) >> 1) & 1;                   // octants 1, 2, 5, 6
-    const bool neg_cos = ((q + 2) >> 2) & 1;                // octants 2..5
-    const bool neg_sin = (q >> 2) & 1;                      // octants 4..7
+    const bool swap = (0x66u >> q) & 1u;                    // octants 1, 2, 5, 6
+    const bool neg_cos = (0x3Cu >> q) & 1u;                 // octants 2..5
+    const bool neg_sin = (q >> 2) & 1u;                     // octants 4..7
     float c0 = swap ? sn : cs;
     float s0 = swap ? cs : sn;
     if (neg_cos) c0 = -c0;
