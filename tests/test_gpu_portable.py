@@ -1,7 +1,8 @@
 """The portable mode on the GPU is bit-identical to the CPU oracle's binary32
 definition (Appendix B: every device regenerates the same noise): the
 Gaussians themselves, and the weights after perturb, fused updates and replay,
-for fp32 and bf16 storage, small ragged sets and the full 125M set."""
+for fp32 and bf16 storage, small ragged sets, the full 125M set and the full
+6.7B bf16 set (sampled elements) with an update that moves the weights."""
 import numpy as np
 import pytest
 
@@ -110,6 +111,45 @@ def test_portable_full_125m_update_bit_exact(mz, orc):
         ref = orc.perturb(b.copy(), tid, (0, 0, 0), w.eps, idx=ix, portable=True)
         orc.update(ref, tid, seeds, q, w.lr, idx=ix, portable=True)
         assert np.array_equal(bits(a), bits(ref)), f"tensor {tid}"
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
+
+
+def test_portable_full_6p7b_update_bit_exact(mz, orc):
+    """The 6.7B bf16 set (323 tensors, the bench's launch configuration) in
+    portable mode: perturb +eps, then a K = 64 update at lr = 1e-3 (large
+    enough that most bf16 weights change), bit-identical to the oracle's
+    binary32 definition on every sampled element (the first and last 48 of
+    each tensor and 8 random blocks)."""
+    import torch
+    w = synth.WORKLOADS["opt6.7b"]
+    tensors = theta_on_device(w, seed=3, device_rng=True)
+    ps = mz.ParamSet(tensors, gaussian=mz.GAUSS_PORTABLE)
+    rng = np.random.Generator(np.random.PCG64(9))
+    idx = [synth.sample_indices(t.numel(), rng, edge=48, blocks=8) for t in tensors]
+
+    def gather():
+        return [to_host(t.index_select(0, torch.from_numpy(ix.astype(np.int64)).cuda()))
+                for t, ix in zip(tensors, idx)]
+
+    before = gather()
+    seeds = synth.workload_seeds(w)
+    q = synth.grads_int8(w.K, seed=4)
+    ps.perturb((0, 5, 0), w.eps)
+    ps.update_multi(seeds, q, 1e-3)
+    sync()
+    after = gather()
+    changed = total = 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        perturbed = orc.perturb(b.copy(), tid, (0, 5, 0), w.eps, idx=ix, portable=True)
+        ref = orc.update(perturbed.copy(), tid, seeds, q, 1e-3, idx=ix, portable=True)
+        assert np.array_equal(bits(a), bits(ref)), f"tensor {tid}"
+        changed += int(np.sum(ref != perturbed))   # moved by the update itself
+        total += ref.size
+    print(f"opt6.7b portable perturb + K=64 update at lr=1e-3: {total} sampled elements bit-exact, "
+          f"{changed} changed by the update")
+    assert changed > total // 2
     ps.close()
     del tensors
     torch.cuda.empty_cache()
