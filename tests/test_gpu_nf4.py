@@ -265,10 +265,13 @@ def test_checksum_of_nf4_tensors(mz, orc, nf4):
     ps.close()
 
 
-def test_full_size_nf4_6p7b(mz, orc, nf4):
+@pytest.mark.parametrize("portable", [False, True])
+def test_full_size_nf4_6p7b(mz, orc, nf4, portable):
     """The 6.7B-shaped set in 4-bit storage (3.3 GB of codes), perturb and the
     K = 64 update, on sampled blocks (first, last and 16 random blocks of every
-    tensor), fast mode."""
+    tensor): within the fast-mode rule, or bit-exact in portable mode, where
+    the two-record pass (restore of one sample fused with the next sample's
+    perturbation, requantized after each) is checked too."""
     import torch
     w = synth.WORKLOADS["opt6.7b-nf4"]
     g = torch.Generator(device="cuda")
@@ -279,7 +282,7 @@ def test_full_size_nf4_6p7b(mz, orc, nf4):
         codes = torch.randint(0, 256, ((n + 1) // 2,), generator=g, device="cuda", dtype=torch.int32).to(torch.uint8)
         absmax = torch.rand(((n + 63) // 64,), generator=g, device="cuda") * 0.02 + 0.04
         dev.append(mz.NF4Tensor(codes, absmax, n))
-    ps = mz.ParamSet(dev)
+    ps = mz.ParamSet(dev, gaussian=mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST)
     rng = np.random.Generator(np.random.PCG64(11))
     picks = []
     for t in dev:
@@ -295,24 +298,36 @@ def test_full_size_nf4_6p7b(mz, orc, nf4):
             out.append((nf4.unpack(p, p.size * 2), t.absmax.index_select(0, bi).cpu().numpy()))
         return out
 
-    s = (0, 0, 0)
+    s, s2 = (0, 0, 0), (0, 0, 1)
     seeds = synth.workload_seeds(w)
     q = synth.grads_int8(w.K, w.grad_kind, seed=1)
-    for what, op, app in [
+    ops = [
         ("perturb", lambda: ps.perturb(s, w.eps),
-         lambda tid: (lambda v, ix: orc.perturb(v, tid, s, w.eps, idx=ix))),
+         lambda tid: [lambda v, ix: orc.perturb(v, tid, s, w.eps, idx=ix, portable=portable)]),
         (f"update K={w.K}", lambda: ps.update_multi(seeds, q, w.lr),
-         lambda tid: (lambda v, ix: orc.update(v, tid, seeds, q, w.lr, idx=ix))),
-    ]:
+         lambda tid: [lambda v, ix: orc.update(v, tid, seeds, q, w.lr, idx=ix, portable=portable)]),
+    ]
+    if portable:
+        ops.append(("restore + next perturb", lambda: ps.perturb_multi([s, s2], [w.eps, w.eps]),
+                    lambda tid: [lambda v, ix: orc.perturb(v, tid, s, w.eps, idx=ix, portable=True),
+                                 lambda v, ix: orc.perturb(v, tid, s2, w.eps, idx=ix, portable=True)]))
+    for what, op, apps in ops:
         before = gather()
         op()
         torch.cuda.synchronize()
         after = gather()
         differing = 0
         for tid, (t, b, st, got) in enumerate(zip(dev, picks, before, after)):
-            r = compare_step(nf4, got, st, t.numel(), tid, app(tid), False, f"{what} tensor {tid}", blocks=b)
-            differing += r["codes_differing"]
-        print(f"6.7B nf4 {what}: codes differing from the oracle near a midpoint: {differing}")
+            steps = apps(tid)
+            # every step but the last: the oracle's own requantized state
+            for app in steps[:-1]:
+                wv = nf4.dequantize(st[0], st[1], t.numel(), b)
+                app(wv, nf4.block_elements(t.numel(), b))
+                st = nf4.quantize(wv, t.numel(), b)
+            r = compare_step(nf4, got, st, t.numel(), tid, steps[-1], portable, f"{what} tensor {tid}", blocks=b)
+            differing += r.get("codes_differing", 0)
+        print(f"6.7B nf4 {what} ({'portable, bit-exact' if portable else 'fast'}): codes differing from the "
+              f"oracle near a midpoint: {differing}")
     ps.close()
     del dev
     torch.cuda.empty_cache()
