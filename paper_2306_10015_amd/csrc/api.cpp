@@ -945,6 +945,6 @@ const char* mezo_strerror(int code)
 
 const char* mezo_last_error(void) { return t_last_error; }
 
-int mezo_version(void) { return 400; }
+int mezo_version(void) { return 500; }
 
 }  // extern "C"
