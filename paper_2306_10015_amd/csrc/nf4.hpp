@@ -17,15 +17,16 @@
 //
 // - kNF4Table, 128 bins: b(x) = floor(fl32(64 x + 64)) clamped to [0, 127]
 //   (fma rounds 64 x + 64 once, exactly as the double expression below
-//   rounded to float does); used by the kernels that apply long record lists
-//   and by the conversions.
+//   rounded to float does); used by the kernel that applies long record
+//   lists.
 // - kNF4RoundTable, 129 bins: b(x) = the integer nearest to 64 x + 64 (ties to
 //   even), which one fma gives directly: t = fl32(64 x + kNF4BinMagic),
 //   kNF4BinMagic = 1.5 * 2^23 + 64, lies in [2^23, 2^24) where floats are 1
 //   apart, so t is 64 x + 64 rounded once to the nearest integer plus 1.5 *
 //   2^23, and the bit pattern of t is kNF4BinBase + b. For |x| <= 1 + 2^-23
 //   (every x of a block whose maximum has a normal reciprocal), b is in
-//   [0, 128] with no clamp; used by the kernel for one- and two-record calls.
+//   [0, 128] with no clamp; used by the kernel for one- and two-record calls
+//   and by the standalone quantization.
 #pragma once
 
 #include <stdint.h>

@@ -54,14 +54,16 @@ __device__ __forceinline__ void nf4_quantize_load(const NF4ConvArgs& a, uint64_t
 // Standalone quantization: kQuantTiles tiles of 2048 elements per workgroup.
 __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
 {
-    // one copy of the bin table per wave: a wave fills its own and reads it
+    // one copy of the round-to-nearest bin table per wave (the bin from one
+    // fma, as in the engine's short calls): a wave fills its own and reads it
     // after its writes (one wave's LDS accesses complete in order), so the
     // waves of a workgroup never wait for each other
-    __shared__ NF4Bin wave_bins[kThreads / 64][kNF4Bins];
+    __shared__ NF4Bin wave_bins[kThreads / 64][kNF4RoundBins];
     NF4Bin* bins = wave_bins[threadIdx.x >> 6];
     const uint32_t lane = threadIdx.x & 63u;
-    bins[lane] = kNF4Table.bin[lane];
-    bins[lane + 64] = kNF4Table.bin[lane + 64];
+    bins[lane] = kNF4RoundTable.bin[lane];
+    bins[lane + 64] = kNF4RoundTable.bin[lane + 64];
+    if (lane == 0) bins[128] = kNF4RoundTable.bin[128];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
         for (uint32_t t = 0; t < kQuantTiles; ++t) {
             uint32_t packed;
             float am;
-            nf4_requant<false>(bins, 0xFFu, w[t], packed, am);
+            nf4_requant_round<false>(bins, 0xFFu, w[t], packed, am);
             nf4_store<true>(a.codes, a.absmax, (t0 + t) * kTileNF4 + lane_e, a.n, packed, am);
         }
     } else {
@@ -86,7 +88,7 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
             nf4_quantize_load<false>(a, e0, valid, w);
             uint32_t packed;
             float am;
-            nf4_requant<false>(bins, valid, w, packed, am);
+            nf4_requant_round<false>(bins, valid, w, packed, am);
             nf4_store(a.codes, a.absmax, e0, a.n, packed, am);
         }
     }

@@ -252,9 +252,9 @@ def test_checksum_image(orc, nf4):
 
 def test_kernel_bin_table_is_the_nearest_value_rule(nf4, tmp_path):
     """The kernels' NF4 quantizer looks codes up in a bin table of
-    csrc/nf4.hpp: the floor table (long record lists, conversions) or the
-    round-to-nearest table, its bin read off one fma (short lists' fast path)
-    or clamped (their general path). Replayed on the host over every float x
+    csrc/nf4.hpp: the floor table (long record lists) or the round-to-nearest
+    table, its bin read off one fma (the fast path of short lists and of the
+    standalone quantization) or clamped (their general path). Replayed on the host over every float x
     with |x| <= 1 + 2^-22 and over infinities, NaN and out-of-range values,
     each code equals the number of the oracle's midpoints strictly below x."""
     import shutil
