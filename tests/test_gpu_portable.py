@@ -2,7 +2,8 @@
 definition (Appendix B: every device regenerates the same noise): the
 Gaussians themselves, and the weights after perturb, fused updates and replay,
 for fp32 and bf16 storage, small ragged sets, the full 125M set and the full
-6.7B bf16 set (sampled elements) with an update that moves the weights."""
+6.7B bf16 set (sampled elements) with an update and a replay that move the
+weights."""
 import numpy as np
 import pytest
 
@@ -149,6 +150,41 @@ def test_portable_full_6p7b_update_bit_exact(mz, orc):
         total += ref.size
     print(f"opt6.7b portable perturb + K=64 update at lr=1e-3: {total} sampled elements bit-exact, "
           f"{changed} changed by the update")
+    assert changed > total // 2
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()
+
+
+def test_portable_full_6p7b_replay_bit_exact(mz, orc):
+    """The bench's catch-up on the 6.7B bf16 set in portable mode: a replay of
+    T = 4 logged steps of K = 64 seeds (256 staged records, rounded to bf16 at
+    every step end) at lr = 1e-3, bit-identical to the oracle's step-by-step
+    binary32 replay on every sampled element."""
+    import torch
+    w = synth.WORKLOADS["opt6.7b"]
+    tensors = theta_on_device(w, seed=5, device_rng=True)
+    ps = mz.ParamSet(tensors, gaussian=mz.GAUSS_PORTABLE)
+    rng = np.random.Generator(np.random.PCG64(10))
+    idx = [synth.sample_indices(t.numel(), rng, edge=32, blocks=8) for t in tensors]
+
+    def gather():
+        return [to_host(t.index_select(0, torch.from_numpy(ix.astype(np.int64)).cuda()))
+                for t, ix in zip(tensors, idx)]
+
+    log = [(synth.seeds(w.machines, w.samples_per_machine, step=10_000 + t),
+            synth.grads_int8(w.K, "uniform", seed=2000 + t), 1e-3) for t in range(4)]
+    before = gather()
+    ps.replay(log)
+    sync()
+    after = gather()
+    changed = total = 0
+    for tid, (b, a, ix) in enumerate(zip(before, after, idx)):
+        ref = orc.replay(b.copy(), tid, log, idx=ix, portable=True)
+        assert np.array_equal(bits(a), bits(ref)), f"tensor {tid}"
+        changed += int(np.sum(ref != b))
+        total += ref.size
+    print(f"opt6.7b portable replay 4 x 64: {total} sampled elements bit-exact, {changed} changed")
     assert changed > total // 2
     ps.close()
     del tensors
