@@ -104,73 +104,113 @@ __device__ __forceinline__ void short_record(const SeedRec& rec, uint32_t tensor
     }
 }
 
-// A lane's 8 elements through a call of one or two records (inline):
-// dequantize through the pair table, the records (a step's first one
-// assigning the accumulators), and at each step end add and quantize on the
-// round-to-nearest table. kFull: the 8 elements all exist (no masks).
-template <bool kPortable, bool kFull>
-__device__ __forceinline__ void short_records(const EngineArgs& a, const TensorDesc& d, uint64_t e0,
-                                              const NF4ShortLds& s, uint32_t& packed, float& am)
+// A step of one record on a lane's 8 values: w = round(w + c z). Portable
+// mode: acc = c z, then w + acc, the two roundings its definition states.
+// Fast mode: w = fma(c r, cos, w) and fma(c r, sin, w), one rounding of the
+// value plus the noise (as the oracle's step, a sum rounded once to binary32;
+// the fast mode's z is within its tolerance either way).
+template <bool kPortable>
+__device__ __forceinline__ void short_step(const SeedRec& rec, uint32_t tensor_id, BlockPre pre0, BlockPre pre1,
+                                           float (&w)[8])
 {
-    const uint32_t valid = kFull ? 0xFFu : nf4_valid(e0, d.numel);
-    float w[8];
-    nf4_dequant_pairs(s, packed, am, valid, w);
-    const uint64_t blk = (d.first + e0) >> 2;  // block of the logical tensor
-    const BlockPre pre0 = block_pre(uint32_t(blk));
-    const BlockPre pre1 = block_pre(uint32_t(blk + 1));
-    float acc[8];
-    const auto step_end = [&]() {
+    if constexpr (kPortable) {
+        float acc[8];
+        short_record<true, true>(rec, tensor_id, pre0, pre1, acc);
 #pragma unroll
         for (int j = 0; j < 8; ++j) w[j] = w[j] + acc[j];
+    } else {
+        const SeedUniform u = seed_uniform(rec, tensor_id);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            uint32_t w0, w1, w2, w3;
+            philox_words(u, h ? pre1 : pre0, w0, w1, w2, w3);
+            box_muller_pair_acc(w0, w1, rec.coef, w[4 * h], w[4 * h + 1]);
+            box_muller_pair_acc(w2, w3, rec.coef, w[4 * h + 2], w[4 * h + 3]);
+        }
+    }
+}
+
+// A lane's 8 elements (Philox blocks blk and blk + 1 of its tensor) through a
+// call of one or two records (inline): dequantize through the pair table, the
+// records, and at each step end quantize on the round-to-nearest table.
+// kFull: the 8 elements all exist (no masks).
+template <bool kPortable, bool kFull>
+__device__ __forceinline__ void short_records(const EngineArgs& a, uint32_t tensor_id, uint32_t blk, uint32_t valid,
+                                              const NF4ShortLds& s, uint32_t& packed, float& am)
+{
+    float w[8];
+    nf4_dequant_pairs(s, packed, am, valid, w);
+    const BlockPre pre0 = block_pre(blk);
+    const BlockPre pre1 = block_pre(blk + 1);
+    const auto mask = [&]() {
         if (!kFull && partial_wave(valid)) {  // only waves that reach a tensor's end
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 if (!((valid >> j) & 1u)) w[j] = 0.0f;
         }
     };
-    short_record<kPortable, true>(a.inl[0], d.tensor_id, pre0, pre1, acc);
-    if (a.n_rec == 2) {
-        if (a.inl[0].last) {
-            step_end();
+    if (a.n_rec == 2 && !a.inl[0].last) {  // two records in one step: their sum, one rounding
+        float acc[8];
+        short_record<kPortable, true>(a.inl[0], tensor_id, pre0, pre1, acc);
+        short_record<kPortable, false>(a.inl[1], tensor_id, pre0, pre1, acc);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w[j] = w[j] + acc[j];
+    } else {  // every step of one record
+        short_step<kPortable>(a.inl[0], tensor_id, pre0, pre1, w);
+        if (a.n_rec == 2) {
+            mask();
             nf4_requant_round<true>(s.bin, valid, w, packed, am);
-            short_record<kPortable, true>(a.inl[1], d.tensor_id, pre0, pre1, acc);
-        } else {
-            short_record<kPortable, false>(a.inl[1], d.tensor_id, pre0, pre1, acc);
+            short_step<kPortable>(a.inl[1], tensor_id, pre0, pre1, w);
         }
     }
-    step_end();
+    mask();
     nf4_requant_round<false>(s.bin, valid, w, packed, am);
 }
 
 // A call of at most two records (inline): a perturbation, or a restore fused
 // with the next perturbation, where the per-tile work around the noise weighs
-// most; whole tiles take a path compiled without bounds or masks. With no
-// records (out of place with nothing to apply) a tile is copied. Compiled for
-// 8 waves per SIMD (at most 64 VGPRs), the occupancy of the other kernels.
+// most. A whole tile (every tile but a tensor's last) takes a path compiled
+// without bounds or masks, its codes and absmax addressed as the tile's scalar
+// base plus a 32-bit lane offset; the 8 lanes of a block all store its absmax
+// (the same value to the same address). With no records (out of place with
+// nothing to apply) a tile is copied. NF4 tensors are never shards (first =
+// 0), so element e of the tile is element e of the tensor. Compiled for 8
+// waves per SIMD (at most 64 VGPRs), the occupancy of the other kernels.
 template <bool kPortable>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kPortable ? 1 : 8, 8)))
 void engine_nf4_short_kernel(EngineArgs a)
 {
-    const uint64_t tile = blockIdx.x;  // the grid is exactly the tiles of this table
+    const uint32_t tile = blockIdx.x;  // the grid is exactly the tiles of this table (< 2^31)
     const uint32_t ti = a.tile_tensor[tile];
     const TensorDesc d = a.tensors[ti];
     __shared__ NF4ShortLds lds;
     // out of place: read tensor ti of the source set (same layout), write d
     const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
     const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
-    const uint64_t local = tile - d.tile_begin;
-    const uint64_t e0 = local * kTileNF4 + threadIdx.x * 8u;
-    uint32_t packed;
-    float am;
-    if ((local + 1) * kTileNF4 <= d.numel) {  // uniform: all but a tensor's last tile
-        nf4_load<true>(codes, absmax, e0, d.numel, packed, am);
+    const uint32_t local = tile - uint32_t(d.tile_begin);
+    const uint32_t lane = threadIdx.x;
+    if (local < uint32_t(d.numel / kTileNF4)) {  // uniform: a whole tile
+        constexpr uint32_t kWords = kTileNF4 / 8, kBlocks = kTileNF4 / kNF4Block;  // per tile
+        const MEZO_GLOBAL uint32_t* cin = reinterpret_cast<const MEZO_GLOBAL uint32_t*>(codes) + uint64_t(local) * kWords;
+        const gfloat_t* ain = reinterpret_cast<const gfloat_t*>(absmax) + uint64_t(local) * kBlocks;
+        uint32_t packed = __builtin_nontemporal_load(cin + lane);
+        float am = ain[lane >> 3];
         nf4_short_lds_init(lds);
-        if (a.n_rec) short_records<kPortable, true>(a, d, e0, lds, packed, am);
-        nf4_store<true>(d.data, d.aux, e0, d.numel, packed, am);
+        if (a.n_rec) short_records<kPortable, true>(a, d.tensor_id, local * uint32_t(kTileNF4 / 4) + 2 * lane, 0xFFu,
+                                                    lds, packed, am);
+        MEZO_GLOBAL uint32_t* cout = reinterpret_cast<MEZO_GLOBAL uint32_t*>(d.data) + uint64_t(local) * kWords;
+        gfloat_t* aout = reinterpret_cast<gfloat_t*>(d.aux) + uint64_t(local) * kBlocks;
+        __builtin_nontemporal_store(packed, cout + lane);
+        aout[lane >> 3] = am;
     } else {
+        const uint64_t e0 = uint64_t(local) * kTileNF4 + lane * 8u;
+        uint32_t packed;
+        float am;
         nf4_load(codes, absmax, e0, d.numel, packed, am);
         nf4_short_lds_init(lds);
-        if (a.n_rec) short_records<kPortable, false>(a, d, e0, lds, packed, am);
+        if (a.n_rec)
+            short_records<kPortable, false>(a, d.tensor_id, uint32_t(e0 >> 2), nf4_valid(e0, d.numel), lds, packed,
+                                            am);
         nf4_store(d.data, d.aux, e0, d.numel, packed, am);
     }
 }

@@ -149,17 +149,35 @@ __device__ __forceinline__ void nf4_requant(const NF4Bin* bins, uint32_t valid, 
 
 // ---- the short path: calls of one or two records ---------------------------
 
-struct NF4ShortLds {
+// The LDS tables of the short path, laid out as one image of 257 rows of 16
+// bytes that a workgroup copies from constant memory with one row per lane
+// (and the last row by lane 0): the 129 round-to-nearest bins, then byte b ->
+// the values of its two codes (b & 15, b >> 4).
+struct NF4Pair {
+    float v_lo, v_hi;
+};
+struct alignas(16) NF4ShortLds {
     NF4Bin bin[kNF4RoundBins];
-    float2 pair[kNF4Pairs];  // byte b -> (value of code b & 15, value of code b >> 4)
+    NF4Pair pair[kNF4Pairs];
 };
 static_assert(kThreads == kNF4Pairs && kThreads >= kNF4RoundBins, "one table entry per lane");
+static_assert(sizeof(NF4ShortLds) == 16 * (kThreads + 1), "257 rows of 16 bytes");
+
+constexpr NF4ShortLds make_nf4_short_image()
+{
+    NF4ShortLds s{};
+    for (int b = 0; b < kNF4RoundBins; ++b) s.bin[b] = kNF4RoundTable.bin[b];
+    for (int b = 0; b < kNF4Pairs; ++b) s.pair[b] = NF4Pair{kNF4Values[b & 15], kNF4Values[b >> 4]};
+    return s;
+}
+constexpr NF4ShortLds kNF4ShortImage = make_nf4_short_image();
 
 __device__ __forceinline__ void nf4_short_lds_init(NF4ShortLds& s)
 {
-    const uint32_t t = threadIdx.x;
-    s.pair[t] = make_float2(kNF4Values[t & 15u], kNF4Values[t >> 4]);
-    if (t < uint32_t(kNF4RoundBins)) s.bin[t] = kNF4RoundTable.bin[t];
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(&kNF4ShortImage);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(&s);
+    dst[threadIdx.x] = src[threadIdx.x];
+    if (threadIdx.x == 0) dst[kThreads] = src[kThreads];
     __syncthreads();
 }
 
@@ -214,6 +232,15 @@ __device__ __forceinline__ void nf4_dequant_pairs(const NF4ShortLds& s, uint32_t
     }
 }
 
+// (p << 4) | c as one v_lshl_or_b32 (left to itself the compiler splits a
+// chain of these into separate shifts and three-way ors).
+__device__ __forceinline__ uint32_t shl4_or(uint32_t p, uint32_t c)
+{
+    uint32_t r;
+    asm("v_lshl_or_b32 %0, %1, 4, %2" : "=v"(r) : "v"(p), "v"(c));
+    return r;
+}
+
 // Block maxima whose reciprocal takes the short sequence: [2^-64, 2^64].
 constexpr uint32_t kRecipLo = 0x1F800000u;  // 2^-64
 constexpr uint32_t kRecipHi = 0x5F800000u;  // 2^64
@@ -237,22 +264,26 @@ __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t v
     m = max8(m);
     const bool usual = __float_as_uint(m) - kRecipLo <= kRecipHi - kRecipLo;
     const char* base = reinterpret_cast<const char*>(bins);
+    // the codes enter p from the highest element down: p = (p << 4) | code
+    // (the loops below run j = 7 .. 0)
     uint32_t p = 0u;
     const auto code = [&](int j, float x, uint32_t off) {
         if constexpr (kNext) {
             const NF4Bin e = *reinterpret_cast<const NF4Bin*>(base + off);
             const bool up = x > e.mid;
             w[j] = (up ? e.v_hi : e.v_lo) * m;
-            p |= (e.lo + (up ? 1u : 0u)) << (4 * j);
+            const uint32_t c = e.lo + (up ? 1u : 0u);
+            p = j == 7 ? c : shl4_or(p, c);
         } else {
             const float2 e = *reinterpret_cast<const float2*>(base + off);  // mid, lo
-            p |= (__float_as_uint(e.y) + (x > e.x ? 1u : 0u)) << (4 * j);
+            const uint32_t c = __float_as_uint(e.y) + (x > e.x ? 1u : 0u);
+            p = j == 7 ? c : shl4_or(p, c);
         }
     };
     if (__builtin_amdgcn_ballot_w64(!usual) == 0) {  // uniform
         const float r = div_rn_normal(1.0f, m);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 7; j >= 0; --j) {
             const float x = w[j] * r;
             const uint32_t t = __float_as_uint(__builtin_fmaf(x, 64.0f, kNF4BinMagic));
             code(j, x, (t << 4) - (kNF4BinBase << 4));  // 16 (t - base) = 16 b
@@ -260,7 +291,7 @@ __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t v
     } else {
         const float r = m > 0.0f ? 1.0f / m : 0.0f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
+        for (int j = 7; j >= 0; --j) {
             const float x = w[j] * r;
             const float xs = x == x ? x : -2.0f;
             const int k = int(__float_as_uint(__builtin_fmaf(xs, 64.0f, kNF4BinMagic))) - int(kNF4BinBase);
