@@ -122,11 +122,15 @@ struct RunCursor {
 };
 
 // fp32/bf16 tensors. Workgroup b takes the run of consecutive tiles
-// [T b / G, T (b + 1) / G) of the table's T tiles (G workgroups): the
-// descriptor changes only where the run crosses into the next tensor (no
-// per-tile map lookup). Tiles go in pairs where both lie wholly inside one
-// tensor: both loads are issued before either is mixed, two 16-byte loads in
-// flight per lane (four tiles in flight were slower on the large sets).
+// [T b / G, T (b + 1) / G) of the table's T tiles (G workgroups, two per CU):
+// the descriptor changes only where the run crosses into the next tensor (no
+// per-tile map lookup). Tiles go in groups of eight where all lie wholly
+// inside one tensor: the eight loads are issued before any is mixed, eight
+// 16-byte loads in flight per lane. Few workgroups with many loads each
+// stream faster than many with few: against eight workgroups per CU with
+// two tiles in flight, the 125M fp32 set took 0.093 -> 0.085 ms and the 6.7B
+// bf16 set 1.96 -> 1.90 ms (paired runs, checksums identical; one workgroup
+// per CU or sixteen tiles in flight were slower).
 template <uint32_t kDtype>
 __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
 {
@@ -134,7 +138,7 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
     constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
     constexpr uint64_t kEsz = 16 / kPer;
     constexpr uint64_t kTileElems = uint64_t(kThreads) * kPer;
-    constexpr uint64_t kPair = 2;
+    constexpr uint64_t kPair = 8;
     // chunk number of the lane's first chunk within its tile, times kChunkPos;
     // opaque from here on: otherwise the compiler folds uniform + lane
     // constant back into one per-lane 64-bit multiply in every tile
@@ -182,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
                 for (uint64_t j = 0; j < kPair; ++j) one_tile(t + j);
             }
         }
-        if (t < t_end) one_tile(t);
+        for (; t < t_end; ++t) one_tile(t);
     }
     add_workgroup_sum(sum, a.out);
 }
@@ -317,7 +321,7 @@ __global__ __launch_bounds__(kThreads) void checksum_nf4_kernel(ChecksumArgs a)
                 for (uint64_t j = 0; j < kPair; ++j) one_tile(t + j);
             }
         }
-        if (t < t_end) one_tile(t);
+        for (; t < t_end; ++t) one_tile(t);
     }
     add_workgroup_sum(sum, a.out);
 }
@@ -353,11 +357,11 @@ hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, i
     if (e != hipSuccess) return e;
     for (int i = 0; i < n_tables; ++i) {
         if (tables[i].total_tiles == 0) continue;
-        // as many workgroups as fill the device (8 per CU), each taking a run
-        // of consecutive tiles (NF4: each of its waves a run of its own)
+        // two workgroups per CU (NF4: eight), each taking a run of
+        // consecutive tiles (NF4: each of its waves a run of its own)
         const uint64_t per_wg = dtypes[i] == kNF4 ? kThreads / 64 : 1;
         const uint64_t need = (tables[i].total_tiles + per_wg - 1) / per_wg;
-        const uint64_t cap = uint64_t(cus) * 8;
+        const uint64_t cap = uint64_t(cus) * (dtypes[i] == kNF4 ? 8 : 2);
         const uint64_t grid = need < cap ? need : cap;
         const dim3 g{uint32_t(grid)};
         const dim3 b{uint32_t(kThreads)};
