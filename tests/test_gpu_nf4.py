@@ -176,6 +176,62 @@ def test_perturb_triple_and_updates(mz, orc, nf4, portable):
 
 
 @pytest.mark.parametrize("portable", [True, False])
+def test_short_calls_on_ragged_tiles(mz, orc, nf4, portable):
+    """Calls of one or two records (their own kernel) on every kind of last
+    tile (SET_SIZES): an update of two records (one step), an update of one
+    record, a perturbation out of place from a backup (the backup left as it
+    was) and, bit-exact in portable mode, two perturbations in one pass, each
+    its own step (a restore and the next perturbation, requantized after
+    each)."""
+    import torch
+    dev, ids = nf4_set(mz, SET_SIZES, seed=7, ids=[2, 11, 0, 6, 1 << 19, 30])
+    gauss = mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST
+    ps = mz.ParamSet(dev, ids, gaussian=gauss)
+    eps = 1e-3
+    s1, s2 = (3, 1, 4), (3, 1, 5)
+    seeds2 = synth.seeds(2, 1, step=2)
+    q2 = np.array([-77, 101], np.int8)
+    seeds1 = synth.seeds(1, 1, step=6)
+    q1 = np.array([59], np.int8)
+    ops = [
+        ("update K=2", lambda: ps.update_multi(seeds2, q2, 2e-3),
+         lambda tid: [lambda w, ix: orc.update(w, tid, seeds2, q2, 2e-3, idx=ix, portable=portable)]),
+        ("update K=1", lambda: ps.update_multi(seeds1, q1, 2e-3),
+         lambda tid: [lambda w, ix: orc.update(w, tid, seeds1, q1, 2e-3, idx=ix, portable=portable)]),
+    ]
+    if portable:
+        ops.append(("restore + next perturb", lambda: ps.perturb_multi([s1, s2], [-eps, eps]),
+                    lambda tid: [lambda w, ix: orc.perturb(w, tid, s1, -eps, idx=ix, portable=True),
+                                 lambda w, ix: orc.perturb(w, tid, s2, eps, idx=ix, portable=True)]))
+    for what, op, apps in ops:
+        before = [download(t) for t in dev]
+        op()
+        torch.cuda.synchronize()
+        for t, n, tid, st in zip(dev, SET_SIZES, ids, before):
+            steps = apps(tid)
+            for app in steps[:-1]:  # every step but the last: the oracle's own requantized state
+                w = nf4.dequantize(nf4.unpack(st[0], n), st[1], n)
+                app(w, nf4.block_elements(n, np.arange((n + 63) // 64)))
+                c, a = nf4.quantize(w, n)
+                st = (nf4.pack(c), a)
+            compare_step(nf4, download(t), st, n, tid, steps[-1], portable, f"{what} tensor {tid}")
+    # out of place: theta = backup + eps z, one record
+    work = [mz.NF4Tensor.empty(n) for n in SET_SIZES]
+    wk = mz.ParamSet(work, ids, gaussian=gauss)
+    host = [download(t) for t in dev]
+    wk.perturb_from(ps, s2, eps)
+    torch.cuda.synchronize()
+    for t, tb, n, tid, hb in zip(work, dev, SET_SIZES, ids, host):
+        compare_step(nf4, download(t), hb, n, tid,
+                     lambda w, ix, tid=tid: orc.perturb(w, tid, s2, eps, idx=ix, portable=portable),
+                     portable, f"perturb from backup tensor {tid}")
+        pb, ab = download(tb)
+        assert np.array_equal(pb, hb[0]) and np.array_equal(ab, hb[1])
+    wk.close()
+    ps.close()
+
+
+@pytest.mark.parametrize("portable", [True, False])
 def test_replay_requantizes_every_step(mz, orc, nf4, portable):
     import torch
     sizes = [4097, 64 * 100 + 3]
