@@ -300,6 +300,26 @@ __device__ __forceinline__ void accumulate4(float c, uint32_t w0, uint32_t w1, u
     }
 }
 
+// acc_j = c z_j for the four Gaussians of one block in fast mode (a step's
+// first record: no accumulator to clear first). The product differs from
+// fma(c, z, +0) only in the sign of a zero product, which changes theta + acc
+// only for theta = -0 (a -0 result where the accumulator's +0 gives +0).
+__device__ __forceinline__ void assign4_fast(float c, uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3,
+                                             float& a0, float& a1, float& a2, float& a3)
+{
+    constexpr float kTwoM24 = 0x1p-24f;
+    const float u1a = __builtin_fmaf(float(w0 >> 8), kTwoM24, kTwoM24);
+    const float u2a = float(w1 >> 8) * kTwoM24;
+    const float cra = c * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1a));
+    a0 = cra * __builtin_amdgcn_cosf(u2a);
+    a1 = cra * __builtin_amdgcn_sinf(u2a);
+    const float u1b = __builtin_fmaf(float(w2 >> 8), kTwoM24, kTwoM24);
+    const float u2b = float(w3 >> 8) * kTwoM24;
+    const float crb = c * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1b));
+    a2 = crb * __builtin_amdgcn_cosf(u2b);
+    a3 = crb * __builtin_amdgcn_sinf(u2b);
+}
+
 // Record r of a launch: from the kernel arguments (kInline) or the staged
 // device buffer. Either way a wave-uniform address: the words go to SGPRs.
 template <bool kInline>

@@ -73,6 +73,19 @@ __device__ __forceinline__ void store_group_full(uint64_t dst, uint64_t tile, in
     store_tile_b128(r, (uint32_t(g * kThreads) + threadIdx.x) * 16u, v);
 }
 
+// Whether every step of the call is one record (a perturbation, or a restore
+// and the next perturbation in one pass) and the Gaussian is the fast one:
+// each record's noise then assigns the accumulators (assign4_fast) instead of
+// being added to cleared ones.
+template <bool kInline, bool kPortable>
+__device__ __forceinline__ bool single_record_steps(const EngineArgs& a)
+{
+    if constexpr (!kInline || kPortable)
+        return false;
+    else
+        return a.n_rec == 1 || (a.n_rec == 2 && a.inl[0].last);
+}
+
 // One tile of an fp32 tensor: each lane owns kGroups groups of 4 elements
 // (one Philox block each).
 template <bool kInline, bool kPortable>
@@ -117,26 +130,42 @@ __device__ __forceinline__ void tile_f32(const EngineArgs& a, const TensorDesc& 
             accumulate4<kPortable>(c, w0, w1, w2, w3, acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
         }
     };
-    // the last record ends the call's last step: peeled off the loop, it
-    // needs no reset of acc afterwards
-    for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
-        accumulate(r);
-        if (rec_at<kInline>(a, r).last) {
+    if (single_record_steps<kInline, kPortable>(a)) {
+        const auto step = [&](const SeedRec& rec) {
+            const SeedUniform u = seed_uniform(rec, d.tensor_id);
+#pragma unroll
+            for (int g = 0; g < kGroups; ++g) {
+                uint32_t w0, w1, w2, w3;
+                philox_words(u, pre[g], w0, w1, w2, w3);
+                assign4_fast(rec.coef, w0, w1, w2, w3, acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) th[g][j] = th[g][j] + acc[g][j];
+            }
+        };
+        step(a.inl[0]);
+        if (a.n_rec == 2) step(a.inl[1]);
+    } else {
+        // the last record ends the call's last step: peeled off the loop, it
+        // needs no reset of acc afterwards
+        for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {
+            accumulate(r);
+            if (rec_at<kInline>(a, r).last) {
+#pragma unroll
+                for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        th[g][j] = th[g][j] + acc[g][j];
+                        acc[g][j] = 0.0f;
+                    }
+            }
+        }
+        if (a.n_rec > 0) {
+            accumulate(a.n_rec - 1);
 #pragma unroll
             for (int g = 0; g < kGroups; ++g)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    th[g][j] = th[g][j] + acc[g][j];
-                    acc[g][j] = 0.0f;
-                }
+                for (int j = 0; j < 4; ++j) th[g][j] = th[g][j] + acc[g][j];
         }
-    }
-    if (a.n_rec > 0) {
-        accumulate(a.n_rec - 1);
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) th[g][j] = th[g][j] + acc[g][j];
     }
 
     if (full) {
@@ -201,6 +230,24 @@ __device__ __forceinline__ void groups_bf16(const EngineArgs& a, const TensorDes
             for (int j = 0; j < 4; ++j)
                 th[g][j] = pack_bf16(bf16_lo(th[g][j]) + acc[g][2 * j], bf16_hi(th[g][j]) + acc[g][2 * j + 1]);
     };
+    if (single_record_steps<kInline, kPortable>(a)) {
+        const auto step = [&](const SeedRec& rec) {
+            const SeedUniform u = seed_uniform(rec, d.tensor_id);
+#pragma unroll
+            for (int g = 0; g < kGroups; ++g)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t w0, w1, w2, w3;
+                    philox_words(u, pre[g][h], w0, w1, w2, w3);
+                    assign4_fast(rec.coef, w0, w1, w2, w3, acc[g][4 * h + 0], acc[g][4 * h + 1], acc[g][4 * h + 2],
+                                 acc[g][4 * h + 3]);
+                }
+            step_end();
+        };
+        step(a.inl[0]);
+        if (a.n_rec == 2) step(a.inl[1]);
+        return;
+    }
     // the last record ends the call's last step: peeled off the loop, it
     // needs no reset of acc afterwards
     for (uint32_t r = 0; r + 1 < a.n_rec; ++r) {

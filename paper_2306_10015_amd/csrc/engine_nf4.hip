@@ -66,9 +66,9 @@ __device__ __forceinline__ void tile_nf4(const EngineArgs& a, const TensorDesc& 
 }
 
 // The noise of record r for a lane's 8 elements: acc = c z (kSet, a step's
-// first record, which saves zeroing the accumulators: the result can differ
-// from fma(c, z, +0) only in the sign of a zero, which no code depends on, +0
-// and -0 sharing the zero code's bin) or acc += c z.
+// first record, which saves zeroing the accumulators; in fast mode the
+// product can differ from fma(c, z, +0) only in the sign of a zero, which no
+// code depends on, +0 and -0 sharing the zero code's bin) or acc += c z.
 template <bool kPortable, bool kSet>
 __device__ __forceinline__ void short_record(const SeedRec& rec, uint32_t tensor_id, BlockPre pre0, BlockPre pre1,
                                              float (&acc)[8])
@@ -89,17 +89,7 @@ __device__ __forceinline__ void short_record(const SeedRec& rec, uint32_t tensor
             a4[2] = c * z.z2;
             a4[3] = c * z.z3;
         } else {
-            // box_muller_pair_acc with acc = 0: c r once per pair, then c r cos, c r sin
-            constexpr float kTwoM24 = 0x1p-24f;
-#pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                const uint32_t wa = p ? w2 : w0, wb = p ? w3 : w1;
-                const float u1 = __builtin_fmaf(float(wa >> 8), kTwoM24, kTwoM24);
-                const float u2 = float(wb >> 8) * kTwoM24;
-                const float cr = c * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u1));
-                a4[2 * p] = cr * __builtin_amdgcn_cosf(u2);
-                a4[2 * p + 1] = cr * __builtin_amdgcn_sinf(u2);
-            }
+            assign4_fast(c, w0, w1, w2, w3, a4[0], a4[1], a4[2], a4[3]);
         }
     }
 }
