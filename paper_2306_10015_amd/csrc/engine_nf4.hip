@@ -157,15 +157,16 @@ __device__ __forceinline__ void short_records(const EngineArgs& a, uint32_t tens
     nf4_requant_round<false>(s.bin, valid, w, packed, am);
 }
 
-// A call of at most two records (inline): a perturbation, or a restore fused
-// with the next perturbation, where the per-tile work around the noise weighs
-// most. A whole tile (every tile but a tensor's last) takes a path compiled
-// without bounds or masks, its codes and absmax addressed as the tile's scalar
-// base plus a 32-bit lane offset; the 8 lanes of a block all store its absmax
-// (the same value to the same address). With no records (out of place with
-// nothing to apply) a tile is copied. NF4 tensors are never shards (first =
-// 0), so element e of the tile is element e of the tensor. Compiled for 8
-// waves per SIMD (at most 64 VGPRs), the occupancy of the other kernels.
+// A call of two records (inline): a restore fused with the next perturbation,
+// or an update of two records, where the per-tile work around the noise weighs
+// most (one-record calls run engine_nf4_sweep_kernel). A whole tile (every
+// tile but a tensor's last) takes a path compiled without bounds or masks, its
+// codes and absmax addressed as the tile's scalar base plus a 32-bit lane
+// offset; the 8 lanes of a block all store its absmax (the same value to the
+// same address). With no records (out of place with nothing to apply) a tile
+// is copied. NF4 tensors are never shards (first = 0), so element e of the
+// tile is element e of the tensor. Compiled for 8 waves per SIMD (at most 64
+// VGPRs), the occupancy of the other kernels.
 template <bool kPortable>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kPortable ? 1 : 8, 8)))
 void engine_nf4_short_kernel(EngineArgs a)
@@ -205,6 +206,97 @@ void engine_nf4_short_kernel(EngineArgs a)
     }
 }
 
+// A lane's 16 elements (Philox blocks blk .. blk + 3 of its tensor) through a
+// call of one record: dequantize, add the noise (fast mode: straight into the
+// values, as short_step; portable mode: acc = c z, then w + acc), quantize.
+template <bool kPortable, bool kFull>
+__device__ __forceinline__ void sweep16(const SeedRec& rec, uint32_t tensor_id, uint32_t blk, uint32_t valid,
+                                        const NF4ShortLds& s, uint32_t (&packed)[2], float& am)
+{
+    float w[16];
+    nf4_dequant_pairs16(s, packed, am, valid, w);
+    const SeedUniform u = seed_uniform(rec, tensor_id);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        uint32_t w0, w1, w2, w3;
+        philox_words(u, block_pre(blk + h), w0, w1, w2, w3);
+        float* w4 = w + 4 * h;
+        if constexpr (kPortable) {
+            const Z4 z = gauss4_portable(w0, w1, w2, w3);
+            w4[0] = w4[0] + rec.coef * z.z0;
+            w4[1] = w4[1] + rec.coef * z.z1;
+            w4[2] = w4[2] + rec.coef * z.z2;
+            w4[3] = w4[3] + rec.coef * z.z3;
+        } else {
+            box_muller_pair_acc(w0, w1, rec.coef, w4[0], w4[1]);
+            box_muller_pair_acc(w2, w3, rec.coef, w4[2], w4[3]);
+        }
+    }
+    if (!kFull && partial_wave16(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
+    nf4_requant_round16(s.bin, valid, w, packed, am);
+}
+
+// A call of one record (a perturbation): 16 elements per lane, 128-lane
+// workgroups over the same 2048-element tiles (nf4_ops.hpp). Whole tiles are
+// addressed as in engine_nf4_short_kernel (codes: 8 bytes per lane; absmax
+// stored by the block's 4 lanes); the last tile of a tensor reads and writes
+// its code bytes one by one.
+template <bool kPortable>
+__global__ __launch_bounds__(kSweepLanes) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void engine_nf4_sweep_kernel(EngineArgs a)
+{
+    const uint32_t tile = blockIdx.x;  // the grid is exactly the tiles of this table (< 2^31)
+    const uint32_t ti = a.tile_tensor[tile];
+    const TensorDesc d = a.tensors[ti];
+    __shared__ NF4ShortLds lds;
+    // out of place: read tensor ti of the source set (same layout), write d
+    const uint64_t codes = a.src_tensors ? a.src_tensors[ti].data : d.data;
+    const uint64_t absmax = a.src_tensors ? a.src_tensors[ti].aux : d.aux;
+    const uint32_t local = tile - uint32_t(d.tile_begin);
+    const uint32_t lane = threadIdx.x;
+    if (local < uint32_t(d.numel / kTileNF4)) {  // uniform: a whole tile
+        constexpr uint32_t kPairs = kTileNF4 / 16, kBlocks = kTileNF4 / kNF4Block;  // per tile
+        const gu32x2_t* cin = reinterpret_cast<const gu32x2_t*>(codes) + uint64_t(local) * kPairs;
+        const gfloat_t* ain = reinterpret_cast<const gfloat_t*>(absmax) + uint64_t(local) * kBlocks;
+        const u32x2_t v = __builtin_nontemporal_load(cin + lane);
+        uint32_t packed[2] = {v.x, v.y};
+        float am = ain[lane >> 2];
+        nf4_sweep_lds_init(lds);
+        sweep16<kPortable, true>(a.inl[0], d.tensor_id, local * uint32_t(kTileNF4 / 4) + 4 * lane, 0xFFFFu, lds,
+                                 packed, am);
+        gu32x2_t* cout = reinterpret_cast<gu32x2_t*>(d.data) + uint64_t(local) * kPairs;
+        gfloat_t* aout = reinterpret_cast<gfloat_t*>(d.aux) + uint64_t(local) * kBlocks;
+        const u32x2_t o = {packed[0], packed[1]};
+        __builtin_nontemporal_store(o, cout + lane);
+        aout[lane >> 2] = am;
+    } else {
+        const uint64_t e0 = uint64_t(local) * kTileNF4 + lane * 16u;
+        uint32_t packed[2] = {0u, 0u};
+        float am = 0.0f;
+        if (e0 < d.numel) {
+            const MEZO_GLOBAL uint8_t* cb = reinterpret_cast<const MEZO_GLOBAL uint8_t*>(codes + e0 / 2);
+#pragma unroll
+            for (uint32_t k = 0; k < 8; ++k)
+                if (e0 + 2 * k < d.numel) packed[k >> 2] |= uint32_t(cb[k]) << (8 * (k & 3));
+            am = reinterpret_cast<const gfloat_t*>(absmax)[e0 / kNF4Block];
+        }
+        nf4_sweep_lds_init(lds);
+        sweep16<kPortable, false>(a.inl[0], d.tensor_id, uint32_t(e0 >> 2), nf4_valid16(e0, d.numel), lds, packed,
+                                  am);
+        if (e0 < d.numel) {
+            MEZO_GLOBAL uint8_t* ob = reinterpret_cast<MEZO_GLOBAL uint8_t*>(d.data + e0 / 2);
+#pragma unroll
+            for (uint32_t k = 0; k < 8; ++k)
+                if (e0 + 2 * k < d.numel) ob[k] = uint8_t(packed[k >> 2] >> (8 * (k & 3)));
+            reinterpret_cast<gfloat_t*>(d.aux)[e0 / kNF4Block] = am;
+        }
+    }
+}
+
 // Record lists of more than two records: one loop over the records (tile_nf4).
 template <bool kInline, bool kPortable>
 __global__ __launch_bounds__(kThreads) void engine_nf4_kernel(EngineArgs a)
@@ -236,6 +328,8 @@ template <bool kPortable>
 hipError_t launch_variant(const EngineArgs& args, dim3 g, dim3 b, hipStream_t stream)
 {
     if (args.n_rec > kInlineRecs) return launch1(engine_nf4_kernel<false, kPortable>, g, b, stream, args);
+    if (args.n_rec == 1)
+        return launch1(engine_nf4_sweep_kernel<kPortable>, g, dim3{uint32_t(kSweepLanes)}, stream, args);
     if (args.n_rec <= 2) return launch1(engine_nf4_short_kernel<kPortable>, g, b, stream, args);
     return launch1(engine_nf4_kernel<true, kPortable>, g, b, stream, args);
 }

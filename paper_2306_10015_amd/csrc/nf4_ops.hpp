@@ -8,7 +8,8 @@
 // 128-bin table of nf4.hpp. Calls of one or two records (where the per-element
 // work around the noise weighs most) take the short path at the end of this
 // file: a table of byte -> the values of its two codes, the 129-bin
-// round-to-nearest table, and a shorter reciprocal.
+// round-to-nearest table, and a shorter reciprocal; one-record calls with 16
+// elements per lane (4 lanes per block).
 #pragma once
 
 #include "engine.hpp"
@@ -232,6 +233,80 @@ __device__ __forceinline__ void nf4_dequant_pairs(const NF4ShortLds& s, uint32_t
     }
 }
 
+// ---- one-record calls: 16 elements per lane ----------------------------------
+// A perturbation (one record) needs no accumulators, so a lane can own 16
+// elements (4 Philox blocks, a quarter of an absmax block) within 64 VGPRs:
+// 128-lane workgroups over the same 2048-element tiles, and the work paid per
+// lane (tile addressing, the table copy, the block maximum across lanes, the
+// reciprocal) spread over twice the elements.
+
+constexpr int kSweepLanes = 128;  // lanes per workgroup of the one-record kernel
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef MEZO_GLOBAL u32x2_t gu32x2_t;
+
+// Copy the short-path image to LDS with 128 lanes: rows lane and lane + 128,
+// and the last row by lane 0.
+__device__ __forceinline__ void nf4_sweep_lds_init(NF4ShortLds& s)
+{
+    const u32x4_t* src = reinterpret_cast<const u32x4_t*>(&kNF4ShortImage);
+    u32x4_t* dst = reinterpret_cast<u32x4_t*>(&s);
+    dst[threadIdx.x] = src[threadIdx.x];
+    dst[threadIdx.x + kSweepLanes] = src[threadIdx.x + kSweepLanes];
+    if (threadIdx.x == 0) dst[2 * kSweepLanes] = src[2 * kSweepLanes];
+    __syncthreads();
+}
+static_assert(2 * kSweepLanes == kThreads, "the image is 2 x 128 rows plus one");
+
+// Which of a lane's 16 elements e0 .. e0 + 15 exist (bit j for element e0 + j).
+__device__ __forceinline__ uint32_t nf4_valid16(uint64_t e0, uint64_t numel)
+{
+    if (e0 >= numel) return 0u;
+    if (e0 + 16 <= numel) return 0xFFFFu;
+    return (1u << uint32_t(numel - e0)) - 1u;
+}
+
+__device__ __forceinline__ bool partial_wave16(uint32_t valid)
+{
+    return __builtin_amdgcn_ballot_w64(valid != 0xFFFFu) != 0;
+}
+
+// nf4_dequant_pairs for 16 elements: packed[0] holds elements 0..7, packed[1]
+// elements 8..15.
+__device__ __forceinline__ void nf4_dequant_pairs16(const NF4ShortLds& s, const uint32_t (&packed)[2], float am,
+                                                    uint32_t valid, float (&w)[16])
+{
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const float2 p0 = nf4_pair<0>(s, packed[h]);
+        const float2 p1 = nf4_pair<1>(s, packed[h]);
+        const float2 p2 = nf4_pair<2>(s, packed[h]);
+        const float2 p3 = nf4_pair<3>(s, packed[h]);
+        w[8 * h + 0] = p0.x * am;
+        w[8 * h + 1] = p0.y * am;
+        w[8 * h + 2] = p1.x * am;
+        w[8 * h + 3] = p1.y * am;
+        w[8 * h + 4] = p2.x * am;
+        w[8 * h + 5] = p2.y * am;
+        w[8 * h + 6] = p3.x * am;
+        w[8 * h + 7] = p3.y * am;
+    }
+    if (partial_wave16(valid)) {  // only waves that reach a tensor's end
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (!((valid >> j) & 1u)) w[j] = 0.0f;
+    }
+}
+
+// max over the 4 lanes of a block (one quad) of a value >= 0, on the integers
+// as in max8.
+__device__ __forceinline__ float max4(float m)
+{
+    uint32_t u = __float_as_uint(m);
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0xB1, 0xF, 0xF, false)));
+    u = max(u, uint32_t(__builtin_amdgcn_update_dpp(0, int(u), 0x4E, 0xF, 0xF, false)));
+    return __uint_as_float(u);
+}
+
 // (p << 4) | c as one v_lshl_or_b32 (left to itself the compiler splits a
 // chain of these into separate shifts and three-way ors).
 __device__ __forceinline__ uint32_t shl4_or(uint32_t p, uint32_t c)
@@ -299,6 +374,52 @@ __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t v
         }
     }
     packed = partial_wave(valid) ? p & nf4_nibble_mask(valid) : p;
+    am = m;
+}
+
+// nf4_requant_round (the last step of a call) for a lane's 16 elements, a
+// quarter of a block: the same arithmetic, the block maximum over 4 lanes.
+__device__ __forceinline__ void nf4_requant_round16(const NF4Bin* bins, uint32_t valid, const float (&w)[16],
+                                                    uint32_t (&packed)[2], float& am)
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) m = fmaxf(m, fabsf(w[j]));
+    m = max4(m);
+    const bool usual = __float_as_uint(m) - kRecipLo <= kRecipHi - kRecipLo;
+    const char* base = reinterpret_cast<const char*>(bins);
+    // the codes of elements 8h .. 8h + 7 enter p[h] highest first (j = 15 .. 0)
+    uint32_t p[2] = {0u, 0u};
+    const auto code = [&](int j, float x, uint32_t off) {
+        const float2 e = *reinterpret_cast<const float2*>(base + off);  // mid, lo
+        const uint32_t c = __float_as_uint(e.y) + (x > e.x ? 1u : 0u);
+        p[j >> 3] = (j & 7) == 7 ? c : shl4_or(p[j >> 3], c);
+    };
+    if (__builtin_amdgcn_ballot_w64(!usual) == 0) {  // uniform
+        const float r = div_rn_normal(1.0f, m);
+#pragma unroll
+        for (int j = 15; j >= 0; --j) {
+            const float x = w[j] * r;
+            const uint32_t t = __float_as_uint(__builtin_fmaf(x, 64.0f, kNF4BinMagic));
+            code(j, x, (t << 4) - (kNF4BinBase << 4));  // 16 (t - base) = 16 b
+        }
+    } else {
+        const float r = m > 0.0f ? 1.0f / m : 0.0f;
+#pragma unroll
+        for (int j = 15; j >= 0; --j) {
+            const float x = w[j] * r;
+            const float xs = x == x ? x : -2.0f;
+            const int k = int(__float_as_uint(__builtin_fmaf(xs, 64.0f, kNF4BinMagic))) - int(kNF4BinBase);
+            code(j, x, uint32_t(k < 0 ? 0 : (k > kNF4RoundBins - 1 ? kNF4RoundBins - 1 : k)) << 4);
+        }
+    }
+    if (partial_wave16(valid)) {  // missing elements (a run of high bits of valid) get zero nibbles
+        const uint32_t k = __builtin_popcount(valid);
+        p[0] &= k >= 8 ? 0xFFFFFFFFu : (1u << (4 * k)) - 1u;
+        p[1] &= k >= 16 ? 0xFFFFFFFFu : (k <= 8 ? 0u : (1u << (4 * (k - 8))) - 1u);
+    }
+    packed[0] = p[0];
+    packed[1] = p[1];
     am = m;
 }
 
