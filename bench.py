@@ -491,6 +491,24 @@ def measure_ops(torch, mezo, synth, w, ps, make_backup, stream, recs, proj, seed
         # Algorithm 1's restore of the backup fused into the apply loop
         backup, keep = make_backup()
         ops["update_from_backup"] = entry(K, timed(lambda: ps.update_multi_from(backup, seeds_t[0], q0, lr)))
+        # the same iteration with the two copies Algorithm 1 holds used as a
+        # pair: each sample's weights written out of place from the current
+        # ones (theta+ = theta + eps z, then theta- = theta - eps z, the forward
+        # passes reading the second copy), the current weights never perturbed
+        # and so never restored, then the K-seed update applied to them in
+        # place: one record per pass instead of the in-place sequence's
+        # -2 eps and restore + next +eps
+        cur, nxt = ps, backup
+        samples_b = [(0, 1, j) for j in range(SAMPLES_PER_MACHINE)]
+
+        def iteration_out_of_place():
+            for s in samples_b:
+                nxt.perturb_from(cur, s, w.eps)
+                nxt.perturb_from(cur, s, -w.eps)
+            cur.update_multi(seeds_t[0], q0, lr)
+        ops["iteration_16_samples_out_of_place"] = entry(
+            2 * SAMPLES_PER_MACHINE + K, timed(iteration_out_of_place),
+            bytes_per_launch * (2 * SAMPLES_PER_MACHINE + 1))
         backup.close()
         del keep
     return ops
