@@ -208,3 +208,22 @@ def test_late_joiner_matches_replica_checksum_1p3b(mz):
     ps_j.close()
     del replica, joiner
     torch.cuda.empty_cache()
+
+
+def test_checksum_full_6p7b_set(mz, orc):
+    """ChecksumMatch on the 6.7B-shaped bf16 set in the launch shape the bench
+    times (two workgroups per CU, each streaming a run of about 6,500 tiles,
+    eight in flight): bit-exact with the oracle over all 13.3 GB, tensor by
+    tensor on the host."""
+    import torch
+    w = synth.WORKLOADS["opt6.7b"]
+    tensors = theta_on_device(w, seed=3, device_rng=True)
+    ps = mz.ParamSet(tensors)
+    got = ps.checksum()
+    want = 0
+    for tid, t in enumerate(tensors):
+        want = (want + orc.checksum_tensor(to_host(t), tid)) & 0xFFFFFFFFFFFFFFFF
+    assert got == want
+    ps.close()
+    del tensors
+    torch.cuda.empty_cache()

@@ -384,6 +384,12 @@ def test_full_size_nf4_6p7b(mz, orc, nf4, portable):
             differing += r.get("codes_differing", 0)
         print(f"6.7B nf4 {what} ({'portable, bit-exact' if portable else 'fast'}): codes differing from the "
               f"oracle near a midpoint: {differing}")
+    if portable:  # ChecksumMatch over the whole 4-bit image (3.7 GB), tensor by tensor on the host
+        want = 0
+        for tid, t in enumerate(dev):
+            want = (want + nf4.checksum_tensor(t.codes.cpu().numpy(), t.absmax.cpu().numpy(), tid)) \
+                & 0xFFFFFFFFFFFFFFFF
+        assert ps.checksum() == want
     ps.close()
     del dev
     torch.cuda.empty_cache()
