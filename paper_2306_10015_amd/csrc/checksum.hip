@@ -138,7 +138,7 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
     constexpr uint64_t kPer = Layout<kDtype>::kPerGroup;
     constexpr uint64_t kEsz = 16 / kPer;
     constexpr uint64_t kTileElems = uint64_t(kThreads) * kPer;
-    constexpr uint64_t kPair = 8;
+    constexpr uint64_t kInFlight = 8;  // tiles whose loads a lane issues before mixing any
     // chunk number of the lane's first chunk within its tile, times kChunkPos;
     // opaque from here on: otherwise the compiler folds uniform + lane
     // constant back into one per-lane 64-bit multiply in every tile
@@ -170,20 +170,20 @@ __global__ __launch_bounds__(kThreads) void checksum_kernel(ChecksumArgs a)
             }
         };
         uint64_t t = t0;
-        for (; t + kPair <= t_end; t += kPair) {
+        for (; t + kInFlight <= t_end; t += kInFlight) {
             c.seek(t);
             const uint64_t local = t - c.begin;
-            if ((local + kPair) * kTileElems <= c.numel) {  // uniform: both tiles whole, one tensor
-                u32x4_t v[kPair];
+            if ((local + kInFlight) * kTileElems <= c.numel) {  // uniform: all kInFlight tiles whole, one tensor
+                u32x4_t v[kInFlight];
 #pragma unroll
-                for (uint64_t j = 0; j < kPair; ++j) v[j] = load_whole_tile(c.data, local + j);
+                for (uint64_t j = 0; j < kInFlight; ++j) v[j] = load_whole_tile(c.data, local + j);
                 const uint64_t cpos = cpos_of(local);
                 const uint64_t tmix = uint64_t(c.id) * kChunkTensor;
 #pragma unroll
-                for (uint64_t j = 0; j < kPair; ++j)
+                for (uint64_t j = 0; j < kInFlight; ++j)
                     sum += mix_whole_tile(v[j], cpos + j * (2 * kThreads * kChunkPos), tmix, cpos_lane);
             } else {
-                for (uint64_t j = 0; j < kPair; ++j) one_tile(t + j);
+                for (uint64_t j = 0; j < kInFlight; ++j) one_tile(t + j);
             }
         }
         for (; t < t_end; ++t) one_tile(t);

@@ -1,8 +1,11 @@
-// engine_nf4.hip — the engine kernel on 4-bit NF4 storage (gfx950): the
-// same record loop as on fp32/bf16 storage, with the block dequantized once
+// engine_nf4.hip — the engine kernels on 4-bit NF4 storage (gfx950): the
+// same records as on fp32/bf16 storage, with the block dequantized once
 // before the first record and quantized again at every step end (Section 3:
 // the weights are dequantized before the noise is added and quantized again
-// afterwards).
+// afterwards). Three kernels by the length of the record list: one loop over
+// any number of records (engine_nf4_kernel), two records
+// (engine_nf4_short_kernel) and one record, 16 elements per lane
+// (engine_nf4_sweep_kernel).
 #include "engine.hpp"
 #include "engine_launch.hpp"
 #include "nf4_ops.hpp"
