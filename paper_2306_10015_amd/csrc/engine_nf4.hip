@@ -152,12 +152,12 @@ __device__ __forceinline__ void short_records(const EngineArgs& a, uint32_t tens
         short_step<kPortable>(a.inl[0], tensor_id, pre0, pre1, w);
         if (a.n_rec == 2) {
             mask();
-            nf4_requant_round<true>(s.bin, valid, w, packed, am);
+            nf4_requant_round<true, kPortable>(s.bin, valid, w, packed, am);
             short_step<kPortable>(a.inl[1], tensor_id, pre0, pre1, w);
         }
     }
     mask();
-    nf4_requant_round<false>(s.bin, valid, w, packed, am);
+    nf4_requant_round<false, kPortable>(s.bin, valid, w, packed, am);
 }
 
 // A call of two records (inline): a restore fused with the next perturbation,
@@ -209,15 +209,42 @@ void engine_nf4_short_kernel(EngineArgs a)
     }
 }
 
+// Block maxima and coefficients for which the fast sweep works on w / am
+// (below): am in [2^-64, 2^64] and |c| <= 2^60, so that c / am, the values
+// v + (c / am) z and am times their maximum stay finite.
+constexpr uint32_t kFoldAmLo = 0x1F800000u;  // 2^-64
+constexpr uint32_t kFoldAmHi = 0x5F800000u;  // 2^64
+constexpr float kFoldCoefMax = 0x1p60f;
+
 // A lane's 16 elements (Philox blocks blk .. blk + 3 of its tensor) through a
 // call of one record: dequantize, add the noise (fast mode: straight into the
 // values, as short_step; portable mode: acc = c z, then w + acc), quantize.
+// Fast mode, when every lane's block maximum am and the coefficient c are in
+// range (uniform): the values are kept divided by am, v + (c / am) z with v
+// the table values themselves, and the new absmax is am times their maximum.
+// The quantizer only sees the ratio w / max |w|, so codes and absmax are those
+// of v am + c z up to a few roundings (within the fast mode's tolerance), and
+// the 16 products v am are saved. Otherwise the values are v am as in
+// portable mode.
 template <bool kPortable, bool kFull>
 __device__ __forceinline__ void sweep16(const SeedRec& rec, uint32_t tensor_id, uint32_t blk, uint32_t valid,
                                         const NF4ShortLds& s, uint32_t (&packed)[2], float& am)
 {
     float w[16];
-    nf4_dequant_pairs16(s, packed, am, valid, w);
+    float c = rec.coef;
+    float scale = 1.0f;  // the factor from the quantized values' maximum to the new absmax
+    if constexpr (kPortable) {
+        nf4_dequant_pairs16(s, packed, am, valid, w);
+    } else {
+        const bool in_range = __float_as_uint(am) - kFoldAmLo <= kFoldAmHi - kFoldAmLo;
+        if (__builtin_amdgcn_ballot_w64(!in_range) == 0 && fabsf(c) <= kFoldCoefMax) {  // uniform
+            nf4_dequant_pairs16(s, packed, 1.0f, valid, w);
+            c = c * __builtin_amdgcn_rcpf(am);
+            scale = am;
+        } else {
+            nf4_dequant_pairs16(s, packed, am, valid, w);
+        }
+    }
     const SeedUniform u = seed_uniform(rec, tensor_id);
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
@@ -231,8 +258,8 @@ __device__ __forceinline__ void sweep16(const SeedRec& rec, uint32_t tensor_id, 
             w4[2] = w4[2] + rec.coef * z.z2;
             w4[3] = w4[3] + rec.coef * z.z3;
         } else {
-            box_muller_pair_acc(w0, w1, rec.coef, w4[0], w4[1]);
-            box_muller_pair_acc(w2, w3, rec.coef, w4[2], w4[3]);
+            box_muller_pair_acc(w0, w1, c, w4[0], w4[1]);
+            box_muller_pair_acc(w2, w3, c, w4[2], w4[3]);
         }
     }
     if (!kFull && partial_wave16(valid)) {  // only waves that reach a tensor's end
@@ -240,7 +267,8 @@ __device__ __forceinline__ void sweep16(const SeedRec& rec, uint32_t tensor_id, 
         for (int j = 0; j < 16; ++j)
             if (!((valid >> j) & 1u)) w[j] = 0.0f;
     }
-    nf4_requant_round16(s.bin, valid, w, packed, am);
+    nf4_requant_round16<kPortable>(s.bin, valid, w, packed, am);
+    if constexpr (!kPortable) am = am * scale;
 }
 
 // A call of one record (a perturbation): 16 elements per lane, 128-lane

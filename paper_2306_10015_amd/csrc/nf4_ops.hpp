@@ -328,8 +328,10 @@ constexpr uint32_t kRecipHi = 0x5F800000u;  // 2^64
 // directly. Otherwise (a = 0, tiny or huge blocks; x may be infinite or NaN)
 // the wave takes the general division and clamps the bin to the table, a NaN
 // x (0 * inf) taking the lowest bin like the comparisons it fails. Same
-// result as nf4_requant either way.
-template <bool kNext>
+// result as nf4_requant either way. kExactRecip = false (the engine's fast
+// mode) takes v_rcp_f32's reciprocal in the usual case, as
+// nf4_requant_round16 does.
+template <bool kNext, bool kExactRecip = true>
 __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t valid, float (&w)[8],
                                                   uint32_t& packed, float& am)
 {
@@ -356,7 +358,7 @@ __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t v
         }
     };
     if (__builtin_amdgcn_ballot_w64(!usual) == 0) {  // uniform
-        const float r = div_rn_normal(1.0f, m);
+        const float r = kExactRecip ? div_rn_normal(1.0f, m) : __builtin_amdgcn_rcpf(m);
 #pragma unroll
         for (int j = 7; j >= 0; --j) {
             const float x = w[j] * r;
@@ -379,6 +381,12 @@ __device__ __forceinline__ void nf4_requant_round(const NF4Bin* bins, uint32_t v
 
 // nf4_requant_round (the last step of a call) for a lane's 16 elements, a
 // quarter of a block: the same arithmetic, the block maximum over 4 lanes.
+// kExactRecip = false (fast mode): in the usual case r is v_rcp_f32's
+// reciprocal (within 1 ulp of 1 / m) instead of the correctly rounded one, so
+// x is within about 2 ulp of fl32(w * (1 / m)) and |x| <= 1 + 2^-22, which
+// still takes bin 0 or 128 at the ends; a code can then differ from the
+// exact quantizer's only where x lies within about 2^-23 of a midpoint.
+template <bool kExactRecip>
 __device__ __forceinline__ void nf4_requant_round16(const NF4Bin* bins, uint32_t valid, const float (&w)[16],
                                                     uint32_t (&packed)[2], float& am)
 {
@@ -396,7 +404,7 @@ __device__ __forceinline__ void nf4_requant_round16(const NF4Bin* bins, uint32_t
         p[j >> 3] = (j & 7) == 7 ? c : shl4_or(p[j >> 3], c);
     };
     if (__builtin_amdgcn_ballot_w64(!usual) == 0) {  // uniform
-        const float r = div_rn_normal(1.0f, m);
+        const float r = kExactRecip ? div_rn_normal(1.0f, m) : __builtin_amdgcn_rcpf(m);
 #pragma unroll
         for (int j = 15; j >= 0; --j) {
             const float x = w[j] * r;
