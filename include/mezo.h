@@ -338,7 +338,12 @@ MEZO_API int mezo_update_multi_from(mezo_paramset_t dst, mezo_paramset_t src,
  * tensor's bytes are its ceil(numel / 2) code bytes
  * zero-padded to a multiple of 8, followed by its absmax values (chunk numbers
  * continue). Written asynchronously to out_dev, a device pointer to 8 bytes
- * (8-byte aligned; MEZO_EINVAL otherwise), on stream. */
+ * (8-byte aligned; MEZO_EINVAL otherwise), on stream. The workgroups sum into
+ * a running sum the paramset owns, one per stream it tracks (calls on
+ * different streams may overlap), and the call's last workgroup moves the
+ * total to out_dev and clears the sum, so no zeroing precedes the call.
+ * Calls captured into graphs share one running sum per paramset: replays of
+ * such graphs must not overlap in time. */
 MEZO_API int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream);
 
 /* ---- 4-bit storage (Section 3, the 4-bit forward-only variant) -------- */

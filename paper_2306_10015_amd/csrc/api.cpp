@@ -224,6 +224,11 @@ struct mezo_paramset {
     static constexpr size_t kUses = 16;
     Use uses[kUses];
     uint64_t use_seq = 0;
+    // The checksum's running sums: two words per use entry (a stream's calls
+    // are ordered, and an entry changes stream only after its work is done),
+    // and one pair more for calls captured into a graph. Zero between calls.
+    static constexpr size_t kCkPairs = kUses + 1;
+    unsigned long long* d_ck = nullptr;
 
     // Staging of record lists too long for the kernel arguments: a ring of
     // slots, each reused only after the launch that read it has completed.
@@ -277,6 +282,12 @@ int ensure_device(mezo_paramset* ps)
     }
     for (size_t i = 0; i < mezo_paramset::kUses && e == hipSuccess; ++i)
         e = hipEventCreateWithFlags(&ps->uses[i].done, hipEventDisableTiming);
+    if (e == hipSuccess) {
+        const std::vector<unsigned long long> zeros(2 * mezo_paramset::kCkPairs, 0ull);
+        e = hipMalloc(reinterpret_cast<void**>(&ps->d_ck), zeros.size() * sizeof(zeros[0]));
+        if (e == hipSuccess)
+            e = hipMemcpy(ps->d_ck, zeros.data(), zeros.size() * sizeof(zeros[0]), hipMemcpyHostToDevice);
+    }
     // the device address of mezo_replay_noalloc's staging array, resolved at
     // set-up (once per device, cached), so that entry point makes no such
     // query itself, also not under graph capture
@@ -293,6 +304,8 @@ int ensure_device(mezo_paramset* ps)
             if (u.done) (void)hipEventDestroy(u.done);
             u.done = nullptr;
         }
+        if (ps->d_ck) (void)hipFree(ps->d_ck);
+        ps->d_ck = nullptr;
         return hip_fail(e, "paramset device table");
     }
     ps->device = dev;
@@ -318,23 +331,37 @@ int refuse_first_use_in_capture(const mezo_paramset* ps)
     return MEZO_EINVAL;
 }
 
-// Record that ps's tables are read by work enqueued so far on stream (after
-// ensure_device: the events exist; nothing is created here).
-int mark_use(mezo_paramset* ps, hipStream_t stream)
+// The use entry of stream: its own, else one not used yet (seq 0), else the
+// one used longest ago, taken over after its work has completed (a host wait).
+int use_entry(mezo_paramset* ps, hipStream_t stream, mezo_paramset::Use*& out)
 {
     mezo_paramset::Use* use = nullptr;
     for (auto& u : ps->uses)
         if (u.seq && u.stream == stream) use = &u;
     if (!use) {
-        // an entry not used yet (seq 0), else the one used longest ago
         use = std::min_element(std::begin(ps->uses), std::end(ps->uses),
                                [](const mezo_paramset::Use& a, const mezo_paramset::Use& b) { return a.seq < b.seq; });
         if (use->seq) MEZO_HIP(hipEventSynchronize(use->done));
         use->stream = stream;
     }
+    out = use;
+    return MEZO_OK;
+}
+
+// Record that ps's tables are read by work enqueued so far on stream, in its
+// use entry (after ensure_device: the events exist; nothing is created here).
+int record_use(mezo_paramset* ps, mezo_paramset::Use* use, hipStream_t stream)
+{
     use->seq = ++ps->use_seq;
     MEZO_HIP(hipEventRecord(use->done, stream));
     return MEZO_OK;
+}
+
+int mark_use(mezo_paramset* ps, hipStream_t stream)
+{
+    mezo_paramset::Use* use = nullptr;
+    const int rc = use_entry(ps, stream, use);
+    return rc ? rc : record_use(ps, use, stream);
 }
 
 // Records one engine launch applies at most when a call can split its list
@@ -588,6 +615,7 @@ void mezo_paramset_destroy(mezo_paramset_t ps)
             if (ps->d_table[dt]) (void)hipFree(ps->d_table[dt]);
             if (ps->d_tile_tensor[dt]) (void)hipFree(ps->d_tile_tensor[dt]);
         }
+        if (ps->d_ck) (void)hipFree(ps->d_ck);
     }
     delete ps;
 }
@@ -816,7 +844,7 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
         if (rc) return rc;
         rc = ensure_device(ps);
         if (rc) return rc;
-        mezo::ChecksumArgs tabs[mezo_paramset::kTypes];
+        mezo::ChecksumArgs tabs[mezo_paramset::kTypes] = {};
         uint32_t dts[mezo_paramset::kTypes];
         int n = 0;
         for (uint32_t dt = 0; dt < mezo::kStorageTypes; ++dt) {
@@ -824,13 +852,20 @@ int mezo_checksum(mezo_paramset_t ps, uint64_t* out_dev, void* stream)
             tabs[n].tensors = ps->d_table[dt];
             tabs[n].tile_tensor = ps->d_tile_tensor[dt];
             tabs[n].total_tiles = ps->total_tiles[dt];
-            tabs[n].out = reinterpret_cast<unsigned long long*>(out_dev);
             dts[n] = dt;
             ++n;
         }
+        // the running sum of the stream's use entry (captured: the graphs' own)
+        mezo_paramset::Use* use = nullptr;
+        size_t pair = mezo_paramset::kUses;
+        if (!capture) {
+            rc = use_entry(ps, st, use);
+            if (rc) return rc;
+            pair = static_cast<size_t>(use - ps->uses);
+        }
         MEZO_HIP(mezo::launch_checksum(tabs, dts, n, reinterpret_cast<unsigned long long*>(out_dev),
-                                       ps->device, st));
-        return capture ? MEZO_OK : mark_use(ps, st);
+                                       ps->d_ck + 2 * pair, ps->device, st));
+        return capture ? MEZO_OK : record_use(ps, use, st);
     });
 }
 

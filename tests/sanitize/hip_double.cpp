@@ -263,12 +263,15 @@ hipError_t launch_engine_dense(const EngineArgs& a, uint32_t dtype, bool, hipStr
 
 hipError_t launch_engine_nf4(const EngineArgs& a, bool, hipStream_t) { return engine(a, kNF4); }
 
-hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n, unsigned long long* out, int,
-                           hipStream_t)
+hipError_t launch_checksum(const ChecksumArgs* tables, const uint32_t* dtypes, int n, unsigned long long* out,
+                           unsigned long long* acc, int, hipStream_t)
 {
     std::lock_guard<std::mutex> lock(g_mu);
+    // the running sum: two words of a device allocation, zero between calls
+    if (!inside(g_dev, acc, 2 * sizeof(*acc))) fail("checksum running sum outside a device allocation");
+    if (acc[0] != 0 || acc[1] != 0) fail("checksum running sum not zero at a call");
+    (void)out;
     for (int i = 0; i < n; ++i) {
-        if (tables[i].out != out) fail("checksum tables disagree on the output");
         const TensorDesc* t = tables[i].tensors;
         uint32_t cnt = 0;
         // the table's length is not passed: count the entries that the tile

@@ -434,6 +434,31 @@ def test_checksum_on_a_side_stream(mz, orc):
     assert got == orc.checksum([to_host(d) for d in devs])
 
 
+def test_checksums_of_one_set_on_many_streams(mz, orc):
+    """Checksum calls of one paramset (fp32 and bf16 tensors: two launches a
+    call, each of hundreds of workgroups) queued twice on each of 20 streams
+    with no ordering between them, more streams than the paramset tracks (so
+    entries change stream after a host wait): each stream's calls sum in the
+    running sum of its own entry, every result equals the oracle's, and the
+    sums are left at zero (later calls on the current stream agree)."""
+    import torch
+    f32, bf16 = tiny_hosts(synth.F32), tiny_hosts(synth.BF16)
+    hosts = [f32[0], bf16[1], f32[2], bf16[3]]
+    devs, ps = make_set(mz, hosts)
+    want = orc.checksum(hosts)
+    assert ps.checksum() == want
+    streams = [torch.cuda.Stream() for _ in range(20)]
+    outs = torch.zeros((20, 2), dtype=torch.int64, device="cuda")
+    torch.cuda.synchronize()
+    for rep in range(2):
+        for k, s in enumerate(streams):
+            ps.checksum_into(outs[k, rep:rep + 1], stream=s)
+    torch.cuda.synchronize()
+    got = [int(v) & 0xFFFFFFFFFFFFFFFF for v in outs.flatten().tolist()]
+    assert got == [want] * 40
+    assert ps.checksum() == want and ps.checksum() == want
+
+
 def test_checksum_full_125m_set(mz, orc):
     import torch
     from gpu_util import theta_on_device
