@@ -128,11 +128,17 @@ extern "C" {
 /* How z is computed (a property of a training run: every machine must use
  * the same one).
  *  FAST:     hardware transcendentals (v_log, v_sqrt, v_sin, v_cos); z within
- *            1e-6 * max|z| of the exact Box-Muller value; the default.
+ *            1e-6 * max|z| of the exact Box-Muller value; the default. On
+ *            MEZO_NF4 storage the quantizer may also round differently (a
+ *            hardware reciprocal; in one-record calls the block's values
+ *            scaled by 1 / absmax): a code can then differ from the rule
+ *            stated with mezo_tensor_t only where x lies within about 2^-22
+ *            of a midpoint, and the absmax by a few ulp.
  *  PORTABLE: z and the update from IEEE binary32 +, -, *, fma, correctly
  *            rounded / and sqrt only (Appendix B: noise every device
  *            reproduces), so any IEEE machine computes bit-identical z and
- *            weights; about 2.5x the arithmetic of FAST. Per pair of words:
+ *            weights; about 2.8x the instructions of FAST (2.0x its time).
+ *            Per pair of words:
  *            ln u1 from an exact reduction u1 = m 2^e and the series
  *            2 atanh((m-1)/(m+1)), r = sqrt(-2 ln u1), and cos/sin of 2 pi u2
  *            from its octant and Taylor polynomials on [0, pi/4]; every
