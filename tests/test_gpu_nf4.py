@@ -232,6 +232,50 @@ def test_short_calls_on_ragged_tiles(mz, orc, nf4, portable):
 
 
 @pytest.mark.parametrize("portable", [True, False])
+def test_blocks_outside_the_usual_range(mz, orc, nf4, portable):
+    """Whole tiles whose blocks have absmax 0, subnormal, tiny or huge, and a
+    perturbation whose coefficient is huge: the waves holding them take the
+    general paths (fast mode: no values kept divided by the absmax, IEEE
+    division in the quantizer). A one-record perturbation, a two-record update
+    and the huge perturbation, each against the oracle (bit-exact in portable
+    mode, else within the fast-mode rule)."""
+    import torch
+    n = 3 * 2048
+    nb = n // 64
+    rng = np.random.Generator(np.random.PCG64(31))
+    normal = (0.02 + 0.08 * rng.random(nb)).astype(np.float32)
+    regimes = {
+        "zero blocks": np.where(np.arange(nb) % 3 == 1, np.float32(0), normal),
+        "tiny and subnormal": np.where(np.arange(nb) % 2 == 0, np.float32(1e-30), np.float32(1e-40)),
+        "huge": np.full(nb, 1e25, np.float32),
+        "normal": normal,
+    }
+    dev, host = [], []
+    for a in regimes.values():
+        packed = nf4.pack(rng.integers(0, 16, n).astype(np.uint8))
+        host.append((packed, a.astype(np.float32)))
+        dev.append(upload(mz, packed, a.astype(np.float32), n))
+    ids = list(range(len(dev)))
+    ps = mz.ParamSet(dev, ids, gaussian=mz.GAUSS_PORTABLE if portable else mz.GAUSS_FAST)
+    s = (4, 4, 2)
+    seeds2 = synth.seeds(2, 1, step=9)
+    q2 = np.array([93, -41], np.int8)
+    ops = [("perturb +eps", lambda: ps.perturb(s, 1e-3),
+            lambda tid: (lambda w, ix: orc.perturb(w, tid, s, 1e-3, idx=ix, portable=portable))),
+           ("update K=2", lambda: ps.update_multi(seeds2, q2, 3e-3),
+            lambda tid: (lambda w, ix: orc.update(w, tid, seeds2, q2, 3e-3, idx=ix, portable=portable))),
+           ("perturb by 1e20", lambda: ps.perturb(s, 1e20),
+            lambda tid: (lambda w, ix: orc.perturb(w, tid, s, 1e20, idx=ix, portable=portable)))]
+    for what, gpu_op, oracle_op in ops:
+        before = [download(t) for t in dev]
+        gpu_op()
+        torch.cuda.synchronize()
+        for t, tid, name, b in zip(dev, ids, regimes, before):
+            compare_step(nf4, download(t), b, n, tid, oracle_op(tid), portable, f"{what}, {name}")
+    ps.close()
+
+
+@pytest.mark.parametrize("portable", [True, False])
 def test_replay_requantizes_every_step(mz, orc, nf4, portable):
     import torch
     sizes = [4097, 64 * 100 + 3]
