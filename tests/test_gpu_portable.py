@@ -89,6 +89,37 @@ def test_portable_from_backup_bit_exact(mz, orc):
         assert np.array_equal(bits(to_host(d)), bits(ref))
 
 
+def test_portable_subnormal_weights_and_scales_bit_exact(mz, orc):
+    """Subnormal weights (fp32 and bf16 storage), a perturbation of subnormal
+    scale and an update whose coefficients are subnormal: the results, still
+    mostly subnormal, equal the oracle's bit for bit (denormals kept on both
+    sides; a flush to zero anywhere on the GPU would show)."""
+    rng = np.random.Generator(np.random.PCG64(41))
+    n = 4097
+    sign32 = rng.integers(0, 2, n, dtype=np.uint32) << np.uint32(31)
+    f = (rng.integers(1, 1 << 23, n, dtype=np.uint32) | sign32).view(np.float32)
+    sign16 = (rng.integers(0, 2, n, dtype=np.uint16) << np.uint16(15)).astype(np.uint16)
+    b = (rng.integers(1, 1 << 7, n, dtype=np.uint16) | sign16).astype(np.uint16)
+    hosts, ids = [f, b], [3, 8]
+    devs, ps = portable_set(mz, hosts, ids)
+    refs = [h.copy() for h in hosts]
+    s = (6, 1, 0)
+    ps.perturb(s, 1e-39)
+    for r, tid in zip(refs, ids):
+        orc.perturb(r, tid, s, 1e-39, portable=True)
+    seeds = synth.seeds(3, 1, step=2)
+    q = synth.grads_int8(3, seed=4)
+    ps.update_multi(seeds, q, 1e-40)
+    for r, tid in zip(refs, ids):
+        orc.update(r, tid, seeds, q, 1e-40, portable=True)
+    sync()
+    for h, d, r in zip(hosts, devs, refs):
+        assert np.array_equal(bits(to_host(d)), bits(r)), f"{h.dtype}"
+    tiny = np.finfo(np.float32).tiny
+    assert np.mean((refs[0] != 0) & (np.abs(refs[0]) < tiny)) > 0.5
+    assert not np.array_equal(bits(refs[0]), bits(f)) and not np.array_equal(refs[1], b)
+
+
 def test_portable_full_125m_update_bit_exact(mz, orc):
     import torch
     w = synth.WORKLOADS["opt125m"]
