@@ -390,6 +390,42 @@ def test_algorithm1_iteration_restore_fused(mz, orc, dtype):
         assert_theta_close(to_host(d), orc.update(h.copy(), i, seeds, q, 1e-3), f"tensor {i}", inp=h)
 
 
+def float_class(a):
+    """Per element: 1 = +inf, -1 = -inf, 2 = NaN, 0 = finite (fp32 values or
+    bf16 bit patterns)."""
+    if a.dtype == np.float32:
+        return np.where(np.isnan(a), 2, np.where(np.isposinf(a), 1, np.where(np.isneginf(a), -1, 0)))
+    special = ((a >> 7) & 0xFF) == 0xFF
+    nan = special & ((a & 0x7F) != 0)
+    inf = special & ((a & 0x7F) == 0)
+    return np.where(nan, 2, np.where(inf, np.where(a >> 15, -1, 1), 0))
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_non_finite_weights_stay_non_finite(mz, orc, dtype):
+    """Weights holding +inf, -inf and NaN (a diverged model): a perturbation
+    and an update leave each of them +inf, -inf or NaN as it was, and every
+    finite weight within the bar of the oracle applied to the same input."""
+    h = synth.theta0_tensor((9001,), dtype, 0, 3)
+    special = [0, 17, 4095, 4096, 8999, 9000]
+    if dtype == synth.F32:
+        h[special] = np.array([np.inf, -np.inf, np.nan, np.inf, -np.nan, -np.inf], np.float32)
+    else:
+        h[special] = np.array([0x7F80, 0xFF80, 0x7FC0, 0x7F80, 0xFFC1, 0xFF80], np.uint16)
+    devs, ps = make_set(mz, [h])
+    s = (5, 5, 5)
+    seeds, q = synth.seeds(6, 1, step=4), synth.grads_int8(6, seed=9)
+    ps.perturb(s, 1e-3)
+    ps.update_multi(seeds, q, 1e-3)
+    sync()
+    got = to_host(devs[0])
+    assert np.array_equal(float_class(got), float_class(h))
+    finite = float_class(h) == 0
+    ref = orc.update(orc.perturb(h.copy(), 0, s, 1e-3), 0, seeds, q, 1e-3)
+    mid = orc.perturb(h.copy(), 0, s, 1e-3)
+    assert_theta_close(got[finite], ref[finite], f"finite weights ({dtype})", inp=mid[finite])
+
+
 # ---- checksum (ChecksumMatch, Algorithm 1) ---------------------------------
 
 def test_checksum_matches_oracle_and_is_additive(mz, orc):
