@@ -51,6 +51,53 @@ __device__ __forceinline__ void nf4_quantize_load(const NF4ConvArgs& a, uint64_t
     }
 }
 
+// Whole fp32 tiles: a lane's 8 consecutive values are 32 bytes, and loading
+// them as two 16-byte loads 16 bytes apart leaves every load instruction
+// touching each cache line it reaches only half. So wave v loads its 512
+// values of a tile (bytes [2048 v, 2048 v + 2048)) as two fully coalesced
+// 16-byte loads per lane (bytes 16 l and 1024 + 16 l of that range) and hands
+// them to their lanes through 2 KB of LDS of its own: every lane writes its
+// two chunks and reads back the two at 32 l and 32 l + 16. A wave's LDS
+// accesses complete in the order issued, so the wave needs no barrier with
+// the others; the wavefront-scope fences keep the compiler from moving the
+// accesses across each other. 0.169 -> 0.155 ms for the loads alone on the
+// 206M-element embedding (paired).
+struct QuantStage {
+    u32x4_t chunk[128];  // one wave's 512 fp32 values of a tile
+};
+
+__device__ __forceinline__ void wave_lds_order()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The two coalesced chunks of lane l of wave v of tile `tile` (whole tiles).
+__device__ __forceinline__ void quantize_load_f32_coalesced(const NF4ConvArgs& a, uint64_t tile, u32x4_t& c0,
+                                                            u32x4_t& c1)
+{
+    const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+    const gu32x4_t* base = reinterpret_cast<const gu32x4_t*>(a.values + (tile * kTileNF4 + wave * 512u) * 4u);
+    c0 = __builtin_nontemporal_load(base + lane);
+    c1 = __builtin_nontemporal_load(base + 64u + lane);
+}
+
+// Chunks -> the lane's 8 consecutive values, through the wave's stage.
+__device__ __forceinline__ void quantize_exchange_f32(QuantStage& st, u32x4_t c0, u32x4_t c1, float (&w)[8])
+{
+    const uint32_t lane = threadIdx.x & 63u;
+    wave_lds_order();  // the previous tile's reads of the stage come first
+    st.chunk[lane] = c0;
+    st.chunk[64u + lane] = c1;
+    wave_lds_order();
+    const u32x4_t r0 = st.chunk[2u * lane];
+    const u32x4_t r1 = st.chunk[2u * lane + 1u];
+    const uint32_t u[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) w[j] = __uint_as_float(u[j]);
+}
+
 // Standalone quantization: kQuantTiles tiles of 2048 elements per workgroup.
 __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
 {
@@ -69,7 +116,21 @@ __global__ __launch_bounds__(kThreads) void nf4_quantize_kernel(NF4ConvArgs a)
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     const uint64_t t0 = uint64_t(blockIdx.x) * kQuantTiles;
     const uint64_t lane_e = threadIdx.x * 8u;
-    if ((t0 + kQuantTiles) * kTileNF4 <= a.n) {  // uniform: all the workgroup's tiles are whole
+    if ((t0 + kQuantTiles) * kTileNF4 <= a.n && a.dtype == kF32) {  // uniform: whole fp32 tiles
+        __shared__ QuantStage stage[kThreads / 64];
+        u32x4_t c0[kQuantTiles], c1[kQuantTiles];
+#pragma unroll
+        for (uint32_t t = 0; t < kQuantTiles; ++t) quantize_load_f32_coalesced(a, t0 + t, c0[t], c1[t]);
+#pragma unroll
+        for (uint32_t t = 0; t < kQuantTiles; ++t) {
+            float w[8];
+            quantize_exchange_f32(stage[threadIdx.x >> 6], c0[t], c1[t], w);
+            uint32_t packed;
+            float am;
+            nf4_requant_round<false>(bins, 0xFFu, w, packed, am);
+            nf4_store<true>(a.codes, a.absmax, (t0 + t) * kTileNF4 + lane_e, a.n, packed, am);
+        }
+    } else if ((t0 + kQuantTiles) * kTileNF4 <= a.n) {  // uniform: whole bf16 tiles
         float w[kQuantTiles][8];
 #pragma unroll
         for (uint32_t t = 0; t < kQuantTiles; ++t) nf4_quantize_load<true>(a, (t0 + t) * kTileNF4 + lane_e, 0xFFu, w[t]);
